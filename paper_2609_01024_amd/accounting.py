@@ -1,0 +1,52 @@
+"""Algorithmic work of the path-compositional MoE layer: FLOPs and bytes.
+
+Only work the method must do is counted: the expansion of each (token, source)
+pair once (Section 4.3's source-grouped reuse), one projection per (token,
+target) pair after mixing the sources bound for that target (the projection is
+linear, Section 4.1), and the mix itself. Padding rows, dense n x n work and
+per-path projections that the rewrite avoids are never counted.
+"""
+from __future__ import annotations
+
+BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3    # MI355X fp32 vector
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+
+
+def expansion_flops_per_row(H: int, F: int) -> int:
+    """Gate and up projections of one expert for one token (2 flops per MAC)."""
+    return 2 * 2 * H * F
+
+
+def projection_flops_per_row(H: int, F: int) -> int:
+    """Down projection of one expert for one token."""
+    return 2 * H * F
+
+
+def expert_flops(H: int, F: int) -> int:
+    return expansion_flops_per_row(H, F) + projection_flops_per_row(H, F)
+
+
+def gemm_flops(R: int, H: int, F: int, T: int = 0, shared_F: int = 0) -> dict:
+    """Executed MFMA work of the grouped GEMMs for R = T*k rows (+ a shared expert)."""
+    exp = R * expansion_flops_per_row(H, F)
+    proj = R * projection_flops_per_row(H, F)
+    sh_exp = T * expansion_flops_per_row(H, shared_F) if shared_F else 0
+    sh_proj = T * projection_flops_per_row(H, shared_F) if shared_F else 0
+    return {"expand": exp, "project": proj, "shared_expand": sh_exp, "shared_project": sh_proj,
+            "total": exp + proj + sh_exp + sh_proj}
+
+
+def mix_flops(F: int, n_paths: int) -> int:
+    """z_(t,b) = sum_a beta_ab U_(t,a): one multiply-add per path and column."""
+    return 2 * F * n_paths
+
+
+def expanded_bytes(R: int, F: int, elem: int) -> int:
+    return R * F * elem
+
+
+def decode_weight_bytes(touched_experts: int, H: int, F: int, elem: int,
+                        shared_F: int = 0) -> int:
+    """Weight bytes a layer must stream when each touched expert is read once."""
+    return touched_experts * 3 * H * F * elem + (3 * H * shared_F * elem if shared_F else 0)

@@ -1,0 +1,305 @@
+"""Pins of the CPU oracle: checks against things other than the oracle itself.
+
+Each ``pin_*`` function takes a loaded oracle library handle ``L`` and raises
+AssertionError if the oracle disagrees with
+  * brute force (stable sort of all logits, enumeration of all n x n paths,
+    dense per-token evaluation of every U_i and every P_ij),
+  * closed forms (the vanilla top-k MoE when only diagonal paths are allowed;
+    the all-pairs closed form; k = 1; n = 1 as a dense SwiGLU FFN),
+  * invariants (weight sums, expert relabelling, exact bfloat16 widening,
+    reuse of expansion outputs not changing results).
+The same functions run against deliberately broken builds of the oracle in
+test_oracle_mutants.py, which shows that a plausible mistake fails a pin.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+
+RNG = np.random.default_rng(20260901)
+
+
+# ----------------------------------------------------------------- references
+def softmax_renorm_topk(l: np.ndarray, k: int):
+    """Top-k by stable sort of all logits (ties to lower id) and the full softmax
+    renormalised over the selected experts."""
+    order = np.argsort(-l.astype(np.float64), axis=1, kind="stable")[:, :k]
+    full = np.exp(l.astype(np.float64) - l.max(axis=1, keepdims=True))
+    full /= full.sum(axis=1, keepdims=True)
+    sel = np.take_along_axis(full, order, axis=1)
+    return order.astype(np.int32), sel / sel.sum(axis=1, keepdims=True)
+
+
+def textbook_swiglu(x, wg, wu, wd):
+    """F(x) = W_down (SiLU(W_gate x) * (W_up x)) for rows of x (float64)."""
+    g = x @ wg.T
+    u = x @ wu.T
+    return (g / (1.0 + np.exp(-g)) * u) @ wd.T
+
+
+def dense_bruteforce_layer(x, logits, wg, wu, wd, mask, k, beta_mode=oracle.BETA_SRC_COND):
+    """Every token: all n expansions U_i, all n^2 paths P_ij = W_down_j U_i, then the
+    allowed ones among the token's selected experts, weighted by their path weight."""
+    x = np.asarray(x, np.float64)
+    T = x.shape[0]
+    n = wg.shape[0]
+    G = np.einsum("th,nfh->tnf", x, wg)
+    Uall = G / (1.0 + np.exp(-G)) * np.einsum("th,nfh->tnf", x, wu)       # [T, n, F]
+    P = np.einsum("jhf,tif->tijh", wd, Uall)                               # [T, n, n, H]
+    ids, p = softmax_renorm_topk(logits, k)
+    y = np.zeros((T, wd.shape[1]))
+    for t in range(T):
+        E = list(ids[t])
+        prob = {e: p[t, a] for a, e in enumerate(E)}
+        allowed = [(i, j) for i in range(n) for j in range(n)
+                   if i in prob and j in prob and (i == j or mask[i, j])]
+        tot = sum(prob[i] * prob[j] for i, j in allowed)
+        for i, j in allowed:
+            w = prob[i] * prob[j]
+            if beta_mode == oracle.BETA_SRC_COND:
+                w /= sum(prob[jj] for ii, jj in allowed if ii == i)
+            elif beta_mode == oracle.BETA_GLOBAL:
+                w /= tot
+            y[t] += w * P[t, i, j]
+    return y
+
+
+def rand_layer(T, H, F, n, k, density, x_std=1.0, w_std=0.1, ties=False):
+    x = RNG.standard_normal((T, H)) * x_std
+    wg = RNG.standard_normal((n, F, H)) * w_std
+    wu = RNG.standard_normal((n, F, H)) * w_std
+    wd = RNG.standard_normal((n, H, F)) * w_std
+    l = RNG.standard_normal((T, n)).astype(np.float32)
+    if ties:
+        l = (np.round(l * 2) / 2).astype(np.float32)
+    mask = (RNG.random((n, n)) < density).astype(np.uint8)
+    np.fill_diagonal(mask, 1)
+    f32 = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    return f32(x), l, f32(wg), f32(wu), f32(wd), mask
+
+
+def _close(a, b, rel=1e-12, what=""):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    scale = max(np.abs(b).max(), 1e-300)
+    err = np.abs(a - b).max() / scale
+    assert err <= rel, f"{what}: max rel err {err:.3e} > {rel:.1e}"
+
+
+# ----------------------------------------------------------------------- pins
+def pin_topk_bruteforce(L):
+    for n in (1, 2, 3, 8, 16, 64, 256):
+        for k in sorted({1, min(n, 2), min(n, 4), min(n, 8)}):
+            for ties in (False, True):
+                l = RNG.standard_normal((97, n)).astype(np.float32)
+                if ties:
+                    l = (np.round(l * 2) / 2).astype(np.float32)
+                ids, w = oracle.route(l, k, L=L)
+                ref_ids, ref_w = softmax_renorm_topk(l, k)
+                assert np.array_equal(ids, ref_ids), f"top-k ids n={n} k={k} ties={ties}"
+                _close(w, ref_w, 1e-12, f"top-k weights n={n} k={k}")
+                _close(w.sum(axis=1), np.ones(97), 1e-14, "weights sum to 1")
+    # signed zeros are equal logits: the lower id wins
+    l = np.array([[-0.0, 0.0, 0.0, -0.0, -1.0]], np.float32)
+    ids, _ = oracle.route(l, 4, L=L)
+    assert list(ids[0]) == [0, 1, 2, 3], ids
+
+
+def pin_path_bits_bruteforce(L):
+    for n, k, d in ((8, 2, 0.5), (16, 4, 0.3), (64, 8, 0.25), (3, 3, 0.5), (256, 8, 0.2)):
+        l = RNG.standard_normal((50, n)).astype(np.float32)
+        mask = (RNG.random((n, n)) < d).astype(np.uint8)
+        mask[RNG.random(n) < 0.5, :] = 0  # some sources with no off-diagonal targets
+        ids, w = oracle.route(l, k, L=L)
+        m0 = mask.copy()
+        np.fill_diagonal(m0, 0)  # a zero diagonal must be ignored (m_ii = 1 forced)
+        bits, beta = oracle.paths(ids, w, m0, L=L)
+        for t in range(50):
+            slot = {int(e): a for a, e in enumerate(ids[t])}
+            ref = 0
+            for i in range(n):
+                for j in range(n):
+                    if i in slot and j in slot and (i == j or m0[i, j]):
+                        ref |= 1 << (slot[i] * k + slot[j])
+            assert int(bits[t]) == ref, f"path bits n={n} k={k} t={t}"
+            off = [(a, b) for a in range(k) for b in range(k) if not (ref >> (a * k + b)) & 1]
+            assert all(beta[t, a, b] == 0.0 for a, b in off), "beta must be 0 off-path"
+
+
+def pin_beta_closed_forms(L):
+    n, k = 16, 4
+    l = RNG.standard_normal((200, n)).astype(np.float32)
+    mask = (RNG.random((n, n)) < 0.4).astype(np.uint8)
+    ids, p = oracle.route(l, k, L=L)
+    bits, b_src = oracle.paths(ids, p, mask, oracle.BETA_SRC_COND, L=L)
+    _, b_prod = oracle.paths(ids, p, mask, oracle.BETA_PRODUCT, L=L)
+    _, b_glob = oracle.paths(ids, p, mask, oracle.BETA_GLOBAL, L=L)
+    on = np.array([[[(int(bits[t]) >> (a * k + b)) & 1 for b in range(k)] for a in range(k)]
+                   for t in range(200)], np.float64)
+    prod = p[:, :, None] * p[:, None, :] * on
+    _close(b_prod, prod, 1e-15, "PRODUCT = p_a p_b on paths")
+    _close(b_glob, prod / prod.sum(axis=(1, 2), keepdims=True), 1e-14, "GLOBAL")
+    _close(b_glob.sum(axis=(1, 2)), np.ones(200), 1e-14, "GLOBAL sums to 1")
+    _close(b_src.sum(axis=(1, 2)), np.ones(200), 1e-14, "SRC_COND sums to 1")
+    _close(b_src.sum(axis=2), p, 1e-14, "SRC_COND source row sums to p_a")
+    srcsum = (p[:, None, :] * on).sum(axis=2)                      # sum_{b in T_a} p_b
+    _close(b_src, prod / srcsum[:, :, None], 1e-14, "SRC_COND closed form")
+    # every pair allowed: the three readings coincide and equal the product
+    full = np.ones((n, n), np.uint8)
+    for mode in (0, 1, 2):
+        _, b = oracle.paths(ids, p, full, mode, L=L)
+        _close(b, p[:, :, None] * p[:, None, :], 1e-14, f"full mask mode {mode}")
+    # diagonal only: SRC_COND gives beta_aa = p_a, i.e. the vanilla weights alpha_e
+    eye = np.eye(n, dtype=np.uint8)
+    _, b = oracle.paths(ids, p, eye, oracle.BETA_SRC_COND, L=L)
+    _close(np.einsum("taa->ta", b), p, 1e-15, "diagonal-only beta_aa = p_a")
+
+
+def pin_permutation_bruteforce(L):
+    for T, n, k in ((0, 4, 2), (1, 1, 1), (37, 8, 2), (300, 64, 8), (129, 256, 8), (64, 5, 5)):
+        ids = np.array([RNG.permutation(n)[:k] for _ in range(T)], np.int32).reshape(T, k)
+        off, rt, rs, ro = oracle.permute(ids, n, L=L)
+        pairs = sorted((int(ids[t, a]), t, a) for t in range(T) for a in range(k))
+        assert list(rt) == [t for _, t, _ in pairs], "row_token"
+        assert list(rs) == [a for _, _, a in pairs], "row_slot"
+        counts = np.bincount(ids.ravel(), minlength=n) if T else np.zeros(n, int)
+        assert list(off) == [0] + list(np.cumsum(counts)), "expert_offsets"
+        for r, (_, t, a) in enumerate(pairs):
+            assert ro[t, a] == r, "row_of inverse"
+
+
+def pin_layer_bruteforce(L):
+    cases = [(6, 16, 8, 8, 2, 0.5), (5, 8, 16, 16, 4, 0.4), (4, 16, 8, 3, 3, 0.7),
+             (7, 64, 16, 12, 8, 0.3), (3, 8, 8, 2, 1, 1.0)]
+    for T, H, F, n, k, d in cases:
+        for ties in (False, True):
+            x, l, wg, wu, wd, mask = rand_layer(T, H, F, n, k, d, ties=ties)
+            for mode in (0, 1, 2):
+                y = oracle.layer(x, l, wg, wu, wd, mask, k, beta_mode=mode, L=L)
+                ref = dense_bruteforce_layer(x, l, wg, wu, wd, mask, k, mode)
+                _close(y, ref, 1e-12, f"layer vs brute force T={T} n={n} k={k} mode={mode}")
+
+
+def pin_diagonal_is_vanilla_moe(L):
+    """Only diagonal paths allowed: the layer is the standard top-k MoE (Section 4.1)."""
+    T, H, F, n, k = 9, 32, 16, 8, 3
+    x, l, wg, wu, wd, _ = rand_layer(T, H, F, n, k, 0.0)
+    mask = np.eye(n, dtype=np.uint8)
+    y = oracle.layer(x, l, wg, wu, wd, mask, k, L=L)
+    ids, p = softmax_renorm_topk(l, k)
+    ref = np.zeros((T, H))
+    for t in range(T):
+        for a in range(k):
+            e = ids[t, a]
+            ref[t] += p[t, a] * textbook_swiglu(x[t:t + 1].astype(np.float64), wg[e].astype(np.float64),
+                                                wu[e].astype(np.float64), wd[e].astype(np.float64))[0]
+    _close(y, ref, 1e-12, "diagonal-only = vanilla top-k MoE")
+
+
+def pin_full_mask_closed_form(L):
+    """Every pair allowed: y = sum_b p_b W_down_b (sum_a p_a U_a) by linearity of D."""
+    T, H, F, n, k = 8, 16, 24, 6, 4
+    x, l, wg, wu, wd, _ = rand_layer(T, H, F, n, k, 1.0)
+    y = oracle.layer(x, l, wg, wu, wd, np.ones((n, n), np.uint8), k, L=L)
+    ids, p = softmax_renorm_topk(l, k)
+    ref = np.zeros((T, H))
+    for t in range(T):
+        xt = x[t].astype(np.float64)
+        U = [(lambda g, u: g / (1 + np.exp(-g)) * u)(wg[e].astype(np.float64) @ xt,
+                                                     wu[e].astype(np.float64) @ xt) for e in ids[t]]
+        mix = sum(p[t, a] * U[a] for a in range(k))
+        ref[t] = sum(p[t, b] * (wd[ids[t, b]].astype(np.float64) @ mix) for b in range(k))
+    _close(y, ref, 1e-12, "full mask closed form")
+
+
+def pin_k1_and_n1(L):
+    T, H, F = 7, 16, 32
+    x, l, wg, wu, wd, mask = rand_layer(T, H, F, 5, 1, 0.8)
+    y = oracle.layer(x, l, wg, wu, wd, mask, 1, L=L)
+    top = np.argmax(l, axis=1)
+    f64 = lambda a: a.astype(np.float64)
+    ref = np.stack([textbook_swiglu(f64(x[t:t + 1]), f64(wg[e]), f64(wu[e]), f64(wd[e]))[0]
+                    for t, e in enumerate(top)])
+    _close(y, ref, 1e-12, "k = 1 is the single selected expert")
+    x, l, wg, wu, wd, mask = rand_layer(T, H, F, 1, 1, 0.0)
+    y = oracle.layer(x, l, wg, wu, wd, mask, 1, L=L)
+    _close(y, textbook_swiglu(f64(x), f64(wg[0]), f64(wu[0]), f64(wd[0])), 1e-12, "n = 1 dense FFN")
+    ys = oracle.dense_swiglu(x, wg[0], wu[0], wd[0], L=L)
+    _close(ys, textbook_swiglu(f64(x), f64(wg[0]), f64(wu[0]), f64(wd[0])), 1e-12, "shared expert")
+
+
+def pin_reuse_and_target_mix(L):
+    """Reusing U_i per source (Section 4.3) changes nothing; mixing per target before the
+    linear D_j agrees to rounding."""
+    T, H, F, n, k = 6, 16, 16, 8, 4
+    x, l, wg, wu, wd, mask = rand_layer(T, H, F, n, k, 0.5)
+    y_lit = oracle.layer(x, l, wg, wu, wd, mask, k, reuse=False, L=L)
+    y_re = oracle.layer(x, l, wg, wu, wd, mask, k, reuse=True, L=L)
+    assert np.array_equal(y_lit, y_re), "reuse must be bit-identical to per-path evaluation"
+    ids, p = oracle.route(l, k, L=L)
+    bits, beta = oracle.paths(ids, p, mask, L=L)
+    U = oracle.expansion_rows(x, wg, wu, np.repeat(np.arange(T), k), ids.ravel(), L=L).reshape(T, k, F)
+    Z = np.einsum("tab,taf->tbf", beta, U)
+    y_mix = np.stack([sum(wd[ids[t, b]].astype(np.float64) @ Z[t, b] for b in range(k)) for t in range(T)])
+    _close(y_re, y_mix, 1e-12, "target-mixed rewrite")
+
+
+def pin_expansion_rows(L):
+    T, H, F, n = 5, 32, 8, 4
+    x, _, wg, wu, _, _ = rand_layer(T, H, F, n, 1, 0.0)
+    tok = np.array([0, 4, 2, 2]); ex = np.array([3, 0, 1, 3], np.int32)
+    U = oracle.expansion_rows(x, wg, wu, tok, ex, L=L)
+    for i, (t, e) in enumerate(zip(tok, ex)):
+        g = wg[e].astype(np.float64) @ x[t].astype(np.float64)
+        u = wu[e].astype(np.float64) @ x[t].astype(np.float64)
+        _close(U[i], g / (1 + np.exp(-g)) * u, 1e-13, "expansion row")
+
+
+def pin_relabel_invariance(L):
+    T, H, F, n, k = 6, 16, 8, 10, 3
+    x, l, wg, wu, wd, mask = rand_layer(T, H, F, n, k, 0.5)
+    y = oracle.layer(x, l, wg, wu, wd, mask, k, L=L)
+    perm = RNG.permutation(n)            # old expert e becomes perm[e]
+    inv = np.argsort(perm)
+    y2 = oracle.layer(x, np.ascontiguousarray(l[:, inv]), np.ascontiguousarray(wg[inv]),
+                      np.ascontiguousarray(wu[inv]), np.ascontiguousarray(wd[inv]),
+                      np.ascontiguousarray(mask[np.ix_(inv, inv)]), k, L=L)
+    _close(y2, y, 1e-14, "expert relabelling")
+    ids, _ = oracle.route(l, k, L=L)
+    ids2, _ = oracle.route(np.ascontiguousarray(l[:, inv]), k, L=L)
+    assert np.array_equal(ids2, perm[ids]), "ids follow the relabelling"
+
+
+def pin_bf16_widening(L):
+    """bfloat16 inputs are widened exactly: same result as their float32 values."""
+    import torch
+    T, H, F, n, k = 4, 64, 64, 8, 2
+    x, l, wg, wu, wd, mask = rand_layer(T, H, F, n, k, 0.5)
+    tb = [torch.from_numpy(a).to(torch.bfloat16) for a in (x, wg, wu, wd)]
+    y_b = oracle.layer(*tb[:1], l, *tb[1:], mask, k, L=L)
+    y_f = oracle.layer(*[t.float() for t in tb[:1]], l, *[t.float() for t in tb[1:]], mask, k, L=L)
+    assert np.array_equal(y_b, y_f), "bf16 widening must be exact"
+
+
+def pin_edge_cases(L):
+    # T = 0: nothing to do, success
+    ids, w = oracle.route(np.zeros((0, 4), np.float32), 2, L=L)
+    assert ids.shape == (0, 2)
+    # k = n: every expert selected, every allowed pair is a path
+    T, H, F, n = 3, 8, 8, 4
+    x, l, wg, wu, wd, mask = rand_layer(T, H, F, n, n, 0.5)
+    _close(oracle.layer(x, l, wg, wu, wd, mask, n, L=L),
+           dense_bruteforce_layer(x, l, wg, wu, wd, mask, n), 1e-12, "k = n")
+    # invalid arguments are rejected
+    L2 = L
+    st = L2.pcmo_route(0, 1, 4, 5, 0, 0)
+    assert st != 0, "k > n must be rejected"
+    st = L2.pcmo_route(0, 1, 16, 9, 0, 0)
+    assert st != 0, "k > 8 must be rejected"
+
+
+ALL_PINS = [pin_topk_bruteforce, pin_path_bits_bruteforce, pin_beta_closed_forms,
+            pin_permutation_bruteforce, pin_layer_bruteforce, pin_diagonal_is_vanilla_moe,
+            pin_full_mask_closed_form, pin_k1_and_n1, pin_reuse_and_target_mix,
+            pin_expansion_rows, pin_relabel_invariance, pin_bf16_widening, pin_edge_cases]
