@@ -1,0 +1,177 @@
+"""Benchmark of the path-compositional MoE layer on one MI355X.
+
+A step is one forward pass of the whole layer (route, build paths, expand, project
+and combine, plus the shared expert when the workload has one) over one batch of
+synthetic, seeded inputs already resident in HBM. Prints ONE JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+
+The dominant kernel's roofline figure uses its average launch duration, measured
+with HIP events recorded on the stream the kernel runs on, over the timed steps.
+The CPU baseline times the float64 oracle on a bounded sample of the same tokens.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "path-MoE layer tokens/sec and grouped-GEMM TFLOP/s (% bf16 MFMA peak), 1 GPU"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle sample")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file with measured HBM bytes per launch of the dominant kernel")
+    return ap.parse_args()
+
+
+def cpu_baseline(inp, target_s: float) -> dict:
+    import oracle
+    cfg = inp.cfg
+    nt = oracle.num_threads()
+    rng = np.random.default_rng(123)
+    ntok = max(1, nt)
+    spent = 0.0
+    while True:
+        toks = np.sort(rng.choice(cfg.T, min(ntok, cfg.T), replace=False))
+        t0 = time.perf_counter()
+        oracle.layer_inputs(inp, tokens=toks)
+        spent = time.perf_counter() - t0
+        if spent >= target_s / 4 or ntok >= cfg.T:
+            break
+        ntok = min(cfg.T, int(ntok * max(2.0, target_s / max(spent, 1e-3) * 0.9)))
+    return {"value": round(toks.size / spent, 3), "unit": "tokens/s", "cores": nt, "kind": "oracle",
+            "sample": f"{toks.size} of {cfg.T} tokens of the same workload (route, paths, per-path "
+                      f"float64 evaluation), {spent:.1f} s wall on {nt} threads"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the layer is sharded by design, not measured, across GPUs)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_01024_amd as pcm
+    from paper_2609_01024_amd import accounting as acc
+    from workloads import CONFIGS, HEADLINE, make_inputs
+
+    name = args.config or HEADLINE
+    cfg = CONFIGS[name]
+    t0 = time.time()
+    inp = make_inputs(cfg, seed=args.seed)
+    print(f"[bench] {name}: inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    dev = "cuda:0"
+    x = inp.x.to(dev)
+    logits = torch.from_numpy(inp.logits).to(dev)
+    mask = torch.from_numpy(inp.mask).to(dev)
+    wg, wu, wd = inp.w_gate.to(dev), inp.w_up.to(dev), inp.w_down.to(dev)
+    shared = (inp.s_gate.to(dev), inp.s_up.to(dev), inp.s_down.to(dev)) if cfg.shared_F else None
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
+    stream = torch.cuda.current_stream()
+
+    stages = ["route", "build_paths", "expand", "project_combine"] + (["shared"] if shared else [])
+
+    def step(events=None):
+        def mark(i):
+            if events is not None:
+                events[i].record(stream)
+        mark(0)
+        pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
+        mark(1)
+        pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
+        mark(2)
+        pcm.pcm_expand(x, wg, wu, plan.paths, u=plan.u)
+        mark(3)
+        pcm.pcm_project_combine(plan.u, wd, plan.paths, y=plan.y, ws=plan.ws_proj)
+        mark(4)
+        if shared:
+            pcm.pcm_dense_swiglu(x, *shared, y=plan.y, accumulate=True, ws=plan.ws_shared)
+            mark(5)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    stage_ms = {st: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+                for i, st in enumerate(stages)}
+    ms = wall * 1e3 / args.steps
+
+    offsets = plan.paths.expert_offsets.cpu().numpy()
+    touched = int(np.count_nonzero(np.diff(offsets)))
+    R = cfg.R
+    fl = acc.gemm_flops(R, cfg.H, cfg.F, cfg.T, cfg.shared_F)
+    gemm_ms = stage_ms["expand"] + stage_ms["project_combine"] + stage_ms.get("shared", 0.0)
+    gemm_tflops = fl["total"] / (gemm_ms * 1e-3) / 1e12
+    bf16 = cfg.dtype == "bf16"
+    peak = acc.BF16_PEAK_TFLOPS if bf16 else acc.FP32_PEAK_TFLOPS
+
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        traffic = json.load(open(args.traffic)).get(name)
+
+    if name == "decode":
+        # weight streaming: every touched expert's three matrices are read once per step
+        wbytes = acc.decode_weight_bytes(touched, cfg.H, cfg.F, 2, cfg.shared_F)
+        exp_bytes = touched * 2 * cfg.H * cfg.F * 2
+        achieved = exp_bytes / (stage_ms["expand"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": acc.HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / acc.HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "expand (grouped gate/up GEMM + SwiGLU)",
+                "per_launch": f"{touched} touched experts x 2*H*F*2 B of gate/up weights"}
+        extra = {"layer_weight_GBps": round(wbytes / (ms * 1e-3) / 1e9, 1)}
+    else:
+        achieved = fl["expand"] / (stage_ms["expand"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": traffic,
+                "kernel": "expand (grouped gate/up GEMM + SwiGLU)",
+                "per_launch": f"4*H*F flop x R={R} rows"}
+        extra = {}
+
+    line = {
+        "metric": METRIC, "value": round(cfg.T / (ms * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
+        "config": {"workload": f"{name}: T={cfg.T} H={cfg.H} n={cfg.n} F={cfg.F} k={cfg.k} "
+                               f"mask density {cfg.density}"
+                               + (f" shared F={cfg.shared_F}" if cfg.shared_F else ""),
+                   "tokens": cfg.T, "rows": R, "touched_experts": touched},
+        "gemm_tflops": round(gemm_tflops, 1), "gemm_frac_peak": round(gemm_tflops / peak, 4),
+        "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "roofline": roof, **extra,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,146 @@
+/*
+ * pcomoe.h -- C ABI of the path-compositional MoE layer (PCoMoE, arXiv 2609.01024)
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * One layer, per token h with router logits l (Section 2, vanilla MoE; Section 4):
+ *   1. route          top-k experts e_0..e_{k-1} of l (logit descending, ties to the lower
+ *                     id) and weights p_a = softmax over the k selected logits.
+ *   2. build paths    Pi(h) = {(a, b) : m[e_a][e_b] = 1 or a == b} over the token's slots,
+ *                     with the diagonal of the compatibility mask forced to 1 (Section 4.2,
+ *                     m_ii = 1; Section 4.3, fallback to vanilla); path weights beta_ab;
+ *                     the grouped dispatch layout (rows sorted by expert, then token).
+ *   3. expand         U_(t,a) = SiLU(W_gate[e_a] x_t) * (W_up[e_a] x_t), once per
+ *                     (token, source) pair (Section 4.1 U_e; Section 4.3 source-grouped reuse).
+ *   4. project and    y_t = sum_{(a,b) in Pi} beta_ab W_down[e_b] U_(t,a)  (Section 4.1 path
+ *      combine        aggregation, Section 4.3 source-grouped form), computed as
+ *                     y_t = sum_b W_down[e_b] z_(t,b) with z_(t,b) = sum_a beta_ab U_(t,a),
+ *                     which is the same sum because W_down is linear (Section 4.1 D_e).
+ *
+ * Conventions for every call:
+ *   - Pointers named as device pointers must be device memory of the current HIP device,
+ *     16-byte aligned; arrays are dense and row-major. The caller owns every buffer; the
+ *     library never allocates or frees memory and holds no mutable global state.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued and the call
+ *     returns without synchronising. Device-side faults surface at the caller's next sync.
+ *   - Arguments are validated on the host before anything is enqueued. On error nothing
+ *     is enqueued and outputs are untouched. T = 0 is a successful no-op.
+ *   - Limits: 1 <= k <= min(n, 8); n <= 256; H and F multiples of 64; T*k < 2^31.
+ *   - Logits must be finite. Index arrays passed back in (topk_ids, the pcm_paths layout)
+ *     must be what the library produced; other values give undefined results, but every
+ *     gathered index is clamped, so memory outside the buffers is never touched.
+ */
+#ifndef PCOMOE_H
+#define PCOMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pcm_status {
+    PCM_OK = 0,
+    PCM_ERR_ARG = 1,          /* null pointer, misaligned pointer, negative size, k > n ... */
+    PCM_ERR_UNSUPPORTED = 2,  /* outside the limits above */
+    PCM_ERR_WORKSPACE = 3,    /* ws_bytes smaller than pcm_workspace_bytes(...) */
+    PCM_ERR_HIP = 4           /* a launch failed (hipGetLastError) */
+} pcm_status;
+
+typedef enum pcm_dtype {
+    PCM_F32 = 0,   /* x, weights, U and intermediates in float32; FMA on the vector ALUs */
+    PCM_BF16 = 1   /* x, weights, U and intermediates in bfloat16; MFMA, float32 accumulate */
+} pcm_dtype;
+
+/* Path weights beta_ab for (a, b) in Pi (p = the renormalised router weights).
+ * The paper names beta without a formula; the default is the reading under which a
+ * diagonal-only mask reproduces the vanilla layer exactly (beta_aa = p_a, as Section 4.1
+ * requires) and an all-pairs mask gives the product p_a p_b:
+ *   SRC_COND: beta_ab = p_a p_b / sum_{b' : (a,b') in Pi} p_b'   (sum over Pi is 1)
+ *   PRODUCT:  beta_ab = p_a p_b
+ *   GLOBAL:   beta_ab = p_a p_b / sum_{(a',b') in Pi} p_a' p_b'                       */
+typedef enum pcm_beta_mode {
+    PCM_BETA_SRC_COND = 0,
+    PCM_BETA_PRODUCT = 1,
+    PCM_BETA_GLOBAL = 2
+} pcm_beta_mode;
+
+typedef enum pcm_op {
+    PCM_OP_BUILD_PATHS = 0,
+    PCM_OP_EXPAND = 1,
+    PCM_OP_PROJECT_COMBINE = 2,
+    PCM_OP_DENSE_SWIGLU = 3
+} pcm_op;
+
+/* Path table and grouped dispatch layout of T tokens (caller-owned device buffers).
+ * A "row" is one (token, slot) pair; rows are ordered by (expert ascending, token
+ * ascending), so the rows of expert e are [expert_offsets[e], expert_offsets[e+1]). */
+typedef struct pcm_paths {
+    uint64_t* path_bits;       /* [T]      bit a*k+b set iff (a, b) in Pi(token)            */
+    float* beta;               /* [T,k,k]  beta[t][a][b]; exactly 0 where the bit is clear   */
+    int32_t* expert_offsets;   /* [n+1]    first row of each expert; [n] = T*k              */
+    int32_t* row_token;        /* [T*k]    token of each row                                 */
+    int32_t* row_slot;         /* [T*k]    slot a of each row                                */
+    int32_t* row_of;           /* [T*k]    row of pair (t, a) at index t*k + a               */
+} pcm_paths;
+
+/* Route (Section 2's top-k selection; Section 4.3's fused indexing starts here).
+ * logits [T,n] f32 (device). Outputs (device): topk_ids [T,k] i32, experts of slots
+ * 0..k-1 by logit descending with ties to the lower id (signed zeros are equal);
+ * topk_w [T,k] f32, softmax over the k selected logits. */
+pcm_status pcm_route(const float* logits, int64_t T, int n, int k, int32_t* topk_ids,
+                     float* topk_w, void* stream);
+
+/* Build the path table and dispatch layout (Section 4.2's mask with m_ii = 1, applied
+ * before any weighting; Section 4.3's source-grouped dispatch metadata).
+ * topk_ids/topk_w [T,k] from pcm_route; mask [n,n] u8 (device), row = expansion source
+ * expert i, column = projection target expert j, nonzero = allowed; its diagonal is
+ * ignored (treated as 1). Fills every array of *out (the struct itself is host memory).
+ * Deterministic: integer outputs are bit-identical from run to run.
+ * ws: device workspace of pcm_workspace_bytes(PCM_OP_BUILD_PATHS, T, 0, 0, n, k, 0). */
+pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const uint8_t* mask,
+                           int64_t T, int n, int k, pcm_beta_mode beta_mode,
+                           const pcm_paths* out, void* ws, size_t ws_bytes, void* stream);
+
+/* Expansion side, once per (token, source) row (Section 4.1 U_e; Section 4.3 reuse):
+ * u[r,:] = SiLU(x[row_token[r]] W_gate[e]^T) * (x[row_token[r]] W_up[e]^T) for the rows r
+ * of expert e. x [T,H], w_gate/w_up [n,F,H], u [T*k,F], all of `dtype` (device).
+ * bf16: products accumulate in float32, SiLU and the product in float32, u rounded to
+ * nearest even. ws: pcm_workspace_bytes(PCM_OP_EXPAND, ...) bytes (currently 0; may be NULL). */
+pcm_status pcm_expand(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                      const pcm_paths* paths, int64_t T, int H, int F, int n, int k, void* u,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* Projection side and combine (Section 4.1 D_e and path aggregation; Section 4.3):
+ * z_(t,b) = sum_{a : (a,b) in Pi} beta_ab u_(t,a)   (float32 math, stored in `dtype`),
+ * o_(t,b) = W_down[e_b] z_(t,b)                     (float32 accumulate),
+ * y_t = [y_t if accumulate] + sum_{b ascending} o_(t,b).
+ * u [T*k,F] from pcm_expand, w_down [n,H,F] of `dtype`, y [T,H] f32 (device).
+ * ws: pcm_workspace_bytes(PCM_OP_PROJECT_COMBINE, ...) bytes (holds z and o). */
+pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_down,
+                               const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
+                               float* y, int accumulate, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/* A dense SwiGLU FFN applied to every token with weight 1 (Section 2's expert F_e), for an
+ * always-on shared expert that sits beside the routed experts and outside the path
+ * space: y_t = [y_t if accumulate] + W_down (SiLU(W_gate x_t) * (W_up x_t)).
+ * x [T,H], w_gate/w_up [Fs,H], w_down [H,Fs] of `dtype`; y [T,H] f32 (device).
+ * ws: pcm_workspace_bytes(PCM_OP_DENSE_SWIGLU, T, H, Fs, 1, 1, dtype) bytes. */
+pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate,
+                            const void* w_up, const void* w_down, int64_t T, int H, int Fs,
+                            float* y, int accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/* Device workspace bytes an operation needs (0 if none). Returns 0 for invalid sizes. */
+size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm_dtype dtype);
+
+/* Static description of a status code (never NULL). */
+const char* pcm_status_string(pcm_status status);
+
+/* ABI version of this header (major * 100 + minor). */
+int pcm_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PCOMOE_H */

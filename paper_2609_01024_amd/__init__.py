@@ -1,0 +1,13 @@
+"""MI355X-native path-compositional MoE layer (PCoMoE, arXiv 2609.01024).
+
+The layer runs in libpcomoe.so (hand-written HIP for gfx950) behind the C ABI in
+include/pcomoe.h; this package is its thin Python binding. The library is loaded
+on first use and there is no fallback path: if it is missing, calls raise.
+"""
+from .binding import (BETA_GLOBAL, BETA_PRODUCT, BETA_SRC_COND, PCM_BF16, PCM_F32, LayerPlan,
+                      PathTable, layer_forward, lib, pcm_build_paths, pcm_dense_swiglu,
+                      pcm_expand, pcm_project_combine, pcm_route, workspace_bytes)
+
+__all__ = ["BETA_GLOBAL", "BETA_PRODUCT", "BETA_SRC_COND", "PCM_BF16", "PCM_F32", "LayerPlan",
+           "PathTable", "layer_forward", "lib", "pcm_build_paths", "pcm_dense_swiglu", "pcm_expand",
+           "pcm_project_combine", "pcm_route", "workspace_bytes"]

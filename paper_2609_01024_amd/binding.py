@@ -1,0 +1,231 @@
+"""ctypes binding of libpcomoe (include/pcomoe.h) for torch tensors on a ROCm device.
+
+The functions carry the C entry points' names and only marshal arguments: they
+check shapes and dtypes, allocate outputs with torch when the caller passes none,
+and pass raw device pointers plus the current HIP stream. Every step of the layer
+runs in the library's HIP kernels; there is no fallback path. If the library is
+not built, the first call raises RuntimeError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpcomoe.so")
+
+PCM_F32, PCM_BF16 = 0, 1
+BETA_SRC_COND, BETA_PRODUCT, BETA_GLOBAL = 0, 1, 2
+OP_BUILD_PATHS, OP_EXPAND, OP_PROJECT_COMBINE, OP_DENSE_SWIGLU = 0, 1, 2, 3
+
+EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
+           "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version")
+
+
+class PcmPaths(ctypes.Structure):
+    _fields_ = [("path_bits", ctypes.c_void_p), ("beta", ctypes.c_void_p),
+                ("expert_offsets", ctypes.c_void_p), ("row_token", ctypes.c_void_p),
+                ("row_slot", ctypes.c_void_p), ("row_of", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
+    """Load libpcomoe.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -c 'import __graft_entry__ as g; "
+                           "g.build()'` (the layer has no fallback path)")
+    L = ctypes.CDLL(path)
+    P, I, I64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+    L.pcm_route.argtypes = [P, I64, I, I, P, P, P]
+    L.pcm_build_paths.argtypes = [P, P, P, I64, I, I, I, ctypes.POINTER(PcmPaths), P, SZ, P]
+    L.pcm_expand.argtypes = [I, P, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, P, P, SZ, P]
+    L.pcm_project_combine.argtypes = [I, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, P, I, P,
+                                      SZ, P]
+    L.pcm_dense_swiglu.argtypes = [I, P, P, P, P, I64, I, I, P, I, P, SZ, P]
+    L.pcm_workspace_bytes.argtypes = [I, I64, I, I, I, I, I]
+    L.pcm_workspace_bytes.restype = SZ
+    L.pcm_status_string.argtypes = [I]
+    L.pcm_status_string.restype = ctypes.c_char_p
+    for name in ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
+                 "pcm_dense_swiglu", "pcm_abi_version"):
+        getattr(L, name).restype = I
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise RuntimeError(lib().pcm_status_string(status).decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream: Optional[torch.cuda.Stream]):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return PCM_BF16
+    if t.dtype == torch.float32:
+        return PCM_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError("tensors must be contiguous device tensors")
+
+
+def workspace_bytes(op: int, T: int, H: int, F: int, n: int, k: int, dtype: int) -> int:
+    return int(lib().pcm_workspace_bytes(op, T, H, F, n, k, dtype))
+
+
+def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
+    return torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=device) if nbytes else None
+
+
+# ------------------------------------------------------------------------ calls
+def pcm_route(logits: torch.Tensor, k: int, topk_ids=None, topk_w=None, stream=None):
+    _dev(logits)
+    T, n = logits.shape
+    ids = topk_ids if topk_ids is not None else torch.empty((T, k), dtype=torch.int32, device=logits.device)
+    w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=logits.device)
+    _dev(ids, w)
+    _check(lib().pcm_route(_ptr(logits), T, n, k, _ptr(ids), _ptr(w), _stream(stream)))
+    return ids, w
+
+
+@dataclass
+class PathTable:
+    """Device buffers of one pcm_paths layout for T tokens, n experts, top-k."""
+    T: int
+    n: int
+    k: int
+    path_bits: torch.Tensor
+    beta: torch.Tensor
+    expert_offsets: torch.Tensor
+    row_token: torch.Tensor
+    row_slot: torch.Tensor
+    row_of: torch.Tensor
+
+    @classmethod
+    def empty(cls, T: int, n: int, k: int, device) -> "PathTable":
+        i32 = dict(dtype=torch.int32, device=device)
+        return cls(T, n, k, torch.empty((T,), dtype=torch.int64, device=device),
+                   torch.empty((T, k, k), dtype=torch.float32, device=device),
+                   torch.empty((n + 1,), **i32), torch.empty((T * k,), **i32),
+                   torch.empty((T * k,), **i32), torch.empty((T, k), **i32))
+
+    def struct(self) -> PcmPaths:
+        return PcmPaths(self.path_bits.data_ptr(), self.beta.data_ptr(), self.expert_offsets.data_ptr(),
+                        self.row_token.data_ptr(), self.row_slot.data_ptr(), self.row_of.data_ptr())
+
+
+def pcm_build_paths(topk_ids, topk_w, mask, beta_mode: int = BETA_SRC_COND, out: PathTable = None,
+                    ws: torch.Tensor = None, stream=None) -> PathTable:
+    _dev(topk_ids, topk_w, mask)
+    T, k = topk_ids.shape
+    n = mask.shape[0]
+    out = out or PathTable.empty(T, n, k, topk_ids.device)
+    need = workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0)
+    if ws is None:
+        ws = _workspace(need, topk_ids.device)
+    st = out.struct()
+    _check(lib().pcm_build_paths(_ptr(topk_ids), _ptr(topk_w), _ptr(mask), T, n, k, beta_mode,
+                                 ctypes.byref(st), _ptr(ws), ws.numel() if ws is not None else 0,
+                                 _stream(stream)))
+    return out
+
+
+def pcm_expand(x, w_gate, w_up, paths: PathTable, u=None, stream=None) -> torch.Tensor:
+    _dev(x, w_gate, w_up, u)
+    T, H = x.shape
+    n, F, _ = w_gate.shape
+    u = u if u is not None else torch.empty((T * paths.k, F), dtype=x.dtype, device=x.device)
+    st = paths.struct()
+    _check(lib().pcm_expand(_dtype_code(x), _ptr(x), _ptr(w_gate), _ptr(w_up), ctypes.byref(st), T, H,
+                            F, n, paths.k, _ptr(u), None, 0, _stream(stream)))
+    return u
+
+
+def pcm_project_combine(u, w_down, paths: PathTable, y=None, accumulate: bool = False,
+                        ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+    _dev(u, w_down, y)
+    n, H, F = w_down.shape
+    T, k = paths.T, paths.k
+    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
+    dt = _dtype_code(u)
+    if ws is None:
+        ws = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), u.device)
+    st = paths.struct()
+    _check(lib().pcm_project_combine(dt, _ptr(u), _ptr(w_down), ctypes.byref(st), T, H, F, n, k,
+                                     _ptr(y), int(bool(accumulate)), _ptr(ws),
+                                     ws.numel() if ws is not None else 0, _stream(stream)))
+    return y
+
+
+def pcm_dense_swiglu(x, w_gate, w_up, w_down, y=None, accumulate: bool = False,
+                     ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+    _dev(x, w_gate, w_up, w_down, y)
+    T, H = x.shape
+    Fs = w_gate.shape[0]
+    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
+    dt = _dtype_code(x)
+    if ws is None:
+        ws = _workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, Fs, 1, 1, dt), x.device)
+    _check(lib().pcm_dense_swiglu(dt, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down), T, H, Fs,
+                                  _ptr(y), int(bool(accumulate)), _ptr(ws),
+                                  ws.numel() if ws is not None else 0, _stream(stream)))
+    return y
+
+
+class LayerPlan:
+    """Preallocated buffers for repeated forward passes of one layer shape, so that a
+    forward pass enqueues kernels only (no allocation)."""
+
+    def __init__(self, T, H, F, n, k, dtype: torch.dtype, device, shared_F: int = 0,
+                 beta_mode: int = BETA_SRC_COND):
+        self.T, self.H, self.F, self.n, self.k, self.shared_F = T, H, F, n, k, shared_F
+        self.beta_mode = beta_mode
+        dt = PCM_BF16 if dtype == torch.bfloat16 else PCM_F32
+        self.ids = torch.empty((T, k), dtype=torch.int32, device=device)
+        self.w = torch.empty((T, k), dtype=torch.float32, device=device)
+        self.paths = PathTable.empty(T, n, k, device)
+        self.ws_paths = _workspace(workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0), device)
+        self.u = torch.empty((T * k, F), dtype=dtype, device=device)
+        self.ws_proj = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), device)
+        self.ws_shared = (_workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, shared_F, 1, 1, dt), device)
+                          if shared_F else None)
+        self.y = torch.empty((T, H), dtype=torch.float32, device=device)
+
+    def forward(self, x, logits, mask, w_gate, w_up, w_down, shared=None, stream=None):
+        pcm_route(logits, self.k, self.ids, self.w, stream=stream)
+        pcm_build_paths(self.ids, self.w, mask, self.beta_mode, out=self.paths, ws=self.ws_paths,
+                        stream=stream)
+        pcm_expand(x, w_gate, w_up, self.paths, u=self.u, stream=stream)
+        pcm_project_combine(self.u, w_down, self.paths, y=self.y, ws=self.ws_proj, stream=stream)
+        if shared is not None:
+            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=True, ws=self.ws_shared, stream=stream)
+        return self.y
+
+
+def layer_forward(x, logits, mask, w_gate, w_up, w_down, k: int, beta_mode: int = BETA_SRC_COND,
+                  shared=None, stream=None) -> torch.Tensor:
+    """One layer: route, build paths, expand, project and combine (+ shared expert)."""
+    T, H = x.shape
+    n, F, _ = w_gate.shape
+    plan = LayerPlan(T, H, F, n, k, x.dtype, x.device, shared[0].shape[0] if shared else 0, beta_mode)
+    return plan.forward(x, logits, mask, w_gate, w_up, w_down, shared, stream)

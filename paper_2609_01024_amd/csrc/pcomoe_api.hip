@@ -1,0 +1,212 @@
+// C ABI of libpcomoe: host-side validation, workspace layout and launch sequencing.
+// Every check runs before anything is enqueued; the library never allocates, frees or
+// synchronises.
+#include "pcomoe.h"
+
+#include "internal.h"
+
+using namespace pcm;
+
+namespace {
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+pcm_status check_shape(int64_t T, int n, int k) {
+    if (T < 0 || n < 1 || k < 1 || k > n) return PCM_ERR_ARG;
+    if (k > kMaxK || n > kMaxN) return PCM_ERR_UNSUPPORTED;
+    if (T * (int64_t)k >= ((int64_t)1 << 31)) return PCM_ERR_UNSUPPORTED;
+    return PCM_OK;
+}
+
+pcm_status check_dims(int H, int F) {
+    if (H < 1 || F < 1) return PCM_ERR_ARG;
+    if (H % 64 || F % 64) return PCM_ERR_UNSUPPORTED;
+    return PCM_OK;
+}
+
+pcm_status check_paths(const pcm_paths* p) {
+    if (!p || !p->path_bits || !p->beta || !p->expert_offsets || !p->row_token || !p->row_slot ||
+        !p->row_of)
+        return PCM_ERR_ARG;
+    return PCM_OK;
+}
+
+pcm_status from_hip(hipError_t e) { return e == hipSuccess ? PCM_OK : PCM_ERR_HIP; }
+
+size_t elem_bytes(pcm_dtype d) { return d == PCM_BF16 ? 2 : 4; }
+
+// project_combine workspace: z [R,F] of dtype, then o [R,H] f32, each 256-byte aligned.
+size_t project_ws(int64_t T, int H, int F, int k, pcm_dtype dt, size_t* o_offset) {
+    const size_t R = (size_t)T * k;
+    const size_t z = align_up(R * F * elem_bytes(dt), 256);
+    if (o_offset) *o_offset = z;
+    return z + align_up(R * H * sizeof(float), 256);
+}
+
+}  // namespace
+
+extern "C" {
+
+int pcm_abi_version(void) { return 100; }
+
+const char* pcm_status_string(pcm_status s) {
+    switch (s) {
+        case PCM_OK: return "PCM_OK: success";
+        case PCM_ERR_ARG: return "PCM_ERR_ARG: invalid argument (null or misaligned pointer, bad size, k > n)";
+        case PCM_ERR_UNSUPPORTED: return "PCM_ERR_UNSUPPORTED: outside the supported limits (k <= 8, n <= 256, H and F multiples of 64, T*k < 2^31)";
+        case PCM_ERR_WORKSPACE: return "PCM_ERR_WORKSPACE: workspace smaller than pcm_workspace_bytes()";
+        case PCM_ERR_HIP: return "PCM_ERR_HIP: a HIP launch failed";
+    }
+    return "unknown pcm_status";
+}
+
+size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm_dtype dtype) {
+    if (T < 0 || n < 1 || k < 1) return 0;
+    switch (op) {
+        case PCM_OP_BUILD_PATHS: return build_paths_ws_bytes(T, n);
+        case PCM_OP_EXPAND: return 0;
+        case PCM_OP_PROJECT_COMBINE:
+            if (H < 1 || F < 1) return 0;
+            return project_ws(T, H, F, k, dtype, nullptr);
+        case PCM_OP_DENSE_SWIGLU:
+            if (H < 1 || F < 1) return 0;
+            return align_up((size_t)T * F * elem_bytes(dtype), 256);
+    }
+    return 0;
+}
+
+pcm_status pcm_route(const float* logits, int64_t T, int n, int k, int32_t* topk_ids,
+                     float* topk_w, void* stream) {
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if (T == 0) return PCM_OK;
+    if (!logits || !topk_ids || !topk_w) return PCM_ERR_ARG;
+    if (!aligned16(logits) || !aligned16(topk_ids) || !aligned16(topk_w)) return PCM_ERR_ARG;
+    return from_hip(launch_route(logits, T, n, k, topk_ids, topk_w, (hipStream_t)stream));
+}
+
+pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const uint8_t* mask,
+                           int64_t T, int n, int k, pcm_beta_mode beta_mode, const pcm_paths* out,
+                           void* ws, size_t ws_bytes, void* stream) {
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if (beta_mode < PCM_BETA_SRC_COND || beta_mode > PCM_BETA_GLOBAL) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!topk_ids || !topk_w || !mask || check_paths(out) != PCM_OK) return PCM_ERR_ARG;
+    const size_t need = build_paths_ws_bytes(T, n);
+    if (ws_bytes < need || (need && !ws)) return PCM_ERR_WORKSPACE;
+    return from_hip(launch_build_paths(topk_ids, topk_w, mask, T, n, k, (int)beta_mode,
+                                       out->path_bits, out->beta, out->expert_offsets,
+                                       out->row_token, out->row_slot, out->row_of, (int32_t*)ws,
+                                       (hipStream_t)stream));
+}
+
+pcm_status pcm_expand(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                      const pcm_paths* paths, int64_t T, int H, int F, int n, int k, void* u,
+                      void* ws, size_t ws_bytes, void* stream) {
+    (void)ws;
+    (void)ws_bytes;
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if ((st = check_dims(H, F)) != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!x || !w_gate || !w_up || !u || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
+    if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(u)) return PCM_ERR_ARG;
+    GemmArgs g{};
+    g.a = x;
+    g.b0 = w_gate;
+    g.b1 = w_up;
+    g.out = u;
+    g.offsets = paths->expert_offsets;
+    g.gather = paths->row_token;
+    g.a_rows = T;
+    g.n = n;
+    g.K = H;
+    g.N = F;
+    const int64_t R = T * k;
+    hipStream_t s = (hipStream_t)stream;
+    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s)
+                                      : launch_gemm_f32(kExpand, g, R, s));
+}
+
+pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_down,
+                               const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
+                               float* y, int accumulate, void* ws, size_t ws_bytes, void* stream) {
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if ((st = check_dims(H, F)) != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!u || !w_down || !y || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
+    if (!aligned16(u) || !aligned16(w_down) || !aligned16(y)) return PCM_ERR_ARG;
+    size_t o_off = 0;
+    const size_t need = project_ws(T, H, F, k, dtype, &o_off);
+    if (!ws || ws_bytes < need) return PCM_ERR_WORKSPACE;
+    if (!aligned16(ws)) return PCM_ERR_ARG;
+    void* z = ws;
+    float* o = (float*)((char*)ws + o_off);
+    const int64_t R = T * k;
+    hipStream_t s = (hipStream_t)stream;
+    const bool bf16 = dtype == PCM_BF16;
+    hipError_t e = launch_mix(bf16, u, z, paths->path_bits, paths->beta, paths->row_of, T, k, F, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    GemmArgs g{};
+    g.a = z;
+    g.b0 = w_down;
+    g.out = o;
+    g.offsets = paths->expert_offsets;
+    g.a_rows = R;
+    g.n = n;
+    g.K = F;
+    g.N = H;
+    e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s) : launch_gemm_f32(kDownStore, g, R, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    return from_hip(launch_combine(o, paths->row_of, T, k, H, y, accumulate, s));
+}
+
+pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                            const void* w_down, int64_t T, int H, int Fs, float* y, int accumulate,
+                            void* ws, size_t ws_bytes, void* stream) {
+    if (T < 0) return PCM_ERR_ARG;
+    pcm_status st = check_dims(H, Fs);
+    if (st != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T >= ((int64_t)1 << 31)) return PCM_ERR_UNSUPPORTED;
+    if (T == 0) return PCM_OK;
+    if (!x || !w_gate || !w_up || !w_down || !y) return PCM_ERR_ARG;
+    if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y))
+        return PCM_ERR_ARG;
+    const size_t need = align_up((size_t)T * Fs * elem_bytes(dtype), 256);
+    if (!ws || ws_bytes < need) return PCM_ERR_WORKSPACE;
+    if (!aligned16(ws)) return PCM_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    const bool bf16 = dtype == PCM_BF16;
+    GemmArgs g{};
+    g.a = x;
+    g.b0 = w_gate;
+    g.b1 = w_up;
+    g.out = ws;
+    g.offsets = nullptr;
+    g.gather = nullptr;
+    g.a_rows = T;
+    g.n = 1;
+    g.K = H;
+    g.N = Fs;
+    hipError_t e = bf16 ? launch_gemm_bf16(kExpand, g, T, s) : launch_gemm_f32(kExpand, g, T, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    GemmArgs d{};
+    d.a = ws;
+    d.b0 = w_down;
+    d.out = y;
+    d.offsets = nullptr;
+    d.a_rows = T;
+    d.n = 1;
+    d.K = Fs;
+    d.N = H;
+    d.accumulate = accumulate;
+    e = bf16 ? launch_gemm_bf16(kDownAccum, d, T, s) : launch_gemm_f32(kDownAccum, d, T, s);
+    return from_hip(e);
+}
+
+}  // extern "C"

@@ -1,0 +1,104 @@
+"""The C ABI library loads, exports every symbol the header declares, and rejects
+invalid arguments on the host before touching a device (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_01024_amd as pcm
+from paper_2609_01024_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pcomoe.h")
+
+OK, ARG, UNSUP, WS, HIP = 0, 1, 2, 3, 4
+
+
+def declared_functions():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return sorted(set(re.findall(r"\b(pcm_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return pcm.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert set(names) == set(binding.EXPORTS), names
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_abi_version_and_status_strings(L):
+    assert L.pcm_abi_version() == 100
+    for s in (OK, ARG, UNSUP, WS, HIP):
+        assert L.pcm_status_string(s).decode().startswith("PCM_")
+    assert L.pcm_status_string(77) == b"unknown pcm_status"
+
+
+FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: validation fails first
+
+
+def test_route_validation(L):
+    assert L.pcm_route(FAKE, 4, 8, 9, FAKE, FAKE, None) == ARG       # k > n
+    assert L.pcm_route(FAKE, 4, 8, 0, FAKE, FAKE, None) == ARG       # k < 1
+    assert L.pcm_route(FAKE, -1, 8, 2, FAKE, FAKE, None) == ARG      # T < 0
+    assert L.pcm_route(FAKE, 4, 300, 2, FAKE, FAKE, None) == UNSUP   # n > 256
+    assert L.pcm_route(FAKE, 4, 16, 9, FAKE, FAKE, None) == UNSUP    # k > 8
+    assert L.pcm_route(None, 4, 8, 2, FAKE, FAKE, None) == ARG       # null
+    assert L.pcm_route(ctypes.c_void_p(0x10004), 4, 8, 2, FAKE, FAKE, None) == ARG  # misaligned
+    assert L.pcm_route(None, 0, 8, 2, None, None, None) == OK        # T = 0 no-op
+    assert L.pcm_route(FAKE, 1 << 29, 8, 8, FAKE, FAKE, None) == UNSUP  # T*k >= 2^31
+
+
+def _paths(null_field=None):
+    vals = {f: 0x10000 for f, _ in binding.PcmPaths._fields_}
+    if null_field:
+        vals[null_field] = 0
+    return binding.PcmPaths(**vals)
+
+
+def test_build_paths_validation(L):
+    p = _paths()
+    assert L.pcm_build_paths(FAKE, FAKE, FAKE, 4, 8, 2, 3, ctypes.byref(p), None, 0, None) == ARG
+    for f, _ in binding.PcmPaths._fields_:
+        q = _paths(f)
+        assert L.pcm_build_paths(FAKE, FAKE, FAKE, 4, 8, 2, 0, ctypes.byref(q), None, 0, None) == ARG
+    need = L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 5000, 0, 0, 64, 8, 0)
+    assert need > 0
+    assert L.pcm_build_paths(FAKE, FAKE, FAKE, 5000, 64, 8, 0, ctypes.byref(p), FAKE, need - 1,
+                             None) == WS
+    assert L.pcm_build_paths(FAKE, FAKE, FAKE, 0, 64, 8, 0, None, None, 0, None) == OK
+
+
+def test_expand_and_project_validation(L):
+    p = _paths()
+    bp = ctypes.byref(p)
+    assert L.pcm_expand(1, FAKE, FAKE, FAKE, bp, 4, 100, 128, 8, 2, FAKE, None, 0, None) == UNSUP
+    assert L.pcm_expand(1, FAKE, FAKE, FAKE, bp, 4, 128, 96, 8, 2, FAKE, None, 0, None) == UNSUP
+    assert L.pcm_expand(7, FAKE, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
+    assert L.pcm_expand(1, FAKE, None, FAKE, bp, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
+    assert L.pcm_expand(1, FAKE, FAKE, FAKE, None, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
+    need = L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, 4, 128, 128, 8, 2, 1)
+    assert need >= 4 * 2 * 128 * 2 + 4 * 2 * 128 * 4
+    assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, 0, FAKE, need - 1,
+                                 None) == WS
+    assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, 0, None, need,
+                                 None) == WS
+    assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 9, FAKE, 0, FAKE, need,
+                                 None) == ARG
+    needd = L.pcm_workspace_bytes(binding.OP_DENSE_SWIGLU, 16, 128, 256, 1, 1, 1)
+    assert needd == 16 * 256 * 2
+    assert L.pcm_dense_swiglu(1, FAKE, FAKE, FAKE, FAKE, 16, 128, 256, FAKE, 0, FAKE, needd - 1,
+                              None) == WS
+    assert L.pcm_dense_swiglu(1, FAKE, FAKE, FAKE, FAKE, 16, 128, 200, FAKE, 0, FAKE, needd,
+                              None) == UNSUP
+    assert L.pcm_dense_swiglu(1, None, None, None, None, 0, 128, 256, None, 0, None, 0, None) == OK
+
+
+def test_workspace_bytes_invalid(L):
+    assert L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, -1, 128, 128, 8, 2, 1) == 0
+    assert L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 1024, 0, 0, 8, 2, 0) == 0  # one block
