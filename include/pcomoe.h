@@ -48,8 +48,9 @@ typedef enum pcm_status {
 } pcm_status;
 
 typedef enum pcm_dtype {
-    PCM_F32 = 0,   /* x, weights, U and intermediates in float32; FMA on the vector ALUs */
-    PCM_BF16 = 1   /* x, weights, U and intermediates in bfloat16; MFMA, float32 accumulate */
+    PCM_F32 = 0,   /* x and weights float32; FMA on the vector ALUs */
+    PCM_BF16 = 1   /* x and weights bfloat16; bf16 MFMA with float32 accumulate; the
+                      intermediates u and z are kept at float32 accuracy */
 } pcm_dtype;
 
 /* Path weights beta_ab for (a, b) in Pi (p = the renormalised router weights).
@@ -104,18 +105,21 @@ pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const u
 
 /* Expansion side, once per (token, source) row (Section 4.1 U_e; Section 4.3 reuse):
  * u[r,:] = SiLU(x[row_token[r]] W_gate[e]^T) * (x[row_token[r]] W_up[e]^T) for the rows r
- * of expert e. x [T,H], w_gate/w_up [n,F,H], u [T*k,F], all of `dtype` (device).
- * bf16: products accumulate in float32, SiLU and the product in float32, u rounded to
- * nearest even. ws: pcm_workspace_bytes(PCM_OP_EXPAND, ...) bytes (currently 0; may be NULL). */
+ * of expert e. x [T,H] and w_gate/w_up [n,F,H] of `dtype`; u [T*k,F] float32 (device).
+ * bf16: MFMA products accumulate in float32; SiLU and the product are float32 and u is
+ * stored unrounded. ws: pcm_workspace_bytes(PCM_OP_EXPAND, ...) bytes (0; may be NULL). */
 pcm_status pcm_expand(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
                       const pcm_paths* paths, int64_t T, int H, int F, int n, int k, void* u,
                       void* ws, size_t ws_bytes, void* stream);
 
 /* Projection side and combine (Section 4.1 D_e and path aggregation; Section 4.3):
- * z_(t,b) = sum_{a : (a,b) in Pi} beta_ab u_(t,a)   (float32 math, stored in `dtype`),
+ * z_(t,b) = sum_{a : (a,b) in Pi} beta_ab u_(t,a)   (float32),
  * o_(t,b) = W_down[e_b] z_(t,b)                     (float32 accumulate),
  * y_t = [y_t if accumulate] + sum_{b ascending} o_(t,b).
- * u [T*k,F] from pcm_expand, w_down [n,H,F] of `dtype`, y [T,H] f32 (device).
+ * For bf16 layers z enters the bf16 MFMA as a pair of bfloat16 values (hi = z rounded,
+ * lo = the rounding error rounded), both multiplied by the same weight tile, so the
+ * projection sees z to about 2^-17 relative instead of one bfloat16 rounding.
+ * u [T*k,F] f32 from pcm_expand, w_down [n,H,F] of `dtype`, y [T,H] f32 (device).
  * ws: pcm_workspace_bytes(PCM_OP_PROJECT_COMBINE, ...) bytes (holds z and o). */
 pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_down,
                                const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
@@ -125,6 +129,7 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
 /* A dense SwiGLU FFN applied to every token with weight 1 (Section 2's expert F_e), for an
  * always-on shared expert that sits beside the routed experts and outside the path
  * space: y_t = [y_t if accumulate] + W_down (SiLU(W_gate x_t) * (W_up x_t)).
+ * The SwiGLU output is kept at float32 accuracy (bf16 layers: as a hi/lo bfloat16 pair).
  * x [T,H], w_gate/w_up [Fs,H], w_down [H,Fs] of `dtype`; y [T,H] f32 (device).
  * ws: pcm_workspace_bytes(PCM_OP_DENSE_SWIGLU, T, H, Fs, 1, 1, dtype) bytes. */
 pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate,

@@ -154,7 +154,7 @@ def pcm_expand(x, w_gate, w_up, paths: PathTable, u=None, stream=None) -> torch.
     _dev(x, w_gate, w_up, u)
     T, H = x.shape
     n, F, _ = w_gate.shape
-    u = u if u is not None else torch.empty((T * paths.k, F), dtype=x.dtype, device=x.device)
+    u = u if u is not None else torch.empty((T * paths.k, F), dtype=torch.float32, device=x.device)
     st = paths.struct()
     _check(lib().pcm_expand(_dtype_code(x), _ptr(x), _ptr(w_gate), _ptr(w_up), ctypes.byref(st), T, H,
                             F, n, paths.k, _ptr(u), None, 0, _stream(stream)))
@@ -167,7 +167,7 @@ def pcm_project_combine(u, w_down, paths: PathTable, y=None, accumulate: bool = 
     n, H, F = w_down.shape
     T, k = paths.T, paths.k
     y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
-    dt = _dtype_code(u)
+    dt = _dtype_code(w_down)
     if ws is None:
         ws = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), u.device)
     st = paths.struct()
@@ -205,7 +205,7 @@ class LayerPlan:
         self.w = torch.empty((T, k), dtype=torch.float32, device=device)
         self.paths = PathTable.empty(T, n, k, device)
         self.ws_paths = _workspace(workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0), device)
-        self.u = torch.empty((T * k, F), dtype=dtype, device=device)
+        self.u = torch.empty((T * k, F), dtype=torch.float32, device=device)
         self.ws_proj = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), device)
         self.ws_shared = (_workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, shared_F, 1, 1, dt), device)
                           if shared_F else None)

@@ -2,17 +2,20 @@
 // accumulate) for the two sides of a SwiGLU expert (Section 4.1):
 //   expand:  U[r, f] = SiLU(x[tok(r)] . W_gate[e][f]) * (x[tok(r)] . W_up[e][f])
 //            one row per (token, source) pair, rows of expert e contiguous (Section 4.3),
-//            x rows gathered through row_token; SwiGLU fused into the epilogue.
+//            x rows gathered through row_token; SwiGLU fused into the epilogue; U kept in
+//            float32 (or written as split hi/lo bf16 pairs for a dense FFN).
 //   down:    O[r, h] = Z[r] . W_down[e][h]        (store, or accumulate into y for a
 //                                                  dense FFN whose rows are tokens)
+//            Z arrives as split hi/lo bf16 pairs; each weight fragment is multiplied by
+//            both halves, so the product sees Z to ~2^-17 relative.
 // Both operands are K-contiguous (x rows and W rows run along H; Z rows and W_down rows
 // along F), so a lane's 8 consecutive K values of a row are one 16-byte load.
 //
 // Tile: BM rows x BNB weight rows x 64 K per stage, two LDS stages (global loads of
-// stage k+1 overlap the MFMAs of stage k). LDS rows are padded to 144 bytes, which makes
+// stage k+1 overlap the MFMAs of stage k). LDS rows are padded by 16 bytes, which makes
 // the 16-byte fragment reads of 16 consecutive rows bank-conflict-free. The MFMA takes
 // the weight fragment as its first operand, so each lane's four accumulators are four
-// consecutive output columns of one row: 8-byte (bf16 U) or 16-byte (f32) stores.
+// consecutive output columns of one row (16-byte float32 stores).
 // For the expansion, a wave's weight rows are half gate and half up for the same columns,
 // so gate and up values of an output element sit in the same lane and register slot.
 //
@@ -28,24 +31,32 @@ namespace pcm {
 namespace {
 
 constexpr int BK = 64;
-constexpr int LDS_STRIDE = BK + 8;  // bf16 elements per LDS row
 
-template <int BM_, int BNB_, int WM_, int WN_>
+template <int BM_, int BNB_, int WM_, int WN_, int AK_>
 struct Cfg {
     static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_;
+    static constexpr int AK = AK_;                 // A columns staged per K step (64, or 128 = hi|lo)
     static constexpr int NT = WM * WN * 64;
     static constexpr int WTM = BM / WM, WTN = BNB / WN;
     static constexpr int MB = WTM / 16, NBK = WTN / 16;
-    static constexpr int A_CHUNKS = BM * BK / 8, B_CHUNKS = BNB * BK / 8;
+    static constexpr int A_STRIDE = AK + 8, B_STRIDE = BK + 8;  // bf16 elements per LDS row
+    static constexpr int A_CPR = AK / 8, B_CPR = BK / 8;       // 16-byte chunks per row
+    static constexpr int A_CHUNKS = BM * A_CPR, B_CHUNKS = BNB * B_CPR;
     static constexpr int A_PER_T = (A_CHUNKS + NT - 1) / NT, B_PER_T = (B_CHUNKS + NT - 1) / NT;
-    static constexpr int LDS_A = BM * LDS_STRIDE, LDS_B = BNB * LDS_STRIDE;
+    static constexpr int LDS_A = BM * A_STRIDE, LDS_B = BNB * B_STRIDE;
     static constexpr int LDS_BYTES = 2 * (LDS_A + LDS_B) * 2;
-    static_assert(WTM % 16 == 0 && WTN % 32 == 0, "wave tile must hold whole MFMA blocks");
+    static_assert(WTM % 16 == 0 && WTN % 16 == 0, "wave tile must hold whole MFMA blocks");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
 
-using CfgL = Cfg<256, 256, 2, 4>;  // large groups
-using CfgM = Cfg<128, 128, 2, 2>;  // medium groups
-using CfgS = Cfg<16, 256, 1, 4>;   // few rows per group: weight streaming
+// expansion tiles (A = x rows, 64 K per stage)
+using ExpL = Cfg<256, 256, 2, 4, 64>;
+using ExpM = Cfg<128, 128, 2, 2, 64>;
+using ExpS = Cfg<16, 256, 1, 4, 64>;
+// projection tiles (A = split z rows: 64 hi + 64 lo per stage)
+using DownL = Cfg<128, 256, 2, 4, 128>;
+using DownM = Cfg<64, 128, 1, 4, 128>;
+using DownS = Cfg<16, 128, 1, 4, 128>;
 
 // Find this workgroup's group and row range. Returns false past the last tile.
 template <int BM>
@@ -97,10 +108,16 @@ __device__ bool find_tile(const int32_t* __restrict__ offsets, int n, int64_t a_
     return s_tile[0] >= 0;
 }
 
+__device__ inline uint32_t pack_bf16x2(float a, float b) {
+    return (uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16);
+}
+
 template <class C, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt_upper) {
     extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
     __shared__ int s_tile[3];
+    constexpr bool kSplitA = C::AK == 2 * BK;
+    static_assert(MODE == kExpand ? !kSplitA : kSplitA, "expand reads x, down reads split z");
     const int64_t mt = blockIdx.x % mt_upper;
     const int ntile = (int)(blockIdx.x / mt_upper);
     if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
@@ -109,6 +126,7 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / C::WN, wn = wave % C::WN;
     const int K = g.K, N = g.N;
+    const int64_t a_row_elems = kSplitA ? 2 * (int64_t)K : K;      // bf16 elements per A row
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;  // output columns per tile
 
     // Global source of each 16-byte chunk this thread stages.
@@ -118,7 +136,7 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
 #pragma unroll
     for (int i = 0; i < C::A_PER_T; ++i) {
         const int c = tid + i * C::NT;
-        const int row = c / (BK / 8), kc = c % (BK / 8);
+        const int row = c / C::A_CPR, kc = c % C::A_CPR;
         const int r = row0 + row;
         aptr[i] = nullptr;
         if (c < C::A_CHUNKS && r < row1) {
@@ -127,13 +145,13 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
                 src = g.gather[r];
                 src = src < 0 ? 0 : (src >= g.a_rows ? g.a_rows - 1 : src);
             }
-            aptr[i] = A + src * K + kc * 8;
+            aptr[i] = A + src * a_row_elems + kc * 8;
         }
     }
 #pragma unroll
     for (int i = 0; i < C::B_PER_T; ++i) {
         const int c = tid + i * C::NT;
-        const int j = c / (BK / 8), kc = c % (BK / 8);
+        const int j = c / C::B_CPR, kc = c % C::B_CPR;
         bptr[i] = nullptr;
         if (c < C::B_CHUNKS) {
             if (MODE == kExpand) {
@@ -152,7 +170,7 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
     auto gload = [&](int kt) {
 #pragma unroll
         for (int i = 0; i < C::A_PER_T; ++i)
-            ra[i] = aptr[i] ? *(const uint4*)(aptr[i] + (int64_t)kt * BK) : make_uint4(0, 0, 0, 0);
+            ra[i] = aptr[i] ? *(const uint4*)(aptr[i] + (int64_t)kt * C::AK) : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int i = 0; i < C::B_PER_T; ++i)
             rb[i] = bptr[i] ? *(const uint4*)(bptr[i] + (int64_t)kt * BK) : make_uint4(0, 0, 0, 0);
@@ -163,14 +181,12 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
 #pragma unroll
         for (int i = 0; i < C::A_PER_T; ++i) {
             const int c = tid + i * C::NT;
-            if (c < C::A_CHUNKS)
-                *(uint4*)(As + (c / (BK / 8)) * LDS_STRIDE + (c % (BK / 8)) * 8) = ra[i];
+            if (c < C::A_CHUNKS) *(uint4*)(As + (c / C::A_CPR) * C::A_STRIDE + (c % C::A_CPR) * 8) = ra[i];
         }
 #pragma unroll
         for (int i = 0; i < C::B_PER_T; ++i) {
             const int c = tid + i * C::NT;
-            if (c < C::B_CHUNKS)
-                *(uint4*)(Bs + (c / (BK / 8)) * LDS_STRIDE + (c % (BK / 8)) * 8) = rb[i];
+            if (c < C::B_CHUNKS) *(uint4*)(Bs + (c / C::B_CPR) * C::B_STRIDE + (c % C::B_CPR) * 8) = rb[i];
         }
     };
 
@@ -195,15 +211,25 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
             const int koff = ks * 32 + (lane >> 4) * 8;
 #pragma unroll
             for (int nb = 0; nb < C::NBK; ++nb)
-                bfr[nb] = *(const bf16x8*)(Bs + (wn * C::WTN + nb * 16 + (lane & 15)) * LDS_STRIDE + koff);
+                bfr[nb] = *(const bf16x8*)(Bs + (wn * C::WTN + nb * 16 + (lane & 15)) * C::B_STRIDE + koff);
 #pragma unroll
             for (int mb = 0; mb < C::MB; ++mb)
-                afr[mb] = *(const bf16x8*)(As + (wm * C::WTM + mb * 16 + (lane & 15)) * LDS_STRIDE + koff);
+                afr[mb] = *(const bf16x8*)(As + (wm * C::WTM + mb * 16 + (lane & 15)) * C::A_STRIDE + koff);
 #pragma unroll
             for (int nb = 0; nb < C::NBK; ++nb)
 #pragma unroll
                 for (int mb = 0; mb < C::MB; ++mb)
                     acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
+            if (kSplitA) {  // the low halves, same weight fragments
+#pragma unroll
+                for (int mb = 0; mb < C::MB; ++mb)
+                    afr[mb] = *(const bf16x8*)(As + (wm * C::WTM + mb * 16 + (lane & 15)) * C::A_STRIDE + BK + koff);
+#pragma unroll
+                for (int nb = 0; nb < C::NBK; ++nb)
+#pragma unroll
+                    for (int mb = 0; mb < C::MB; ++mb)
+                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
+            }
         }
         if (kt + 1 < KT) lstore(cur ^ 1);
         __syncthreads();
@@ -215,18 +241,26 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
         const int r = row0 + wm * C::WTM + mb * 16 + (lane & 15);
         if (r >= row1) continue;
         if (MODE == kExpand) {
-            uint16_t* U = (uint16_t*)g.out;
 #pragma unroll
             for (int nb = 0; nb < C::NBK / 2; ++nb) {
                 const int f = ntile * kOutCols + wn * (C::WTN / 2) + nb * 16 + (lane >> 4) * 4;
                 if (f >= N) continue;
                 const floatx4 gt = acc[nb][mb], up = acc[nb + C::NBK / 2][mb];
-                uint16_t h[4];
+                float v[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) h[i] = f32_to_bf16_rne(gt[i] / (1.0f + __expf(-gt[i])) * up[i]);
-                uint2 packed = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16),
-                                          (uint32_t)h[2] | ((uint32_t)h[3] << 16));
-                *(uint2*)(U + (int64_t)r * N + f) = packed;
+                for (int i = 0; i < 4; ++i) v[i] = gt[i] / (1.0f + __expf(-gt[i])) * up[i];
+                if (g.split_out) {
+                    // hi at [blk][0..63], lo at [blk][64..127] of the row's split layout
+                    uint16_t* U = (uint16_t*)g.out + (int64_t)r * 2 * N + (f / kSplitBlock) * 2 * kSplitBlock
+                                  + f % kSplitBlock;
+                    float lo[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) lo[i] = v[i] - bf16_bits_to_f32(f32_to_bf16_rne(v[i]));
+                    *(uint2*)U = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                    *(uint2*)(U + kSplitBlock) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+                } else {
+                    *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
+                }
             }
         } else {
             float* O = (float*)g.out;
@@ -275,23 +309,23 @@ char pick_tile(int64_t R, int groups) {
     return 'L';
 }
 
-template <int MODE>
-hipError_t launch_mode(const GemmArgs& g, int64_t R, hipStream_t s) {
-    switch (pick_tile(R, g.offsets ? g.n : 1)) {
-        case 'S': return launch_cfg<CfgS, MODE>(g, R, s);
-        case 'M': return launch_cfg<CfgM, MODE>(g, R, s);
-        default: return launch_cfg<CfgL, MODE>(g, R, s);
-    }
-}
-
 }  // namespace
 
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s) {
-    switch (mode) {
-        case kExpand: return launch_mode<kExpand>(g, R, s);
-        case kDownStore: return launch_mode<kDownStore>(g, R, s);
-        default: return launch_mode<kDownAccum>(g, R, s);
+    const char t = pick_tile(R, g.offsets ? g.n : 1);
+    if (mode == kExpand) {
+        if (t == 'S') return launch_cfg<ExpS, kExpand>(g, R, s);
+        if (t == 'M') return launch_cfg<ExpM, kExpand>(g, R, s);
+        return launch_cfg<ExpL, kExpand>(g, R, s);
     }
+    if (mode == kDownStore) {
+        if (t == 'S') return launch_cfg<DownS, kDownStore>(g, R, s);
+        if (t == 'M') return launch_cfg<DownM, kDownStore>(g, R, s);
+        return launch_cfg<DownL, kDownStore>(g, R, s);
+    }
+    if (t == 'S') return launch_cfg<DownS, kDownAccum>(g, R, s);
+    if (t == 'M') return launch_cfg<DownM, kDownAccum>(g, R, s);
+    return launch_cfg<DownL, kDownAccum>(g, R, s);
 }
 
 }  // namespace pcm

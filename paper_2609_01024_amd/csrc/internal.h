@@ -35,24 +35,34 @@ size_t build_paths_ws_bytes(int64_t T, int n);
 
 enum GemmMode { kExpand = 0, kDownStore = 1, kDownAccum = 2 };
 
+// Layout of a bf16 layer's projection input z (and of a dense FFN's SwiGLU output): a
+// float32 value v is carried as the bfloat16 pair hi = rn(v), lo = rn(v - hi), which
+// represents v to about 2^-17 relative. Row r holds F/64 blocks of [64 hi | 64 lo].
+// The down GEMM multiplies both halves by the same weight tile, so the projection sees
+// the float32 value instead of a single bfloat16 rounding of it.
+constexpr int kSplitBlock = 64;
+
 struct GemmArgs {
-    const void* a;              // expand: x [T,H] (rows gathered); down: z [R,F] (rows in order)
+    const void* a;              // expand: x [T,H] (rows gathered); down: z (split bf16 or f32)
     const void* b0;             // expand: w_gate [n,F,H]; down: w_down [n,H,F]
     const void* b1;             // expand: w_up [n,F,H]; down: unused
-    void* out;                  // expand: u [R,F]; down-store: o [R,H] f32; down-accum: y [R,H] f32
-    const int32_t* offsets;     // [n+1] rows of each group
+    void* out;                  // expand: u [R,F] f32 (or split bf16, see split_out);
+                                // down-store: o [R,H] f32; down-accum: y [R,H] f32
+    const int32_t* offsets;     // [n+1] rows of each group (NULL: one group of a_rows rows)
     const int32_t* gather;      // expand: row_token [R] (NULL: identity); down: unused
     int64_t a_rows;             // rows of `a` (gathered indices are clamped to it)
     int n;                      // groups
     int K;                      // contraction length (H for expand, F for down)
     int N;                      // output columns (F for expand, H for down)
     int accumulate;             // down-accum: add into out
+    int split_out;              // expand (bf16): write u as split hi/lo pairs instead of f32
 };
 
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
 hipError_t launch_gemm_f32(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
 
-hipError_t launch_mix(bool bf16, const void* u, void* z, const uint64_t* bits, const float* beta,
+// z_(t,b) = sum_a beta_ab u_(t,a); u is f32 [R,F]; z is split bf16 (split) or f32 [R,F].
+hipError_t launch_mix(bool split, const float* u, void* z, const uint64_t* bits, const float* beta,
                       const int32_t* row_of, int64_t T, int k, int F, hipStream_t s);
 hipError_t launch_combine(const float* o, const int32_t* row_of, int64_t T, int k, int H,
                           float* y, int accumulate, hipStream_t s);

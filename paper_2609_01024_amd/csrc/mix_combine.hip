@@ -2,40 +2,29 @@
 //   mix:     z_(t,b) = sum_{a : (a,b) in Pi(t)} beta_ab u_(t,a)   (a ascending, float32 math)
 //            Because the projection W_down[e_b] is linear, applying it once to z_(t,b)
 //            equals summing beta_ab W_down[e_b] u_(t,a) over the paths into target b.
+//            For bf16 layers z is written as split hi/lo bf16 pairs for the down GEMM.
 //   combine: y_t = [y_t] + sum_{b ascending} o_(t,b)
-// One workgroup per token; each thread owns 8 consecutive columns (16 or 32 bytes).
+// One workgroup per token; each thread owns 8 consecutive columns.
 #include "internal.h"
 
 namespace pcm {
 namespace {
 
-__device__ inline void load8(const uint16_t* p, float* v) {
-    const uint4 q = *(const uint4*)p;
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        v[2 * i] = bf16_bits_to_f32(w[i] & 0xFFFFu);
-        v[2 * i + 1] = bf16_bits_to_f32(w[i] >> 16);
-    }
-}
-__device__ inline void store8(uint16_t* p, const float* v) {
-    uint32_t w[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        w[i] = (uint32_t)f32_to_bf16_rne(v[2 * i]) | ((uint32_t)f32_to_bf16_rne(v[2 * i + 1]) << 16);
-    *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
-}
 __device__ inline void load8(const float* p, float* v) {
     const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
     v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
-__device__ inline void store8(float* p, const float* v) {
-    *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
-    *(float4*)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+__device__ inline uint4 pack8(const float* v) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        w[i] = (uint32_t)f32_to_bf16_rne(v[2 * i]) | ((uint32_t)f32_to_bf16_rne(v[2 * i + 1]) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void mix_kernel(const T* __restrict__ u, T* __restrict__ z,
+// One token per workgroup; 8 consecutive columns per thread.
+template <bool SPLIT>
+__global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, void* __restrict__ z,
                                                   const uint64_t* __restrict__ bits,
                                                   const float* __restrict__ beta,
                                                   const int32_t* __restrict__ row_of, int k, int F,
@@ -66,7 +55,19 @@ __global__ __launch_bounds__(256) void mix_kernel(const T* __restrict__ u, T* __
                     for (int i = 0; i < 8; ++i) acc[i] = fmaf(w, ua[a][i], acc[i]);
                 }
             }
-            store8(z + rows[b] * F + c, acc);
+            if (SPLIT) {
+                float lo[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) lo[i] = acc[i] - bf16_bits_to_f32(f32_to_bf16_rne(acc[i]));
+                uint16_t* dst = (uint16_t*)z + rows[b] * 2 * F + (c / kSplitBlock) * 2 * kSplitBlock
+                                + c % kSplitBlock;
+                *(uint4*)dst = pack8(acc);
+                *(uint4*)(dst + kSplitBlock) = pack8(lo);
+            } else {
+                float* dst = (float*)z + rows[b] * F + c;
+                *(float4*)dst = make_float4(acc[0], acc[1], acc[2], acc[3]);
+                *(float4*)(dst + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+            }
         }
     }
 }
@@ -101,16 +102,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 
 }  // namespace
 
-hipError_t launch_mix(bool bf16, const void* u, void* z, const uint64_t* bits, const float* beta,
+hipError_t launch_mix(bool split, const float* u, void* z, const uint64_t* bits, const float* beta,
                       const int32_t* row_of, int64_t T, int k, int F, hipStream_t s) {
     if (T == 0) return hipSuccess;
     const int threads = F / 8 >= 256 ? 256 : ((F / 8 + 63) / 64) * 64;
-    if (bf16)
-        mix_kernel<uint16_t><<<(unsigned)T, threads, 0, s>>>((const uint16_t*)u, (uint16_t*)z, bits,
-                                                             beta, row_of, k, F, T * k);
+    if (split)
+        mix_kernel<true><<<(unsigned)T, threads, 0, s>>>(u, z, bits, beta, row_of, k, F, T * k);
     else
-        mix_kernel<float><<<(unsigned)T, threads, 0, s>>>((const float*)u, (float*)z, bits, beta,
-                                                          row_of, k, F, T * k);
+        mix_kernel<false><<<(unsigned)T, threads, 0, s>>>(u, z, bits, beta, row_of, k, F, T * k);
     return hipGetLastError();
 }
 

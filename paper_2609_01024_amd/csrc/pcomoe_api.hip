@@ -33,12 +33,12 @@ pcm_status check_paths(const pcm_paths* p) {
 
 pcm_status from_hip(hipError_t e) { return e == hipSuccess ? PCM_OK : PCM_ERR_HIP; }
 
-size_t elem_bytes(pcm_dtype d) { return d == PCM_BF16 ? 2 : 4; }
-
-// project_combine workspace: z [R,F] of dtype, then o [R,H] f32, each 256-byte aligned.
+// project_combine workspace: z [R,F] (f32, or split bf16 pairs of the same size), then
+// o [R,H] f32, each 256-byte aligned.
 size_t project_ws(int64_t T, int H, int F, int k, pcm_dtype dt, size_t* o_offset) {
+    (void)dt;
     const size_t R = (size_t)T * k;
-    const size_t z = align_up(R * F * elem_bytes(dt), 256);
+    const size_t z = align_up(R * F * sizeof(float), 256);
     if (o_offset) *o_offset = z;
     return z + align_up(R * H * sizeof(float), 256);
 }
@@ -68,9 +68,9 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
         case PCM_OP_PROJECT_COMBINE:
             if (H < 1 || F < 1) return 0;
             return project_ws(T, H, F, k, dtype, nullptr);
-        case PCM_OP_DENSE_SWIGLU:
+        case PCM_OP_DENSE_SWIGLU:  // the SwiGLU output, f32 or split bf16 pairs (same size)
             if (H < 1 || F < 1) return 0;
-            return align_up((size_t)T * F * elem_bytes(dtype), 256);
+            return align_up((size_t)T * F * sizeof(float), 256);
     }
     return 0;
 }
@@ -149,7 +149,8 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
     const int64_t R = T * k;
     hipStream_t s = (hipStream_t)stream;
     const bool bf16 = dtype == PCM_BF16;
-    hipError_t e = launch_mix(bf16, u, z, paths->path_bits, paths->beta, paths->row_of, T, k, F, s);
+    hipError_t e = launch_mix(bf16, (const float*)u, z, paths->path_bits, paths->beta, paths->row_of,
+                              T, k, F, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     GemmArgs g{};
     g.a = z;
@@ -177,7 +178,7 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     if (!x || !w_gate || !w_up || !w_down || !y) return PCM_ERR_ARG;
     if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y))
         return PCM_ERR_ARG;
-    const size_t need = align_up((size_t)T * Fs * elem_bytes(dtype), 256);
+    const size_t need = align_up((size_t)T * Fs * sizeof(float), 256);
     if (!ws || ws_bytes < need) return PCM_ERR_WORKSPACE;
     if (!aligned16(ws)) return PCM_ERR_ARG;
     hipStream_t s = (hipStream_t)stream;
@@ -193,6 +194,7 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     g.n = 1;
     g.K = H;
     g.N = Fs;
+    g.split_out = bf16 ? 1 : 0;
     hipError_t e = bf16 ? launch_gemm_bf16(kExpand, g, T, s) : launch_gemm_f32(kExpand, g, T, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     GemmArgs d{};

@@ -83,7 +83,7 @@ def test_expand_and_project_validation(L):
     assert L.pcm_expand(1, FAKE, None, FAKE, bp, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
     assert L.pcm_expand(1, FAKE, FAKE, FAKE, None, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
     need = L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, 4, 128, 128, 8, 2, 1)
-    assert need >= 4 * 2 * 128 * 2 + 4 * 2 * 128 * 4
+    assert need >= 4 * 2 * 128 * 4 + 4 * 2 * 128 * 4
     assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, 0, FAKE, need - 1,
                                  None) == WS
     assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, 0, None, need,
@@ -91,7 +91,7 @@ def test_expand_and_project_validation(L):
     assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 9, FAKE, 0, FAKE, need,
                                  None) == ARG
     needd = L.pcm_workspace_bytes(binding.OP_DENSE_SWIGLU, 16, 128, 256, 1, 1, 1)
-    assert needd == 16 * 256 * 2
+    assert needd == 16 * 256 * 4
     assert L.pcm_dense_swiglu(1, FAKE, FAKE, FAKE, FAKE, 16, 128, 256, FAKE, 0, FAKE, needd - 1,
                               None) == WS
     assert L.pcm_dense_swiglu(1, FAKE, FAKE, FAKE, FAKE, 16, 128, 200, FAKE, 0, FAKE, needd,

@@ -1,7 +1,8 @@
 """HIP path against the CPU oracle, through the C ABI (needs an MI355X).
 
 Integers (top-k ids, path bits, the dispatch layout) must match bit for bit.
-Floating point: router weights and path weights to 1e-5 relative; layer outputs
+Floating point: router weights and path weights to 1e-5 relative (absolute
+FLT_MIN below float32's normal range); layer outputs
 elementwise within |d| <= 1e-2 + 2e-2 |ref| and, tighter, a relative Frobenius
 error <= 5e-3 for bfloat16 layers (two roundings to bfloat16, of U and of the
 mixed z, each <= 2^-9 relative) and max |d| <= 1e-4 max |ref| for float32 layers.
@@ -19,6 +20,7 @@ from workloads import CONFIGS, make_inputs, scaled, stress_config
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
+FLT_MIN = float(np.finfo(np.float32).tiny)
 
 
 def say(msg):
@@ -57,7 +59,8 @@ def check_route(logits_np, k):
     ids, w = pcm.pcm_route(torch.from_numpy(logits_np).to(DEV), k)
     torch.cuda.synchronize()
     assert np.array_equal(ids.cpu().numpy(), ids_ref), "top-k ids differ"
-    np.testing.assert_allclose(w.cpu().numpy(), w_ref, rtol=1e-5, atol=0)
+    # float32 carries no relative precision below its smallest normal number
+    np.testing.assert_allclose(w.cpu().numpy(), w_ref, rtol=1e-5, atol=FLT_MIN)
     return ids, w
 
 
@@ -70,7 +73,7 @@ def check_paths(ids, w, mask_np, n, beta_mode=0):
     p = pcm.pcm_build_paths(ids, w, torch.from_numpy(mask_np).to(DEV), beta_mode)
     torch.cuda.synchronize()
     assert np.array_equal(p.path_bits.cpu().numpy().view(np.uint64), bits_ref), "path bits differ"
-    np.testing.assert_allclose(p.beta.cpu().numpy(), beta_ref, rtol=1e-5, atol=0)
+    np.testing.assert_allclose(p.beta.cpu().numpy(), beta_ref, rtol=1e-5, atol=FLT_MIN)
     assert np.array_equal(p.expert_offsets.cpu().numpy(), off_ref), "expert offsets differ"
     assert np.array_equal(p.row_token.cpu().numpy(), rt_ref), "row_token differs"
     assert np.array_equal(p.row_slot.cpu().numpy(), rs_ref), "row_slot differs"
@@ -193,9 +196,10 @@ def test_expand_rows_against_oracle():
     tok = p.row_token.cpu().numpy()[rows]
     ex = ids.cpu().numpy()[tok, p.row_slot.cpu().numpy()[rows]]
     ref = oracle.expansion_rows(inp.x, inp.w_gate, inp.w_up, tok, ex)
-    got = u.float().cpu().numpy()[rows]
+    got = u.cpu().numpy()[rows]
     scale = np.sqrt((ref ** 2).mean())
-    assert np.all(np.abs(got - ref) <= 2 ** -8 * np.abs(ref) + 1e-3 * scale)
+    # float32 accumulation of exact bf16 products over H terms
+    assert np.all(np.abs(got - ref) <= 1e-5 * np.abs(ref) + 1e-5 * scale)
 
 
 def test_layer_diagonal_mask_is_vanilla():
