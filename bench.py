@@ -38,7 +38,21 @@ def parse():
                     help="target CPU time of the oracle sample")
     ap.add_argument("--traffic", default=None,
                     help="JSON file with measured HBM bytes per launch of the dominant kernel")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized buffer 5 times (calibrates HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_probe(mib: int):
+    """A plain device-to-device copy of known size, for scaling FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_per_launch": n * 4, "launches": 5}), flush=True)
 
 
 def cpu_baseline(inp, target_s: float) -> dict:
@@ -63,6 +77,9 @@ def cpu_baseline(inp, target_s: float) -> dict:
 
 def main():
     args = parse()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the layer is sharded by design, not measured, across GPUs)", file=sys.stderr)

@@ -11,13 +11,18 @@
 // Both operands are K-contiguous (x rows and W rows run along H; Z rows and W_down rows
 // along F), so a lane's 8 consecutive K values of a row are one 16-byte load.
 //
-// Tile: BM rows x BNB weight rows x 64 K per stage, two LDS stages (global loads of
-// stage k+1 overlap the MFMAs of stage k). LDS rows are padded by 16 bytes, which makes
-// the 16-byte fragment reads of 16 consecutive rows bank-conflict-free. The MFMA takes
-// the weight fragment as its first operand, so each lane's four accumulators are four
-// consecutive output columns of one row (16-byte float32 stores).
-// For the expansion, a wave's weight rows are half gate and half up for the same columns,
-// so gate and up values of an output element sit in the same lane and register slot.
+// Two kernel shapes share the epilogue and the work decomposition:
+//  * "dma" (large tiles): global -> LDS direct loads (global_load_lds_dwordx4, no register
+//    staging), 32-wide K steps in NS LDS stages, loads issued NS-1 steps ahead, one
+//    workgroup barrier per step. LDS rows are 64 bytes; the 16-byte chunk c of row r sits
+//    at position c ^ ((r >> 1) & 3), which keeps the fragment reads (16 rows x 4 chunks per
+//    instruction) free of bank conflicts.
+//  * "staged" (small tiles): loads through registers into two LDS stages of 64-wide K
+//    steps; rows of 128 bytes with chunk c of row r at position c ^ ((r >> 1) & 7).
+// The MFMA takes the weight fragment as its first operand, so each lane's four
+// accumulators are four consecutive output columns of one row (16-byte stores). For the
+// expansion, a wave's weight rows are half gate and half up for the same columns, so the
+// gate and up values of an output element sit in the same lane and register slot.
 //
 // Work decomposition: the grid is (upper bound of M tiles) x (N tiles). Each workgroup
 // finds its group (expert) and row range from the group offsets with one wave-wide scan
@@ -27,36 +32,16 @@
 
 #include "internal.h"
 
+#define PCM_LDS __attribute__((address_space(3)))
+
 namespace pcm {
 namespace {
 
-constexpr int BK = 64;
-
-template <int BM_, int BNB_, int WM_, int WN_, int AK_>
-struct Cfg {
-    static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_;
-    static constexpr int AK = AK_;                 // A columns staged per K step (64, or 128 = hi|lo)
-    static constexpr int NT = WM * WN * 64;
-    static constexpr int WTM = BM / WM, WTN = BNB / WN;
-    static constexpr int MB = WTM / 16, NBK = WTN / 16;
-    static constexpr int A_STRIDE = AK + 8, B_STRIDE = BK + 8;  // bf16 elements per LDS row
-    static constexpr int A_CPR = AK / 8, B_CPR = BK / 8;       // 16-byte chunks per row
-    static constexpr int A_CHUNKS = BM * A_CPR, B_CHUNKS = BNB * B_CPR;
-    static constexpr int A_PER_T = (A_CHUNKS + NT - 1) / NT, B_PER_T = (B_CHUNKS + NT - 1) / NT;
-    static constexpr int LDS_A = BM * A_STRIDE, LDS_B = BNB * B_STRIDE;
-    static constexpr int LDS_BYTES = 2 * (LDS_A + LDS_B) * 2;
-    static_assert(WTM % 16 == 0 && WTN % 16 == 0, "wave tile must hold whole MFMA blocks");
-    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
-};
-
-// expansion tiles (A = x rows, 64 K per stage)
-using ExpL = Cfg<256, 256, 2, 4, 64>;
-using ExpM = Cfg<128, 128, 2, 2, 64>;
-using ExpS = Cfg<16, 256, 1, 4, 64>;
-// projection tiles (A = split z rows: 64 hi + 64 lo per stage)
-using DownL = Cfg<128, 256, 2, 4, 128>;
-using DownM = Cfg<64, 128, 1, 4, 128>;
-using DownS = Cfg<16, 128, 1, 4, 128>;
+// s_waitcnt immediates (gfx9 encoding: vmcnt[3:0]+[15:14], expcnt[6:4], lgkmcnt[11:8])
+constexpr int waitcnt_imm(int vm, int lgkm) {
+    return (vm & 0xF) | (7 << 4) | ((lgkm & 0xF) << 8) | (((vm >> 4) & 3) << 14);
+}
+constexpr int kNoVm = 63, kNoLgkm = 15;
 
 // Find this workgroup's group and row range. Returns false past the last tile.
 template <int BM>
@@ -108,149 +93,74 @@ __device__ bool find_tile(const int32_t* __restrict__ offsets, int n, int64_t a_
     return s_tile[0] >= 0;
 }
 
+// Tile of workgroup `bid` in a grid of `grid` (a multiple of 8) workgroups.
+// Workgroups are dispatched round-robin over the 8 XCDs (bid % 8), so ids are first
+// remapped to make each XCD's share a contiguous run. That run is walked in groups of GN
+// N-tiles: inside a group the M-tile varies slowest, so the workgroups resident on one XCD
+// at a time share a few weight tiles (same expert, neighbouring M-tiles) and a few
+// activation tiles (same M-tile, neighbouring N-tiles) through that XCD's L2.
+__device__ inline bool tile_of(int64_t bid, int64_t grid, int64_t mt_upper, int nt, int GN,
+                               int64_t* mt, int* ntile) {
+    const int64_t id = (bid % 8) * (grid / 8) + bid / 8;
+    if (id >= mt_upper * nt) return false;
+    const int64_t gsize = (int64_t)GN * mt_upper;
+    const int64_t grp = id / gsize, in = id % gsize;
+    const int64_t gn = min<int64_t>(GN, nt - grp * GN);
+    *mt = in / gn;
+    *ntile = (int)(grp * GN + in % gn);
+    return true;
+}
+
 __device__ inline uint32_t pack_bf16x2(float a, float b) {
     return (uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16);
 }
 
-template <class C, int MODE>
-__global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt_upper) {
-    extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-    __shared__ int s_tile[3];
-    constexpr bool kSplitA = C::AK == 2 * BK;
-    static_assert(MODE == kExpand ? !kSplitA : kSplitA, "expand reads x, down reads split z");
-    const int64_t mt = blockIdx.x % mt_upper;
-    const int ntile = (int)(blockIdx.x / mt_upper);
-    if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
-    const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / C::WN, wn = wave % C::WN;
-    const int K = g.K, N = g.N;
-    const int64_t a_row_elems = kSplitA ? 2 * (int64_t)K : K;      // bf16 elements per A row
-    constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;  // output columns per tile
-
-    // Global source of each 16-byte chunk this thread stages.
-    const uint16_t* aptr[C::A_PER_T];
-    const uint16_t* bptr[C::B_PER_T];
-    const uint16_t* A = (const uint16_t*)g.a;
-#pragma unroll
-    for (int i = 0; i < C::A_PER_T; ++i) {
-        const int c = tid + i * C::NT;
-        const int row = c / C::A_CPR, kc = c % C::A_CPR;
-        const int r = row0 + row;
-        aptr[i] = nullptr;
-        if (c < C::A_CHUNKS && r < row1) {
-            int64_t src = r;
-            if (g.gather) {
-                src = g.gather[r];
-                src = src < 0 ? 0 : (src >= g.a_rows ? g.a_rows - 1 : src);
-            }
-            aptr[i] = A + src * a_row_elems + kc * 8;
-        }
+// Source row of A row r of the tile (rows past row1 repeat a valid row; their outputs are
+// never stored).
+__device__ inline int64_t a_source_row(const GemmArgs& g, int r, int row1) {
+    if (r >= row1) r = row1 - 1;
+    int64_t src = r;
+    if (g.gather) {
+        src = g.gather[r];
+        src = src < 0 ? 0 : (src >= g.a_rows ? g.a_rows - 1 : src);
     }
-#pragma unroll
-    for (int i = 0; i < C::B_PER_T; ++i) {
-        const int c = tid + i * C::NT;
-        const int j = c / C::B_CPR, kc = c % C::B_CPR;
-        bptr[i] = nullptr;
-        if (c < C::B_CHUNKS) {
-            if (MODE == kExpand) {
-                const int grp = j / C::WTN, jj = j % C::WTN, half = jj / (C::WTN / 2);
-                const int f = ntile * kOutCols + grp * (C::WTN / 2) + jj % (C::WTN / 2);
-                if (f < N)
-                    bptr[i] = (const uint16_t*)(half ? g.b1 : g.b0) + ((int64_t)e * N + f) * K + kc * 8;
-            } else {
-                const int h = ntile * kOutCols + j;
-                if (h < N) bptr[i] = (const uint16_t*)g.b0 + ((int64_t)e * N + h) * K + kc * 8;
-            }
-        }
+    return src;
+}
+
+// Weight row (element offset of its K = 0) of B row j of the tile; rows past N repeat row
+// N - 1 (their outputs are never stored).
+template <int MODE, int WTN, int OUT_COLS>
+__device__ inline const uint16_t* b_source_row(const GemmArgs& g, int e, int ntile, int j) {
+    if (MODE == kExpand) {
+        const int grp = j / WTN, jj = j % WTN, half = jj / (WTN / 2);
+        int f = ntile * OUT_COLS + grp * (WTN / 2) + jj % (WTN / 2);
+        f = f < g.N ? f : g.N - 1;
+        return (const uint16_t*)(half ? g.b1 : g.b0) + ((int64_t)e * g.N + f) * g.K;
     }
+    int h = ntile * OUT_COLS + j;
+    h = h < g.N ? h : g.N - 1;
+    return (const uint16_t*)g.b0 + ((int64_t)e * g.N + h) * g.K;
+}
 
-    uint4 ra[C::A_PER_T], rb[C::B_PER_T];
-    auto gload = [&](int kt) {
+// Shared epilogue: acc[nb][mb] holds C[row = .. + (lane & 15)][cols c0 .. c0+3].
+template <int MODE, int MB, int NBK, int WTM, int WTN, int OUT_COLS>
+__device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB], int row0,
+                                int row1, int ntile, int wm, int wn, int lane) {
+    const int N = g.N;
 #pragma unroll
-        for (int i = 0; i < C::A_PER_T; ++i)
-            ra[i] = aptr[i] ? *(const uint4*)(aptr[i] + (int64_t)kt * C::AK) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < C::B_PER_T; ++i)
-            rb[i] = bptr[i] ? *(const uint4*)(bptr[i] + (int64_t)kt * BK) : make_uint4(0, 0, 0, 0);
-    };
-    auto lstore = [&](int buf) {
-        uint16_t* As = lds + buf * (C::LDS_A + C::LDS_B);
-        uint16_t* Bs = As + C::LDS_A;
-#pragma unroll
-        for (int i = 0; i < C::A_PER_T; ++i) {
-            const int c = tid + i * C::NT;
-            if (c < C::A_CHUNKS) *(uint4*)(As + (c / C::A_CPR) * C::A_STRIDE + (c % C::A_CPR) * 8) = ra[i];
-        }
-#pragma unroll
-        for (int i = 0; i < C::B_PER_T; ++i) {
-            const int c = tid + i * C::NT;
-            if (c < C::B_CHUNKS) *(uint4*)(Bs + (c / C::B_CPR) * C::B_STRIDE + (c % C::B_CPR) * 8) = rb[i];
-        }
-    };
-
-    floatx4 acc[C::NBK][C::MB];
-#pragma unroll
-    for (int nb = 0; nb < C::NBK; ++nb)
-#pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    const int KT = K / BK;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < KT) gload(kt + 1);
-        const uint16_t* As = lds + cur * (C::LDS_A + C::LDS_B);
-        const uint16_t* Bs = As + C::LDS_A;
-#pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            bf16x8 bfr[C::NBK], afr[C::MB];
-            const int koff = ks * 32 + (lane >> 4) * 8;
-#pragma unroll
-            for (int nb = 0; nb < C::NBK; ++nb)
-                bfr[nb] = *(const bf16x8*)(Bs + (wn * C::WTN + nb * 16 + (lane & 15)) * C::B_STRIDE + koff);
-#pragma unroll
-            for (int mb = 0; mb < C::MB; ++mb)
-                afr[mb] = *(const bf16x8*)(As + (wm * C::WTM + mb * 16 + (lane & 15)) * C::A_STRIDE + koff);
-#pragma unroll
-            for (int nb = 0; nb < C::NBK; ++nb)
-#pragma unroll
-                for (int mb = 0; mb < C::MB; ++mb)
-                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
-            if (kSplitA) {  // the low halves, same weight fragments
-#pragma unroll
-                for (int mb = 0; mb < C::MB; ++mb)
-                    afr[mb] = *(const bf16x8*)(As + (wm * C::WTM + mb * 16 + (lane & 15)) * C::A_STRIDE + BK + koff);
-#pragma unroll
-                for (int nb = 0; nb < C::NBK; ++nb)
-#pragma unroll
-                    for (int mb = 0; mb < C::MB; ++mb)
-                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
-            }
-        }
-        if (kt + 1 < KT) lstore(cur ^ 1);
-        __syncthreads();
-    }
-
-    // Epilogue: lane holds columns c0..c0+3 of row (lane & 15) of each 16x16 block.
-#pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb) {
-        const int r = row0 + wm * C::WTM + mb * 16 + (lane & 15);
+    for (int mb = 0; mb < MB; ++mb) {
+        const int r = row0 + wm * WTM + mb * 16 + (lane & 15);
         if (r >= row1) continue;
         if (MODE == kExpand) {
 #pragma unroll
-            for (int nb = 0; nb < C::NBK / 2; ++nb) {
-                const int f = ntile * kOutCols + wn * (C::WTN / 2) + nb * 16 + (lane >> 4) * 4;
+            for (int nb = 0; nb < NBK / 2; ++nb) {
+                const int f = ntile * OUT_COLS + wn * (WTN / 2) + nb * 16 + (lane >> 4) * 4;
                 if (f >= N) continue;
-                const floatx4 gt = acc[nb][mb], up = acc[nb + C::NBK / 2][mb];
+                const floatx4 gt = acc[nb][mb], up = acc[nb + NBK / 2][mb];
                 float v[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) v[i] = gt[i] / (1.0f + __expf(-gt[i])) * up[i];
                 if (g.split_out) {
-                    // hi at [blk][0..63], lo at [blk][64..127] of the row's split layout
                     uint16_t* U = (uint16_t*)g.out + (int64_t)r * 2 * N + (f / kSplitBlock) * 2 * kSplitBlock
                                   + f % kSplitBlock;
                     float lo[4];
@@ -265,8 +175,8 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
         } else {
             float* O = (float*)g.out;
 #pragma unroll
-            for (int nb = 0; nb < C::NBK; ++nb) {
-                const int h = ntile * kOutCols + wn * C::WTN + nb * 16 + (lane >> 4) * 4;
+            for (int nb = 0; nb < NBK; ++nb) {
+                const int h = ntile * OUT_COLS + wn * WTN + nb * 16 + (lane >> 4) * 4;
                 if (h >= N) continue;
                 float4 v = make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
                 float4* dst = (float4*)(O + (int64_t)r * N + h);
@@ -280,21 +190,331 @@ __global__ __launch_bounds__(C::NT) void gemm_bf16_kernel(GemmArgs g, int64_t mt
     }
 }
 
+// ------------------------------------------------------------------ dma kernel
+template <int BM_, int BNB_, int WM_, int WN_, bool SPLIT_, int NS_>
+struct DCfg {
+    static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_, NS = NS_;
+    static constexpr bool SPLIT = SPLIT_;
+    static constexpr int NW = WM * WN, NT = NW * 64;
+    static constexpr int WTM = BM / WM, WTN = BNB / WN, MB = WTM / 16, NBK = WTN / 16;
+    static constexpr int A_ROWS = BM * (SPLIT ? 2 : 1);    // LDS rows of A (hi rows, then lo rows)
+    static constexpr int A_INSTR = A_ROWS / 16, B_INSTR = BNB / 16;  // 1 KB wave loads per stage
+    static constexpr int QA = A_INSTR / NW, QB = B_INSTR / NW, LPW = QA + QB;
+    static constexpr int STAGE = (A_ROWS + BNB) * 64;     // bytes
+    static constexpr int LDS_BYTES = NS * STAGE;
+    static_assert(A_INSTR % NW == 0 && B_INSTR % NW == 0, "every wave issues the same loads");
+    static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+    static_assert(NS >= 2 && (NS - 2) * LPW <= 63, "vmcnt range");
+};
+
+using ExpDma = DCfg<256, 256, 2, 4, false, 4>;
+using DownDma = DCfg<128, 256, 2, 4, true, 4>;
+
 template <class C, int MODE>
+__global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_upper, int nt,
+                                                         int group_n) {
+    extern __shared__ __attribute__((aligned(1024))) char lds[];
+    __shared__ int s_tile[3];
+    static_assert(MODE == kExpand ? !C::SPLIT : C::SPLIT, "expand reads x, down reads split z");
+    int64_t mt;
+    int ntile;
+    if (!tile_of(blockIdx.x, gridDim.x, mt_upper, nt, group_n, &mt, &ntile)) return;
+    if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
+    const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / C::WN, wn = wave % C::WN;
+    const int K = g.K;
+    constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
+
+    // Source of this lane's 16 bytes in each of the wave's LPW loads per stage, and the
+    // byte step per K step. Load q covers LDS rows [blk*16, blk*16 + 16) of A (q < QA) or B.
+    const char* src[C::LPW];
+    int64_t step[C::LPW];
+    int dst[C::LPW];
+    const int lrow = lane >> 2;                           // row within the 16-row block
+    const int chunk = (lane & 3) ^ ((lrow >> 1) & 3);     // logical 16-byte chunk it fetches
+#pragma unroll
+    for (int q = 0; q < C::LPW; ++q) {
+        if (q < C::QA) {
+            const int blk = q * C::NW + wave, lr = blk * 16 + lrow;
+            const int part = lr / C::BM, tr = lr % C::BM;  // part 1: low halves of split z
+            const int64_t srow = a_source_row(g, row0 + tr, row1);
+            if (C::SPLIT) {
+                src[q] = (const char*)g.a + srow * (int64_t)K * 4 + part * 64 + chunk * 16;
+                step[q] = 128;
+            } else {
+                src[q] = (const char*)g.a + srow * (int64_t)K * 2 + chunk * 16;
+                step[q] = 64;
+            }
+            dst[q] = blk * 1024;
+        } else {
+            const int blk = (q - C::QA) * C::NW + wave, lb = blk * 16 + lrow;
+            src[q] = (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, lb) + chunk * 16;
+            step[q] = 64;
+            dst[q] = C::A_ROWS * 64 + blk * 1024;
+        }
+    }
+    auto issue = [&](int kt) {
+        char* base = lds + (kt % C::NS) * C::STAGE;
+#pragma unroll
+        for (int q = 0; q < C::LPW; ++q)
+            __builtin_amdgcn_global_load_lds((const void*)(src[q] + kt * step[q]),
+                                             (PCM_LDS void*)(base + dst[q]), 16, 0, 0);
+    };
+
+    floatx4 acc[C::NBK][C::MB];
+#pragma unroll
+    for (int nb = 0; nb < C::NBK; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    const int KT_ = K / 32;
+    // Fragment addressing: row (lane & 15) of a 16-row block, logical chunk (lane >> 4).
+    const int frag_off = (lane & 15) * 64 + (((lane >> 4) ^ (((lane & 15) >> 1) & 3)) * 16);
+    bf16x8 bfr[C::NBK], afr[C::MB], alo[C::SPLIT ? C::MB : 1];
+    auto read_frags = [&](int kt) {
+        const char* S = lds + (kt % C::NS) * C::STAGE;
+#pragma unroll
+        for (int nb = 0; nb < C::NBK; ++nb)
+            bfr[nb] = *(const bf16x8*)(S + (C::A_ROWS + wn * C::WTN + nb * 16) * 64 + frag_off);
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb)
+            afr[mb] = *(const bf16x8*)(S + (wm * C::WTM + mb * 16) * 64 + frag_off);
+        if (C::SPLIT) {
+#pragma unroll
+            for (int mb = 0; mb < C::MB; ++mb)
+                alo[mb] = *(const bf16x8*)(S + (C::BM + wm * C::WTM + mb * 16) * 64 + frag_off);
+        }
+    };
+    auto mfmas = [&]() {
+#pragma unroll
+        for (int nb = 0; nb < C::NBK; ++nb)
+#pragma unroll
+            for (int mb = 0; mb < C::MB; ++mb)
+                acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
+        if (C::SPLIT) {
+#pragma unroll
+            for (int nb = 0; nb < C::NBK; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < C::MB; ++mb)
+                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], alo[mb], acc[nb][mb], 0, 0, 0);
+        }
+    };
+    // barrier that the compiler may not move memory accesses or other instructions across
+    auto barrier = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // this wave's loads of step kt+1 have landed (later steps may still be in flight)
+    auto wait_next_stage = [&](int kt, bool lds_too) {
+        if (kt + C::NS - 1 < KT_) {
+            if (lds_too) __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, 0));
+            else __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, kNoLgkm));
+        } else {
+            if (lds_too) __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+            else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, kNoLgkm));
+        }
+    };
+
+    // Ping-pong: waves 0..NW/2-1 (group 0) and NW/2..NW-1 (group 1) hold one wave per SIMD
+    // each and run half a step apart. Between two barriers one group issues its LDS
+    // fragment reads and the global->LDS loads of step kt+NS-1 ("M" phase) while the
+    // other issues the MFMAs of its previous step ("C" phase), so every SIMD alternates
+    // between its two waves' MFMA streams. Each step is read by group 0 in interval 2kt
+    // and by group 1 in interval 2kt+1; the stage it lived in is refilled only after both
+    // groups have finished reading it (each wave drains its LDS reads before the barrier
+    // that ends its M phase).
+    const bool g1 = wave >= C::NW / 2;
+#pragma unroll
+    for (int s = 0; s < C::NS - 1; ++s)
+        if (s < KT_) issue(s);
+    if (C::NS - 2 < KT_) __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, kNoLgkm));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, kNoLgkm));
+    barrier();                 // step 0 is in LDS for everyone
+    if (g1) barrier();         // group 1 starts half a step later
+    for (int kt = 0; kt < KT_; ++kt) {
+        // M phase
+        if (kt + C::NS - 1 < KT_) issue(kt + C::NS - 1);  // into the stage of step kt-1
+        read_frags(kt);
+        if (g1) wait_next_stage(kt, true);              // group 0 reads step kt+1 next
+        else __builtin_amdgcn_s_waitcnt(waitcnt_imm(kNoVm, 0));
+        barrier();
+        // C phase
+        mfmas();
+        if (!g1) wait_next_stage(kt, false);            // own step kt+1 before reading it
+        barrier();
+    }
+    if (!g1) barrier();        // both groups pass the same number of barriers
+    epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(g, acc, row0, row1, ntile, wm, wn, lane);
+}
+
+// --------------------------------------------------------------- staged kernel
+template <int BM_, int BNB_, int WM_, int WN_, bool SPLIT_>
+struct SCfg {
+    static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_;
+    static constexpr bool SPLIT = SPLIT_;
+    static constexpr int NT = WM * WN * 64;
+    static constexpr int WTM = BM / WM, WTN = BNB / WN, MB = WTM / 16, NBK = WTN / 16;
+    static constexpr int A_ROWS = BM * (SPLIT ? 2 : 1);   // 128-byte LDS rows: 64 K values
+    static constexpr int A_CHUNKS = A_ROWS * 8, B_CHUNKS = BNB * 8;
+    static constexpr int A_PER_T = (A_CHUNKS + NT - 1) / NT, B_PER_T = (B_CHUNKS + NT - 1) / NT;
+    static constexpr int STAGE = (A_ROWS + BNB) * 128;
+    static constexpr int LDS_BYTES = 2 * STAGE;
+    static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+};
+
+using ExpM = SCfg<128, 128, 2, 2, false>;
+using ExpS = SCfg<16, 256, 1, 4, false>;
+using DownM = SCfg<64, 128, 1, 4, true>;
+using DownS = SCfg<16, 128, 1, 4, true>;
+
+template <class C, int MODE>
+__global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t mt_upper, int nt,
+                                                            int group_n) {
+    extern __shared__ __attribute__((aligned(1024))) char lds[];
+    __shared__ int s_tile[3];
+    static_assert(MODE == kExpand ? !C::SPLIT : C::SPLIT, "expand reads x, down reads split z");
+    int64_t mt;
+    int ntile;
+    if (!tile_of(blockIdx.x, gridDim.x, mt_upper, nt, group_n, &mt, &ntile)) return;
+    if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
+    const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / C::WN, wn = wave % C::WN;
+    const int K = g.K;
+    constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
+
+    // chunk i of a stage: LDS row i / 8, logical chunk i % 8 (16 bytes), stored at position
+    // (i % 8) ^ ((row >> 1) & 7)
+    const char* aptr[C::A_PER_T];
+    const char* bptr[C::B_PER_T];
+#pragma unroll
+    for (int i = 0; i < C::A_PER_T; ++i) {
+        const int c = tid + i * C::NT, lr = c / 8, kc = c % 8;
+        aptr[i] = nullptr;
+        if (c < C::A_CHUNKS) {
+            const int part = lr / C::BM, tr = lr % C::BM;
+            const int64_t srow = a_source_row(g, row0 + tr, row1);
+            // split z: a 64-wide step is blocks [hi32|lo32][hi32|lo32]; part 0 takes the hi
+            // halves (chunks 0-3 of each block), part 1 the lo halves
+            aptr[i] = C::SPLIT ? (const char*)g.a + srow * (int64_t)K * 4 + (kc / 4) * 128 + part * 64 + (kc % 4) * 16
+                               : (const char*)g.a + srow * (int64_t)K * 2 + kc * 16;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < C::B_PER_T; ++i) {
+        const int c = tid + i * C::NT, j = c / 8, kc = c % 8;
+        bptr[i] = c < C::B_CHUNKS
+                      ? (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, j) + kc * 16
+                      : nullptr;
+    }
+    const int a_step = C::SPLIT ? 256 : 128;
+
+    uint4 ra[C::A_PER_T], rb[C::B_PER_T];
+    auto gload = [&](int kt) {
+#pragma unroll
+        for (int i = 0; i < C::A_PER_T; ++i)
+            if (aptr[i]) ra[i] = *(const uint4*)(aptr[i] + (int64_t)kt * a_step);
+#pragma unroll
+        for (int i = 0; i < C::B_PER_T; ++i)
+            if (bptr[i]) rb[i] = *(const uint4*)(bptr[i] + (int64_t)kt * 128);
+    };
+    auto lstore = [&](int buf) {
+        char* S = lds + buf * C::STAGE;
+#pragma unroll
+        for (int i = 0; i < C::A_PER_T; ++i) {
+            const int c = tid + i * C::NT, lr = c / 8, kc = c % 8;
+            if (c < C::A_CHUNKS) *(uint4*)(S + lr * 128 + ((kc ^ ((lr >> 1) & 7)) * 16)) = ra[i];
+        }
+#pragma unroll
+        for (int i = 0; i < C::B_PER_T; ++i) {
+            const int c = tid + i * C::NT, j = c / 8, kc = c % 8;
+            if (c < C::B_CHUNKS) *(uint4*)(S + (C::A_ROWS + j) * 128 + ((kc ^ ((j >> 1) & 7)) * 16)) = rb[i];
+        }
+    };
+
+    floatx4 acc[C::NBK][C::MB];
+#pragma unroll
+    for (int nb = 0; nb < C::NBK; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    const int KT = K / 64;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < KT; ++kt) {
+        const int cur = kt & 1;
+        if (kt + 1 < KT) gload(kt + 1);
+        const char* S = lds + cur * C::STAGE;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int ck = ks * 4 + (lane >> 4);
+            const int off = (lane & 15) * 128 + ((ck ^ (((lane & 15) >> 1) & 7)) * 16);
+            bf16x8 bfr[C::NBK], afr[C::MB];
+#pragma unroll
+            for (int nb = 0; nb < C::NBK; ++nb)
+                bfr[nb] = *(const bf16x8*)(S + (C::A_ROWS + wn * C::WTN + nb * 16) * 128 + off);
+#pragma unroll
+            for (int mb = 0; mb < C::MB; ++mb)
+                afr[mb] = *(const bf16x8*)(S + (wm * C::WTM + mb * 16) * 128 + off);
+#pragma unroll
+            for (int nb = 0; nb < C::NBK; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < C::MB; ++mb)
+                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
+            if (C::SPLIT) {
+#pragma unroll
+                for (int mb = 0; mb < C::MB; ++mb)
+                    afr[mb] = *(const bf16x8*)(S + (C::BM + wm * C::WTM + mb * 16) * 128 + off);
+#pragma unroll
+                for (int nb = 0; nb < C::NBK; ++nb)
+#pragma unroll
+                    for (int mb = 0; mb < C::MB; ++mb)
+                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
+            }
+        }
+        if (kt + 1 < KT) lstore(cur ^ 1);
+        __syncthreads();
+    }
+    epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(g, acc, row0, row1, ntile, wm, wn, lane);
+}
+
+// ---------------------------------------------------------------------- launch
+template <class C, int MODE, bool DMA>
 hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
+    const void* fn;
+    if constexpr (DMA)
+        fn = (const void*)gemm_dma_kernel<C, MODE>;
+    else
+        fn = (const void*)gemm_staged_kernel<C, MODE>;
     static bool attr_set = false;  // idempotent; a race only repeats the same call
     if (!attr_set) {
-        hipError_t err = hipFuncSetAttribute((const void*)gemm_bf16_kernel<C, MODE>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+        hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
         if (err != hipSuccess) return err;
         attr_set = true;
     }
     const int64_t mt_upper = g.offsets ? ceil_div(R, C::BM) + g.n : ceil_div(R, C::BM);
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
-    const int64_t nt = ceil_div(g.N, kOutCols);
-    const int64_t grid = mt_upper * nt;
-    if (grid <= 0) return hipSuccess;
-    gemm_bf16_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper);
+    const int nt = (int)ceil_div(g.N, kOutCols);
+    const int64_t grid = ceil_div(mt_upper * nt, 8) * 8;
+    if (mt_upper * nt <= 0) return hipSuccess;
+    static const int group_n = [] {
+        const char* env = getenv("PCM_GEMM_GROUP_N");
+        const int v = env ? atoi(env) : 4;
+        return v > 0 ? v : 4;
+    }();
+    if constexpr (DMA)
+        gemm_dma_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
+    else
+        gemm_staged_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
     return hipGetLastError();
 }
 
@@ -314,18 +534,18 @@ char pick_tile(int64_t R, int groups) {
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s) {
     const char t = pick_tile(R, g.offsets ? g.n : 1);
     if (mode == kExpand) {
-        if (t == 'S') return launch_cfg<ExpS, kExpand>(g, R, s);
-        if (t == 'M') return launch_cfg<ExpM, kExpand>(g, R, s);
-        return launch_cfg<ExpL, kExpand>(g, R, s);
+        if (t == 'S') return launch_cfg<ExpS, kExpand, false>(g, R, s);
+        if (t == 'M') return launch_cfg<ExpM, kExpand, false>(g, R, s);
+        return launch_cfg<ExpDma, kExpand, true>(g, R, s);
     }
     if (mode == kDownStore) {
-        if (t == 'S') return launch_cfg<DownS, kDownStore>(g, R, s);
-        if (t == 'M') return launch_cfg<DownM, kDownStore>(g, R, s);
-        return launch_cfg<DownL, kDownStore>(g, R, s);
+        if (t == 'S') return launch_cfg<DownS, kDownStore, false>(g, R, s);
+        if (t == 'M') return launch_cfg<DownM, kDownStore, false>(g, R, s);
+        return launch_cfg<DownDma, kDownStore, true>(g, R, s);
     }
-    if (t == 'S') return launch_cfg<DownS, kDownAccum>(g, R, s);
-    if (t == 'M') return launch_cfg<DownM, kDownAccum>(g, R, s);
-    return launch_cfg<DownL, kDownAccum>(g, R, s);
+    if (t == 'S') return launch_cfg<DownS, kDownAccum, false>(g, R, s);
+    if (t == 'M') return launch_cfg<DownM, kDownAccum, false>(g, R, s);
+    return launch_cfg<DownDma, kDownAccum, true>(g, R, s);
 }
 
 }  // namespace pcm

@@ -37,10 +37,11 @@ enum GemmMode { kExpand = 0, kDownStore = 1, kDownAccum = 2 };
 
 // Layout of a bf16 layer's projection input z (and of a dense FFN's SwiGLU output): a
 // float32 value v is carried as the bfloat16 pair hi = rn(v), lo = rn(v - hi), which
-// represents v to about 2^-17 relative. Row r holds F/64 blocks of [64 hi | 64 lo].
+// represents v to about 2^-17 relative. Row r holds F/32 blocks of [32 hi | 32 lo], so one
+// 32-wide K step of the down GEMM reads 128 contiguous bytes of a row.
 // The down GEMM multiplies both halves by the same weight tile, so the projection sees
 // the float32 value instead of a single bfloat16 rounding of it.
-constexpr int kSplitBlock = 64;
+constexpr int kSplitBlock = 32;
 
 struct GemmArgs {
     const void* a;              // expand: x [T,H] (rows gathered); down: z (split bf16 or f32)
