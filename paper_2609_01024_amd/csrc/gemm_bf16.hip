@@ -204,12 +204,17 @@ struct DCfg {
     static constexpr int LDS_BYTES = NS * STAGE;
     static_assert(A_INSTR % NW == 0 && B_INSTR % NW == 0, "every wave issues the same loads");
     static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
-    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+    static_assert(LDS_BYTES <= 160 * 1024 - 64, "LDS budget");
     static_assert(NS >= 2 && (NS - 2) * LPW <= 63, "vmcnt range");
+    static_assert(NW % 2 == 0, "two ping-pong groups");
 };
 
 using ExpDma = DCfg<256, 256, 2, 4, false, 4>;
 using DownDma = DCfg<128, 256, 2, 4, true, 4>;
+// few rows per group (decode): weight streaming with 6 stages in flight; one M tile
+// covers a group's rows, the unused MFMA rows cost nothing when HBM is the bound
+using ExpStream = DCfg<64, 256, 1, 4, false, 6>;
+using DownStream = DCfg<64, 256, 1, 4, true, 6>;
 
 template <class C, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_upper, int nt,
@@ -370,9 +375,7 @@ struct SCfg {
 };
 
 using ExpM = SCfg<128, 128, 2, 2, false>;
-using ExpS = SCfg<16, 256, 1, 4, false>;
 using DownM = SCfg<64, 128, 1, 4, true>;
-using DownS = SCfg<16, 128, 1, 4, true>;
 
 template <class C, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t mt_upper, int nt,
@@ -534,16 +537,16 @@ char pick_tile(int64_t R, int groups) {
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s) {
     const char t = pick_tile(R, g.offsets ? g.n : 1);
     if (mode == kExpand) {
-        if (t == 'S') return launch_cfg<ExpS, kExpand, false>(g, R, s);
+        if (t == 'S') return launch_cfg<ExpStream, kExpand, true>(g, R, s);
         if (t == 'M') return launch_cfg<ExpM, kExpand, false>(g, R, s);
         return launch_cfg<ExpDma, kExpand, true>(g, R, s);
     }
     if (mode == kDownStore) {
-        if (t == 'S') return launch_cfg<DownS, kDownStore, false>(g, R, s);
+        if (t == 'S') return launch_cfg<DownStream, kDownStore, true>(g, R, s);
         if (t == 'M') return launch_cfg<DownM, kDownStore, false>(g, R, s);
         return launch_cfg<DownDma, kDownStore, true>(g, R, s);
     }
-    if (t == 'S') return launch_cfg<DownS, kDownAccum, false>(g, R, s);
+    if (t == 'S') return launch_cfg<DownStream, kDownAccum, true>(g, R, s);
     if (t == 'M') return launch_cfg<DownM, kDownAccum, false>(g, R, s);
     return launch_cfg<DownDma, kDownAccum, true>(g, R, s);
 }
