@@ -49,8 +49,11 @@ typedef enum pcm_status {
 
 typedef enum pcm_dtype {
     PCM_F32 = 0,   /* x and weights float32; FMA on the vector ALUs */
-    PCM_BF16 = 1   /* x and weights bfloat16; bf16 MFMA with float32 accumulate; the
-                      intermediates u and z are kept at float32 accuracy */
+    PCM_BF16 = 1   /* x and weights bfloat16; float32 accumulate throughout. The expansion
+                      runs on bf16 MFMA and keeps u in float32; the projection input z is
+                      carried as row-scaled float16 (11 significant bits) and the bf16
+                      projection weights are widened to float16 in registers (exact in
+                      float16's normal range), so the projection runs on f16 MFMA */
 } pcm_dtype;
 
 /* Path weights beta_ab for (a, b) in Pi (p = the renormalised router weights).
@@ -116,9 +119,9 @@ pcm_status pcm_expand(pcm_dtype dtype, const void* x, const void* w_gate, const 
  * z_(t,b) = sum_{a : (a,b) in Pi} beta_ab u_(t,a)   (float32),
  * o_(t,b) = W_down[e_b] z_(t,b)                     (float32 accumulate),
  * y_t = [y_t if accumulate] + sum_{b ascending} o_(t,b).
- * For bf16 layers z enters the bf16 MFMA as a pair of bfloat16 values (hi = z rounded,
- * lo = the rounding error rounded), both multiplied by the same weight tile, so the
- * projection sees z to about 2^-17 relative instead of one bfloat16 rounding.
+ * For bf16 layers each z row is multiplied by a power of two that puts its largest
+ * element just below 2^14 and stored as float16; the down GEMM multiplies its output row
+ * by the inverse (exact), so any activation magnitude stays inside float16's range.
  * u [T*k,F] f32 from pcm_expand, w_down [n,H,F] of `dtype`, y [T,H] f32 (device).
  * ws: pcm_workspace_bytes(PCM_OP_PROJECT_COMBINE, ...) bytes (holds z and o). */
 pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_down,
@@ -129,7 +132,8 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
 /* A dense SwiGLU FFN applied to every token with weight 1 (Section 2's expert F_e), for an
  * always-on shared expert that sits beside the routed experts and outside the path
  * space: y_t = [y_t if accumulate] + W_down (SiLU(W_gate x_t) * (W_up x_t)).
- * The SwiGLU output is kept at float32 accuracy (bf16 layers: as a hi/lo bfloat16 pair).
+ * The SwiGLU output is kept in float32 and, for bf16 layers, enters the down projection
+ * as row-scaled float16 like pcm_project_combine's z.
  * x [T,H], w_gate/w_up [Fs,H], w_down [H,Fs] of `dtype`; y [T,H] f32 (device).
  * ws: pcm_workspace_bytes(PCM_OP_DENSE_SWIGLU, T, H, Fs, 1, 1, dtype) bytes. */
 pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate,

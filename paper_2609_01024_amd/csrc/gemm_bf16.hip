@@ -3,11 +3,12 @@
 //   expand:  U[r, f] = SiLU(x[tok(r)] . W_gate[e][f]) * (x[tok(r)] . W_up[e][f])
 //            one row per (token, source) pair, rows of expert e contiguous (Section 4.3),
 //            x rows gathered through row_token; SwiGLU fused into the epilogue; U kept in
-//            float32 (or written as split hi/lo bf16 pairs for a dense FFN).
-//   down:    O[r, h] = Z[r] . W_down[e][h]        (store, or accumulate into y for a
-//                                                  dense FFN whose rows are tokens)
-//            Z arrives as split hi/lo bf16 pairs; each weight fragment is multiplied by
-//            both halves, so the product sees Z to ~2^-17 relative.
+//            float32. bf16 x bf16 MFMA (v_mfma_f32_16x16x32_bf16).
+//   down:    O[r, h] = row_scale[r] * (Z[r] . W_down[e][h])   (store, or accumulate into y
+//                                                  for a dense FFN whose rows are tokens)
+//            Z arrives as row-scaled float16; each bf16 W_down fragment is widened to
+//            float16 in registers after its LDS read (exact in float16's normal range), and
+//            the product runs on v_mfma_f32_16x16x32_f16 at the same rate.
 // Both operands are K-contiguous (x rows and W rows run along H; Z rows and W_down rows
 // along F), so a lane's 8 consecutive K values of a row are one 16-byte load.
 //
@@ -29,6 +30,8 @@
 // of per-group tile counts; workgroups past the last tile exit.
 #include <stdlib.h>
 #include <string.h>
+
+#include <type_traits>
 
 #include "internal.h"
 
@@ -111,10 +114,6 @@ __device__ inline bool tile_of(int64_t bid, int64_t grid, int64_t mt_upper, int 
     return true;
 }
 
-__device__ inline uint32_t pack_bf16x2(float a, float b) {
-    return (uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16);
-}
-
 // Source row of A row r of the tile (rows past row1 repeat a valid row; their outputs are
 // never stored).
 __device__ inline int64_t a_source_row(const GemmArgs& g, int r, int row1) {
@@ -160,25 +159,17 @@ __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB]
                 float v[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) v[i] = gt[i] / (1.0f + __expf(-gt[i])) * up[i];
-                if (g.split_out) {
-                    uint16_t* U = (uint16_t*)g.out + (int64_t)r * 2 * N + (f / kSplitBlock) * 2 * kSplitBlock
-                                  + f % kSplitBlock;
-                    float lo[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) lo[i] = v[i] - bf16_bits_to_f32(f32_to_bf16_rne(v[i]));
-                    *(uint2*)U = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-                    *(uint2*)(U + kSplitBlock) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
-                } else {
-                    *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
-                }
+                *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
             }
         } else {
             float* O = (float*)g.out;
+            const float sc = g.row_scale ? g.row_scale[r] : 1.0f;
 #pragma unroll
             for (int nb = 0; nb < NBK; ++nb) {
                 const int h = ntile * OUT_COLS + wn * WTN + nb * 16 + (lane >> 4) * 4;
                 if (h >= N) continue;
-                float4 v = make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
+                float4 v = make_float4(acc[nb][mb][0] * sc, acc[nb][mb][1] * sc, acc[nb][mb][2] * sc,
+                                       acc[nb][mb][3] * sc);
                 float4* dst = (float4*)(O + (int64_t)r * N + h);
                 if (MODE == kDownAccum && g.accumulate) {
                     const float4 o = *dst;
@@ -190,14 +181,45 @@ __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB]
     }
 }
 
+// bfloat16 -> float16, 8 lanes of a fragment (exact for |w| in float16's normal range)
+__device__ inline halfx8 widen_to_f16(const bf16x8& v) {
+    const uint4 q = __builtin_bit_cast(uint4, v);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    halfx8 h;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        h[2 * i] = (_Float16)__uint_as_float(w[i] << 16);
+        h[2 * i + 1] = (_Float16)__uint_as_float(w[i] & 0xFFFF0000u);
+    }
+    return h;
+}
+
+// Fragment types and loads of a mode: bf16 x bf16 for the expansion; for the projection
+// the weight fragment is widened to float16 as it is read (outside the MFMA stream).
+template <int MODE>
+struct Frag {
+    using T = typename std::conditional<MODE == kExpand, bf16x8, halfx8>::type;
+    __device__ static T weights(const char* p) {
+        const bf16x8 v = *(const bf16x8*)p;
+        if constexpr (MODE == kExpand) return v;
+        else return widen_to_f16(v);
+    }
+    __device__ static T acts(const char* p) { return *(const T*)p; }
+};
+__device__ inline floatx4 mfma_step(const bf16x8& w, const bf16x8& a, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, a, c, 0, 0, 0);
+}
+__device__ inline floatx4 mfma_step(const halfx8& w, const halfx8& a, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(w, a, c, 0, 0, 0);
+}
+
 // ------------------------------------------------------------------ dma kernel
-template <int BM_, int BNB_, int WM_, int WN_, bool SPLIT_, int NS_>
+template <int BM_, int BNB_, int WM_, int WN_, int NS_>
 struct DCfg {
     static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_, NS = NS_;
-    static constexpr bool SPLIT = SPLIT_;
     static constexpr int NW = WM * WN, NT = NW * 64;
     static constexpr int WTM = BM / WM, WTN = BNB / WN, MB = WTM / 16, NBK = WTN / 16;
-    static constexpr int A_ROWS = BM * (SPLIT ? 2 : 1);    // LDS rows of A (hi rows, then lo rows)
+    static constexpr int A_ROWS = BM;                        // LDS rows of A
     static constexpr int A_INSTR = A_ROWS / 16, B_INSTR = BNB / 16;  // 1 KB wave loads per stage
     static constexpr int QA = A_INSTR / NW, QB = B_INSTR / NW, LPW = QA + QB;
     static constexpr int STAGE = (A_ROWS + BNB) * 64;     // bytes
@@ -209,28 +231,29 @@ struct DCfg {
     static_assert(NW % 2 == 0, "two ping-pong groups");
 };
 
-using ExpDma = DCfg<256, 256, 2, 4, false, 4>;
-using DownDma = DCfg<128, 256, 2, 4, true, 4>;
+using LargeDma = DCfg<256, 256, 2, 4, 4>;
 // few rows per group (decode): weight streaming with 6 stages in flight; one M tile
 // covers a group's rows, the unused MFMA rows cost nothing when HBM is the bound
-using ExpStream = DCfg<64, 256, 1, 4, false, 6>;
-using DownStream = DCfg<64, 256, 1, 4, true, 6>;
+using StreamDma = DCfg<64, 256, 1, 4, 6>;
 
 template <class C, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_upper, int nt,
                                                          int group_n) {
     extern __shared__ __attribute__((aligned(1024))) char lds[];
     __shared__ int s_tile[3];
-    static_assert(MODE == kExpand ? !C::SPLIT : C::SPLIT, "expand reads x, down reads split z");
     int64_t mt;
     int ntile;
-    if (!tile_of(blockIdx.x, gridDim.x, mt_upper, nt, group_n, &mt, &ntile)) return;
+    // K slice: the grid holds ksplit copies of the tile grid, one per slice
+    const int64_t per_slice = gridDim.x / g.ksplit;
+    const int kslice = (int)(blockIdx.x / per_slice);
+    if (!tile_of(blockIdx.x % per_slice, per_slice, mt_upper, nt, group_n, &mt, &ntile)) return;
     if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
     const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / C::WN, wn = wave % C::WN;
-    const int K = g.K;
+    const int K = g.K / g.ksplit;                       // this slice's K range
+    const int64_t k_byte0 = (int64_t)kslice * K * 2;    // its first byte within a row
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
 
     // Source of this lane's 16 bytes in each of the wave's LPW loads per stage, and the
@@ -244,19 +267,13 @@ __global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_
     for (int q = 0; q < C::LPW; ++q) {
         if (q < C::QA) {
             const int blk = q * C::NW + wave, lr = blk * 16 + lrow;
-            const int part = lr / C::BM, tr = lr % C::BM;  // part 1: low halves of split z
-            const int64_t srow = a_source_row(g, row0 + tr, row1);
-            if (C::SPLIT) {
-                src[q] = (const char*)g.a + srow * (int64_t)K * 4 + part * 64 + chunk * 16;
-                step[q] = 128;
-            } else {
-                src[q] = (const char*)g.a + srow * (int64_t)K * 2 + chunk * 16;
-                step[q] = 64;
-            }
+            const int64_t srow = a_source_row(g, row0 + lr, row1);
+            src[q] = (const char*)g.a + srow * (int64_t)g.K * 2 + k_byte0 + chunk * 16;
+            step[q] = 64;
             dst[q] = blk * 1024;
         } else {
             const int blk = (q - C::QA) * C::NW + wave, lb = blk * 16 + lrow;
-            src[q] = (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, lb) + chunk * 16;
+            src[q] = (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, lb) + k_byte0 + chunk * 16;
             step[q] = 64;
             dst[q] = C::A_ROWS * 64 + blk * 1024;
         }
@@ -278,34 +295,21 @@ __global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_
     const int KT_ = K / 32;
     // Fragment addressing: row (lane & 15) of a 16-row block, logical chunk (lane >> 4).
     const int frag_off = (lane & 15) * 64 + (((lane >> 4) ^ (((lane & 15) >> 1) & 3)) * 16);
-    bf16x8 bfr[C::NBK], afr[C::MB], alo[C::SPLIT ? C::MB : 1];
+    typename Frag<MODE>::T bfr[C::NBK], afr[C::MB];
     auto read_frags = [&](int kt) {
         const char* S = lds + (kt % C::NS) * C::STAGE;
 #pragma unroll
-        for (int nb = 0; nb < C::NBK; ++nb)
-            bfr[nb] = *(const bf16x8*)(S + (C::A_ROWS + wn * C::WTN + nb * 16) * 64 + frag_off);
-#pragma unroll
         for (int mb = 0; mb < C::MB; ++mb)
-            afr[mb] = *(const bf16x8*)(S + (wm * C::WTM + mb * 16) * 64 + frag_off);
-        if (C::SPLIT) {
+            afr[mb] = Frag<MODE>::acts(S + (wm * C::WTM + mb * 16) * 64 + frag_off);
 #pragma unroll
-            for (int mb = 0; mb < C::MB; ++mb)
-                alo[mb] = *(const bf16x8*)(S + (C::BM + wm * C::WTM + mb * 16) * 64 + frag_off);
-        }
+        for (int nb = 0; nb < C::NBK; ++nb)
+            bfr[nb] = Frag<MODE>::weights(S + (C::A_ROWS + wn * C::WTN + nb * 16) * 64 + frag_off);
     };
     auto mfmas = [&]() {
 #pragma unroll
         for (int nb = 0; nb < C::NBK; ++nb)
 #pragma unroll
-            for (int mb = 0; mb < C::MB; ++mb)
-                acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
-        if (C::SPLIT) {
-#pragma unroll
-            for (int nb = 0; nb < C::NBK; ++nb)
-#pragma unroll
-                for (int mb = 0; mb < C::MB; ++mb)
-                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], alo[mb], acc[nb][mb], 0, 0, 0);
-        }
+            for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = mfma_step(bfr[nb], afr[mb], acc[nb][mb]);
     };
     // barrier that the compiler may not move memory accesses or other instructions across
     auto barrier = [&]() {
@@ -355,17 +359,18 @@ __global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_
         barrier();
     }
     if (!g1) barrier();        // both groups pass the same number of barriers
-    epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(g, acc, row0, row1, ntile, wm, wn, lane);
+    GemmArgs gs = g;
+    if (kslice) gs.out = (float*)g.out + (int64_t)kslice * g.rows_total * g.N;
+    epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(gs, acc, row0, row1, ntile, wm, wn, lane);
 }
 
 // --------------------------------------------------------------- staged kernel
-template <int BM_, int BNB_, int WM_, int WN_, bool SPLIT_>
+template <int BM_, int BNB_, int WM_, int WN_>
 struct SCfg {
     static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_;
-    static constexpr bool SPLIT = SPLIT_;
     static constexpr int NT = WM * WN * 64;
     static constexpr int WTM = BM / WM, WTN = BNB / WN, MB = WTM / 16, NBK = WTN / 16;
-    static constexpr int A_ROWS = BM * (SPLIT ? 2 : 1);   // 128-byte LDS rows: 64 K values
+    static constexpr int A_ROWS = BM;                      // 128-byte LDS rows: 64 K values
     static constexpr int A_CHUNKS = A_ROWS * 8, B_CHUNKS = BNB * 8;
     static constexpr int A_PER_T = (A_CHUNKS + NT - 1) / NT, B_PER_T = (B_CHUNKS + NT - 1) / NT;
     static constexpr int STAGE = (A_ROWS + BNB) * 128;
@@ -374,15 +379,13 @@ struct SCfg {
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
 
-using ExpM = SCfg<128, 128, 2, 2, false>;
-using DownM = SCfg<64, 128, 1, 4, true>;
+using MediumStaged = SCfg<128, 128, 2, 2>;
 
 template <class C, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t mt_upper, int nt,
                                                             int group_n) {
     extern __shared__ __attribute__((aligned(1024))) char lds[];
     __shared__ int s_tile[3];
-    static_assert(MODE == kExpand ? !C::SPLIT : C::SPLIT, "expand reads x, down reads split z");
     int64_t mt;
     int ntile;
     if (!tile_of(blockIdx.x, gridDim.x, mt_upper, nt, group_n, &mt, &ntile)) return;
@@ -403,12 +406,8 @@ __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t 
         const int c = tid + i * C::NT, lr = c / 8, kc = c % 8;
         aptr[i] = nullptr;
         if (c < C::A_CHUNKS) {
-            const int part = lr / C::BM, tr = lr % C::BM;
-            const int64_t srow = a_source_row(g, row0 + tr, row1);
-            // split z: a 64-wide step is blocks [hi32|lo32][hi32|lo32]; part 0 takes the hi
-            // halves (chunks 0-3 of each block), part 1 the lo halves
-            aptr[i] = C::SPLIT ? (const char*)g.a + srow * (int64_t)K * 4 + (kc / 4) * 128 + part * 64 + (kc % 4) * 16
-                               : (const char*)g.a + srow * (int64_t)K * 2 + kc * 16;
+            const int64_t srow = a_source_row(g, row0 + lr, row1);
+            aptr[i] = (const char*)g.a + srow * (int64_t)K * 2 + kc * 16;
         }
     }
 #pragma unroll
@@ -418,7 +417,7 @@ __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t 
                       ? (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, j) + kc * 16
                       : nullptr;
     }
-    const int a_step = C::SPLIT ? 256 : 128;
+    const int a_step = 128;
 
     uint4 ra[C::A_PER_T], rb[C::B_PER_T];
     auto gload = [&](int kt) {
@@ -461,28 +460,17 @@ __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t 
         for (int ks = 0; ks < 2; ++ks) {
             const int ck = ks * 4 + (lane >> 4);
             const int off = (lane & 15) * 128 + ((ck ^ (((lane & 15) >> 1) & 7)) * 16);
-            bf16x8 bfr[C::NBK], afr[C::MB];
+            typename Frag<MODE>::T bfr[C::NBK], afr[C::MB];
 #pragma unroll
             for (int nb = 0; nb < C::NBK; ++nb)
-                bfr[nb] = *(const bf16x8*)(S + (C::A_ROWS + wn * C::WTN + nb * 16) * 128 + off);
+                bfr[nb] = Frag<MODE>::weights(S + (C::A_ROWS + wn * C::WTN + nb * 16) * 128 + off);
 #pragma unroll
             for (int mb = 0; mb < C::MB; ++mb)
-                afr[mb] = *(const bf16x8*)(S + (wm * C::WTM + mb * 16) * 128 + off);
+                afr[mb] = Frag<MODE>::acts(S + (wm * C::WTM + mb * 16) * 128 + off);
 #pragma unroll
             for (int nb = 0; nb < C::NBK; ++nb)
 #pragma unroll
-                for (int mb = 0; mb < C::MB; ++mb)
-                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
-            if (C::SPLIT) {
-#pragma unroll
-                for (int mb = 0; mb < C::MB; ++mb)
-                    afr[mb] = *(const bf16x8*)(S + (C::BM + wm * C::WTM + mb * 16) * 128 + off);
-#pragma unroll
-                for (int nb = 0; nb < C::NBK; ++nb)
-#pragma unroll
-                    for (int mb = 0; mb < C::MB; ++mb)
-                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[nb], afr[mb], acc[nb][mb], 0, 0, 0);
-            }
+                for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = mfma_step(bfr[nb], afr[mb], acc[nb][mb]);
         }
         if (kt + 1 < KT) lstore(cur ^ 1);
         __syncthreads();
@@ -507,7 +495,7 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     const int64_t mt_upper = g.offsets ? ceil_div(R, C::BM) + g.n : ceil_div(R, C::BM);
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
     const int nt = (int)ceil_div(g.N, kOutCols);
-    const int64_t grid = ceil_div(mt_upper * nt, 8) * 8;
+    const int64_t grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
     if (mt_upper * nt <= 0) return hipSuccess;
     static const int group_n = [] {
         const char* env = getenv("PCM_GEMM_GROUP_N");
@@ -534,21 +522,32 @@ char pick_tile(int64_t R, int groups) {
 
 }  // namespace
 
-hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s) {
+int down_ksplit(int64_t R, int n, int H, int F) {
+    // only the large-tile kernel slices K; its grid is (R/256 + n) x (H/256) tiles
+    if (pick_tile(R, n) != 'L') return 1;
+    const int64_t tiles = (ceil_div(R, 256) + n) * ceil_div(H, 256);
+    return (tiles < 4 * 256 && (F / 2) % 32 == 0 && F / 32 >= 128) ? 2 : 1;
+}
+
+hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStream_t s) {
+    GemmArgs g = g0;
+    if (g.ksplit < 1) g.ksplit = 1;
     const char t = pick_tile(R, g.offsets ? g.n : 1);
-    if (mode == kExpand) {
-        if (t == 'S') return launch_cfg<ExpStream, kExpand, true>(g, R, s);
-        if (t == 'M') return launch_cfg<ExpM, kExpand, false>(g, R, s);
-        return launch_cfg<ExpDma, kExpand, true>(g, R, s);
+    if (g.ksplit > 1 && (mode != kDownStore || t != 'L')) return hipErrorInvalidValue;
+    switch (mode) {
+        case kExpand:
+            if (t == 'S') return launch_cfg<StreamDma, kExpand, true>(g, R, s);
+            if (t == 'M') return launch_cfg<MediumStaged, kExpand, false>(g, R, s);
+            return launch_cfg<LargeDma, kExpand, true>(g, R, s);
+        case kDownStore:
+            if (t == 'S') return launch_cfg<StreamDma, kDownStore, true>(g, R, s);
+            if (t == 'M') return launch_cfg<MediumStaged, kDownStore, false>(g, R, s);
+            return launch_cfg<LargeDma, kDownStore, true>(g, R, s);
+        default:
+            if (t == 'S') return launch_cfg<StreamDma, kDownAccum, true>(g, R, s);
+            if (t == 'M') return launch_cfg<MediumStaged, kDownAccum, false>(g, R, s);
+            return launch_cfg<LargeDma, kDownAccum, true>(g, R, s);
     }
-    if (mode == kDownStore) {
-        if (t == 'S') return launch_cfg<DownStream, kDownStore, true>(g, R, s);
-        if (t == 'M') return launch_cfg<DownM, kDownStore, false>(g, R, s);
-        return launch_cfg<DownDma, kDownStore, true>(g, R, s);
-    }
-    if (t == 'S') return launch_cfg<DownStream, kDownAccum, true>(g, R, s);
-    if (t == 'M') return launch_cfg<DownM, kDownAccum, false>(g, R, s);
-    return launch_cfg<DownDma, kDownAccum, true>(g, R, s);
 }
 
 }  // namespace pcm

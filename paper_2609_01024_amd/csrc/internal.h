@@ -35,20 +35,22 @@ size_t build_paths_ws_bytes(int64_t T, int n);
 
 enum GemmMode { kExpand = 0, kDownStore = 1, kDownAccum = 2 };
 
-// Layout of a bf16 layer's projection input z (and of a dense FFN's SwiGLU output): a
-// float32 value v is carried as the bfloat16 pair hi = rn(v), lo = rn(v - hi), which
-// represents v to about 2^-17 relative. Row r holds F/32 blocks of [32 hi | 32 lo], so one
-// 32-wide K step of the down GEMM reads 128 contiguous bytes of a row.
-// The down GEMM multiplies both halves by the same weight tile, so the projection sees
-// the float32 value instead of a single bfloat16 rounding of it.
-constexpr int kSplitBlock = 32;
+// Projection input of a bf16 layer. z (float32 in the mix) is stored as float16 after
+// multiplying row r by a power of two chosen from the row's largest |z| (so the largest
+// element sits just below 2^14); row_scale[r] holds the inverse, applied exactly in the
+// down GEMM's epilogue. float16 keeps 11 significant bits, eight times the precision of
+// a single bfloat16 rounding, and runs at the bfloat16 MFMA rate; the row scaling keeps
+// any activation magnitude inside float16's range.
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+constexpr int kZScaleExp = 14;
 
 struct GemmArgs {
-    const void* a;              // expand: x [T,H] (rows gathered); down: z (split bf16 or f32)
+    const void* a;              // expand: x [T,H] (rows gathered); down: z [R,F] (f16 or f32)
     const void* b0;             // expand: w_gate [n,F,H]; down: w_down [n,H,F]
     const void* b1;             // expand: w_up [n,F,H]; down: unused
-    void* out;                  // expand: u [R,F] f32 (or split bf16, see split_out);
-                                // down-store: o [R,H] f32; down-accum: y [R,H] f32
+    void* out;                  // expand: u [R,F] f32; down-store: o [R,H] f32;
+                                // down-accum: y [R,H] f32
+    const float* row_scale;     // down (bf16 layers): inverse scale of each z row
     const int32_t* offsets;     // [n+1] rows of each group (NULL: one group of a_rows rows)
     const int32_t* gather;      // expand: row_token [R] (NULL: identity); down: unused
     int64_t a_rows;             // rows of `a` (gathered indices are clamped to it)
@@ -56,16 +58,24 @@ struct GemmArgs {
     int K;                      // contraction length (H for expand, F for down)
     int N;                      // output columns (F for expand, H for down)
     int accumulate;             // down-accum: add into out
-    int split_out;              // expand (bf16): write u as split hi/lo pairs instead of f32
+    int ksplit;                 // down-store: K split into ksplit slices, slice s writes
+                                // out + s * rows_total * N (the combine adds the slices)
+    int64_t rows_total;         // rows of `out` per slice (down-store with ksplit > 1)
 };
+
+// Number of K slices the projection of R rows uses (1 or 2): split when the output tiles
+// alone would leave the chip's 256 compute units idle for much of the last round.
+int down_ksplit(int64_t R, int n, int H, int F);
 
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
 hipError_t launch_gemm_f32(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
 
-// z_(t,b) = sum_a beta_ab u_(t,a); u is f32 [R,F]; z is split bf16 (split) or f32 [R,F].
-hipError_t launch_mix(bool split, const float* u, void* z, const uint64_t* bits, const float* beta,
-                      const int32_t* row_of, int64_t T, int k, int F, hipStream_t s);
-hipError_t launch_combine(const float* o, const int32_t* row_of, int64_t T, int k, int H,
-                          float* y, int accumulate, hipStream_t s);
+// z_(t,b) = sum_a beta_ab u_(t,a); u is f32 [R,F]; z is f16 (scaled rows, inverse scales in
+// zscale) when zscale != NULL, else f32. bits == NULL: identity (k = 1, z_t = u_t).
+hipError_t launch_mix(const float* u, void* z, float* zscale, const uint64_t* bits,
+                      const float* beta, const int32_t* row_of, int64_t T, int k, int F,
+                      hipStream_t s);
+hipError_t launch_combine(const float* o, int ksplit, const int32_t* row_of, int64_t T, int k,
+                          int H, float* y, int accumulate, hipStream_t s);
 
 }  // namespace pcm

@@ -33,14 +33,21 @@ pcm_status check_paths(const pcm_paths* p) {
 
 pcm_status from_hip(hipError_t e) { return e == hipSuccess ? PCM_OK : PCM_ERR_HIP; }
 
-// project_combine workspace: z [R,F] (f32, or split bf16 pairs of the same size), then
-// o [R,H] f32, each 256-byte aligned.
-size_t project_ws(int64_t T, int H, int F, int k, pcm_dtype dt, size_t* o_offset) {
-    (void)dt;
-    const size_t R = (size_t)T * k;
-    const size_t z = align_up(R * F * sizeof(float), 256);
-    if (o_offset) *o_offset = z;
-    return z + align_up(R * H * sizeof(float), 256);
+// Workspace of the projection of R rows of n groups: z [R,F] (f16 for bf16 layers, f32
+// otherwise), the per-row inverse scales [R] f32 (bf16 layers), then, when `with_o`, the
+// projected rows o [ksplit, R, H] f32 (K slices of the projection); parts 256-byte aligned.
+struct ProjWs {
+    size_t zscale_off, o_off, total;
+    int ksplit;
+};
+ProjWs proj_ws(size_t R, int n, int H, int F, pcm_dtype dt, bool with_o) {
+    ProjWs w;
+    w.ksplit = (with_o && dt == PCM_BF16) ? down_ksplit((int64_t)R, n, H, F) : 1;
+    const size_t z = align_up(R * F * (dt == PCM_BF16 ? 2 : 4), 256);
+    w.zscale_off = z;
+    w.o_off = z + (dt == PCM_BF16 ? align_up(R * sizeof(float), 256) : 0);
+    w.total = w.o_off + (with_o ? align_up((size_t)w.ksplit * R * H * sizeof(float), 256) : 0);
+    return w;
 }
 
 }  // namespace
@@ -67,10 +74,11 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
         case PCM_OP_EXPAND: return 0;
         case PCM_OP_PROJECT_COMBINE:
             if (H < 1 || F < 1) return 0;
-            return project_ws(T, H, F, k, dtype, nullptr);
-        case PCM_OP_DENSE_SWIGLU:  // the SwiGLU output, f32 or split bf16 pairs (same size)
+            return proj_ws((size_t)T * k, n, H, F, dtype, true).total;
+        case PCM_OP_DENSE_SWIGLU:  // the SwiGLU output u [T,F] f32, then a projection input
             if (H < 1 || F < 1) return 0;
-            return align_up((size_t)T * F * sizeof(float), 256);
+            return align_up((size_t)T * F * sizeof(float), 256) +
+                   (dtype == PCM_BF16 ? proj_ws((size_t)T, 1, H, F, dtype, false).total : 0);
     }
     return 0;
 }
@@ -140,30 +148,33 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
     if (T == 0) return PCM_OK;
     if (!u || !w_down || !y || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
     if (!aligned16(u) || !aligned16(w_down) || !aligned16(y)) return PCM_ERR_ARG;
-    size_t o_off = 0;
-    const size_t need = project_ws(T, H, F, k, dtype, &o_off);
-    if (!ws || ws_bytes < need) return PCM_ERR_WORKSPACE;
+    const int64_t R = T * k;
+    const ProjWs w = proj_ws((size_t)R, n, H, F, dtype, true);
+    if (!ws || ws_bytes < w.total) return PCM_ERR_WORKSPACE;
     if (!aligned16(ws)) return PCM_ERR_ARG;
     void* z = ws;
-    float* o = (float*)((char*)ws + o_off);
-    const int64_t R = T * k;
-    hipStream_t s = (hipStream_t)stream;
     const bool bf16 = dtype == PCM_BF16;
-    hipError_t e = launch_mix(bf16, (const float*)u, z, paths->path_bits, paths->beta, paths->row_of,
-                              T, k, F, s);
+    float* zscale = bf16 ? (float*)((char*)ws + w.zscale_off) : nullptr;
+    float* o = (float*)((char*)ws + w.o_off);
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = launch_mix((const float*)u, z, zscale, paths->path_bits, paths->beta,
+                              paths->row_of, T, k, F, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     GemmArgs g{};
     g.a = z;
     g.b0 = w_down;
     g.out = o;
+    g.row_scale = zscale;
     g.offsets = paths->expert_offsets;
     g.a_rows = R;
     g.n = n;
     g.K = F;
     g.N = H;
+    g.ksplit = w.ksplit;
+    g.rows_total = R;
     e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s) : launch_gemm_f32(kDownStore, g, R, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
-    return from_hip(launch_combine(o, paths->row_of, T, k, H, y, accumulate, s));
+    return from_hip(launch_combine(o, w.ksplit, paths->row_of, T, k, H, y, accumulate, s));
 }
 
 pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
@@ -178,27 +189,38 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     if (!x || !w_gate || !w_up || !w_down || !y) return PCM_ERR_ARG;
     if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y))
         return PCM_ERR_ARG;
-    const size_t need = align_up((size_t)T * Fs * sizeof(float), 256);
+    const bool bf16 = dtype == PCM_BF16;
+    const size_t u_bytes = align_up((size_t)T * Fs * sizeof(float), 256);
+    const ProjWs w = proj_ws((size_t)T, 1, H, Fs, dtype, false);
+    const size_t need = u_bytes + (bf16 ? w.total : 0);
     if (!ws || ws_bytes < need) return PCM_ERR_WORKSPACE;
     if (!aligned16(ws)) return PCM_ERR_ARG;
     hipStream_t s = (hipStream_t)stream;
-    const bool bf16 = dtype == PCM_BF16;
+    float* u = (float*)ws;
     GemmArgs g{};
     g.a = x;
     g.b0 = w_gate;
     g.b1 = w_up;
-    g.out = ws;
+    g.out = u;
     g.offsets = nullptr;
     g.gather = nullptr;
     g.a_rows = T;
     g.n = 1;
     g.K = H;
     g.N = Fs;
-    g.split_out = bf16 ? 1 : 0;
     hipError_t e = bf16 ? launch_gemm_bf16(kExpand, g, T, s) : launch_gemm_f32(kExpand, g, T, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
+    void* z = u;
+    float* zscale = nullptr;
+    if (bf16) {  // row-scaled float16 projection input
+        z = (char*)ws + u_bytes;
+        zscale = (float*)((char*)z + w.zscale_off);
+        e = launch_mix(u, z, zscale, nullptr, nullptr, nullptr, T, 1, Fs, s);
+        if (e != hipSuccess) return PCM_ERR_HIP;
+    }
     GemmArgs d{};
-    d.a = ws;
+    d.a = z;
+    d.row_scale = zscale;
     d.b0 = w_down;
     d.out = y;
     d.offsets = nullptr;

@@ -83,7 +83,11 @@ def test_expand_and_project_validation(L):
     assert L.pcm_expand(1, FAKE, None, FAKE, bp, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
     assert L.pcm_expand(1, FAKE, FAKE, FAKE, None, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
     need = L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, 4, 128, 128, 8, 2, 1)
-    assert need >= 4 * 2 * 128 * 4 + 4 * 2 * 128 * 4
+    al = lambda v: (v + 255) // 256 * 256
+    R = 4 * 2
+    assert need == al(R * 128 * 2) + al(R * 4) + al(R * 128 * 4)      # z f16, scales, o
+    assert L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, 4, 128, 128, 8, 2, 0) == \
+        al(R * 128 * 4) + al(R * 128 * 4)                                  # f32 layer: z f32, o
     assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, 0, FAKE, need - 1,
                                  None) == WS
     assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, 0, None, need,
@@ -91,7 +95,7 @@ def test_expand_and_project_validation(L):
     assert L.pcm_project_combine(1, FAKE, FAKE, bp, 4, 128, 128, 8, 9, FAKE, 0, FAKE, need,
                                  None) == ARG
     needd = L.pcm_workspace_bytes(binding.OP_DENSE_SWIGLU, 16, 128, 256, 1, 1, 1)
-    assert needd == 16 * 256 * 4
+    assert needd == 16 * 256 * 4 + 16 * 256 * 2 + 256                     # u f32, z f16, scales
     assert L.pcm_dense_swiglu(1, FAKE, FAKE, FAKE, FAKE, 16, 128, 256, FAKE, 0, FAKE, needd - 1,
                               None) == WS
     assert L.pcm_dense_swiglu(1, FAKE, FAKE, FAKE, FAKE, 16, 128, 200, FAKE, 0, FAKE, needd,

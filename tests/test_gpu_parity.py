@@ -159,6 +159,8 @@ SMALL = {
     "fine_s": scaled(CONFIGS["finegrained_shared"], T=1200, H=192, F=320, shared_F=448,
                      name="fine_s"),
     "decode_s": scaled(CONFIGS["decode"], H=512, F=256, name="decode_s"),
+    # long F and few output tiles: the large-tile projection splits K in two slices
+    "splitk_s": scaled(CONFIGS["mixtral"], T=300, H=256, F=4096, n=4, name="splitk_s"),
 }
 
 
