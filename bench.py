@@ -36,8 +36,6 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per launch of the dominant kernel")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer 5 times (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -53,6 +51,21 @@ def copy_probe(mib: int):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_per_launch": n * 4, "launches": 5}), flush=True)
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counters
+    (profiles/traffic.json), or None when they were taken on a different kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = os.path.join(ROOT, rec["kernel_source"])
+    if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["sha256"]:
+        return None
+    w = rec["workloads"].get(workload)
+    return None if w is None else w["bytes_per_launch"]
 
 
 def cpu_baseline(inp, target_s: float) -> dict:
@@ -149,9 +162,7 @@ def main():
     bf16 = cfg.dtype == "bf16"
     peak = acc.BF16_PEAK_TFLOPS if bf16 else acc.FP32_PEAK_TFLOPS
 
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        traffic = json.load(open(args.traffic)).get(name)
+    traffic = measured_traffic(name)
 
     if name == "decode":
         # weight streaming: every touched expert's three matrices are read once per step
