@@ -11,7 +11,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxK = 8;
 constexpr int kMaxN = 256;
-constexpr int kPathBlock = 1024;  // tokens per block of the path/index build
+constexpr int kPathBlock = 256;   // tokens per block of the path/index build
 
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }

@@ -10,7 +10,7 @@
 //   - rows of e before token (wave, lane) = rows of e in earlier blocks (a scan over
 //     block counts) + in earlier waves of this block (popcounts) + popcount(words[wave][e]
 //     & lanes below this one).
-// T <= 1024 runs as one fused launch; larger T as count / scan / scatter launches.
+// T <= 256 runs as one fused launch; larger T as count / scan / scatter launches.
 #include "internal.h"
 
 namespace pcm {
@@ -68,13 +68,19 @@ __global__ __launch_bounds__(kPathBlock) void paths_kernel(
             float p[kMaxK];
 #pragma unroll
             for (int a = 0; a < kMaxK; ++a) p[a] = a < k ? w[t * k + a] : 0.0f;
+            // every (a, b) entry is loaded (e[] is always a valid id), so the 64 loads are
+            // issued together instead of one dependent load per branch
+            uint8_t mv[kMaxK][kMaxK];
+#pragma unroll
+            for (int a = 0; a < kMaxK; ++a)
+#pragma unroll
+                for (int b = 0; b < kMaxK; ++b) mv[a][b] = mask[(int64_t)e[a] * n + e[b]];
             uint64_t bits = 0;
 #pragma unroll
             for (int a = 0; a < kMaxK; ++a)
 #pragma unroll
                 for (int b = 0; b < kMaxK; ++b)
-                    if (a < k && b < k && (a == b || mask[(int64_t)e[a] * n + e[b]]))
-                        bits |= 1ull << (a * k + b);
+                    if (a < k && b < k && (a == b || mv[a][b])) bits |= 1ull << (a * k + b);
             bits_out[t] = bits;
             float global = 0.0f;
 #pragma unroll
@@ -95,8 +101,10 @@ __global__ __launch_bounds__(kPathBlock) void paths_kernel(
                     if (b >= k) break;
                     float v = 0.0f;
                     if ((bits >> (a * k + b)) & 1) {
-                        const float prod = p[a] * p[b];
-                        v = beta_mode == 0 ? prod / src : (beta_mode == 1 ? prod : prod / global);
+                        // p_a (p_b / src) rather than a reciprocal: stays exact (beta_aa = p_a
+                        // for a source whose only target is itself) when p is subnormal
+                        v = beta_mode == 0 ? p[a] * (p[b] / src)
+                                           : (beta_mode == 1 ? p[a] * p[b] : p[a] * p[b] / global);
                     }
                     bt[a * k + b] = v;
                 }
@@ -156,10 +164,15 @@ __global__ __launch_bounds__(kMaxN) void paths_scan_kernel(int32_t* __restrict__
     const int x = threadIdx.x;
     int run = 0;
     if (x < n)
-        for (int64_t b = 0; b < NB; ++b) {
-            const int c = block_counts[b * n + x];
-            block_counts[b * n + x] = run;
-            run += c;
+        for (int64_t b0 = 0; b0 < NB; b0 += 16) {  // 16 independent loads, then the running sum
+            int c[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) c[j] = b0 + j < NB ? block_counts[(b0 + j) * n + x] : 0;
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                if (b0 + j < NB) block_counts[(b0 + j) * n + x] = run;
+                run += c[j];
+            }
         }
     scan[x] = x < n ? run : 0;
     __syncthreads();
@@ -173,7 +186,14 @@ __global__ __launch_bounds__(kMaxN) void paths_scan_kernel(int32_t* __restrict__
     const int excl = scan[x] - own;
     if (x < n) {
         offsets[x] = excl;
-        for (int64_t b = 0; b < NB; ++b) block_counts[b * n + x] += excl;
+        for (int64_t b0 = 0; b0 < NB; b0 += 16) {
+            int c[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) c[j] = b0 + j < NB ? block_counts[(b0 + j) * n + x] : 0;
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+                if (b0 + j < NB) block_counts[(b0 + j) * n + x] = c[j] + excl;
+        }
     }
     if (x == kMaxN - 1) offsets[n] = scan[x];
 }

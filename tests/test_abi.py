@@ -105,4 +105,5 @@ def test_expand_and_project_validation(L):
 
 def test_workspace_bytes_invalid(L):
     assert L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, -1, 128, 128, 8, 2, 1) == 0
-    assert L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 1024, 0, 0, 8, 2, 0) == 0  # one block
+    assert L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 256, 0, 0, 8, 2, 0) == 0  # one block
+    assert L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 257, 0, 0, 8, 2, 0) == 256  # 2 blocks x 8

@@ -131,8 +131,8 @@ def test_build_paths_full_size(name):
 
 
 @pytest.mark.parametrize("beta_mode", [0, 1, 2])
-@pytest.mark.parametrize("T,n,k", [(1, 1, 1), (5, 4, 4), (1023, 8, 2), (1025, 64, 8), (3000, 256, 8),
-                                   (4097, 60, 4)])
+@pytest.mark.parametrize("T,n,k", [(1, 1, 1), (5, 4, 4), (256, 8, 2), (257, 64, 8), (1025, 64, 8),
+                                   (3000, 256, 8), (4097, 60, 4)])
 def test_build_paths_shapes(T, n, k, beta_mode):
     rng = np.random.default_rng(T + n)
     l = rng.standard_normal((T, n)).astype(np.float32)
