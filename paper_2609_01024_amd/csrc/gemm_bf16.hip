@@ -12,14 +12,19 @@
 // Both operands are K-contiguous (x rows and W rows run along H; Z rows and W_down rows
 // along F), so a lane's 8 consecutive K values of a row are one 16-byte load.
 //
-// Two kernel shapes share the epilogue and the work decomposition:
-//  * "dma" (large tiles): global -> LDS direct loads (global_load_lds_dwordx4, no register
-//    staging), 32-wide K steps in NS LDS stages, loads issued NS-1 steps ahead, one
-//    workgroup barrier per step. LDS rows are 64 bytes; the 16-byte chunk c of row r sits
-//    at position c ^ ((r >> 1) & 3), which keeps the fragment reads (16 rows x 4 chunks per
+// Three kernel shapes share the epilogue and the work decomposition:
+//  * "interleaved" (large tiles, 256 x 256): four waves, one per SIMD, each owning a 128 x 128
+//    block of C in 256 accumulation registers. Global -> LDS direct loads
+//    (global_load_lds_dwordx4, no register staging), 32-wide K steps in NS LDS stages
+//    issued NS steps ahead, one workgroup barrier per step; within a step each wave issues
+//    its 64 MFMAs interleaved with the fragment reads of the next step and the loads of a
+//    later one. LDS rows are 64 bytes; the 16-byte chunk c of row r sits at position
+//    c ^ ((r >> 1) & 3), which keeps the fragment reads (16 rows x 4 chunks per
 //    instruction) free of bank conflicts.
-//  * "staged" (small tiles): loads through registers into two LDS stages of 64-wide K
+//  * "staged" (medium tiles): loads through registers into two LDS stages of 64-wide K
 //    steps; rows of 128 bytes with chunk c of row r at position c ^ ((r >> 1) & 7).
+//  * "stream" (a few rows per group, decode): no LDS, fragments loaded straight into a
+//    register ring several k-steps ahead; the weights are the traffic.
 // The MFMA takes the weight fragment as its first operand, so each lane's four
 // accumulators are four consecutive output columns of one row (16-byte stores). For the
 // expansion, a wave's weight rows are half gate and half up for the same columns, so the
@@ -141,6 +146,10 @@ __device__ inline const uint16_t* b_source_row(const GemmArgs& g, int e, int nti
     return (const uint16_t*)g.b0 + ((int64_t)e * g.N + h) * g.K;
 }
 
+// SiLU(g) = g / (1 + e^-g) with the hardware reciprocal (about 1 ulp) instead of an IEEE
+// division; for g below about -88, e^-g is +inf and the result is -0.
+__device__ inline float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
+
 // Shared epilogue: acc[nb][mb] holds C[row = .. + (lane & 15)][cols c0 .. c0+3].
 template <int MODE, int MB, int NBK, int WTM, int WTN, int OUT_COLS>
 __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB], int row0,
@@ -158,7 +167,7 @@ __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB]
                 const floatx4 gt = acc[nb][mb], up = acc[nb + NBK / 2][mb];
                 float v[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) v[i] = gt[i] / (1.0f + __expf(-gt[i])) * up[i];
+                for (int i = 0; i < 4; ++i) v[i] = silu(gt[i]) * up[i];
                 *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
             }
         } else {
@@ -213,105 +222,111 @@ __device__ inline floatx4 mfma_step(const halfx8& w, const halfx8& a, floatx4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(w, a, c, 0, 0, 0);
 }
 
-// ------------------------------------------------------------------ dma kernel
+// ---------------------------------------------------------- interleaved kernel
+// One wave per SIMD, each owning a 128 x 128 block of C (256 accumulator registers). Every
+// k-step is one barrier; between two barriers a wave issues the 64 MFMAs of step kt from
+// registers, interleaved with the LDS fragment reads of step kt+1 (into the other register
+// set) and the global->LDS loads of step kt+NS (into the stage step kt just vacated).
 template <int BM_, int BNB_, int WM_, int WN_, int NS_>
-struct DCfg {
+struct ICfg {
     static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_, NS = NS_;
     static constexpr int NW = WM * WN, NT = NW * 64;
     static constexpr int WTM = BM / WM, WTN = BNB / WN, MB = WTM / 16, NBK = WTN / 16;
-    static constexpr int A_ROWS = BM;                        // LDS rows of A
-    static constexpr int A_INSTR = A_ROWS / 16, B_INSTR = BNB / 16;  // 1 KB wave loads per stage
+    static constexpr int A_ROWS = BM;
+    static constexpr int A_INSTR = A_ROWS / 16, B_INSTR = BNB / 16;
     static constexpr int QA = A_INSTR / NW, QB = B_INSTR / NW, LPW = QA + QB;
-    static constexpr int STAGE = (A_ROWS + BNB) * 64;     // bytes
+    static constexpr int STAGE = (A_ROWS + BNB) * 64;
     static constexpr int LDS_BYTES = NS * STAGE;
     static_assert(A_INSTR % NW == 0 && B_INSTR % NW == 0, "every wave issues the same loads");
     static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
     static_assert(LDS_BYTES <= 160 * 1024 - 64, "LDS budget");
-    static_assert(NS >= 2 && (NS - 2) * LPW <= 63, "vmcnt range");
-    static_assert(NW % 2 == 0, "two ping-pong groups");
+    static_assert(NS >= 2 && (NS - 1) * LPW <= 63, "vmcnt range");
 };
 
-using LargeDma = DCfg<256, 256, 2, 4, 4>;
-// few rows per group (decode): weight streaming with 6 stages in flight; one M tile
-// covers a group's rows, the unused MFMA rows cost nothing when HBM is the bound
-using StreamDma = DCfg<64, 256, 1, 4, 6>;
+using LargeIl = ICfg<256, 256, 2, 2, 4>;
+
+// MFMA through inline assembly with the accumulator pinned to AGPRs ("a" constraint):
+// 256 accumulators per lane exceed what the compiler keeps in AGPRs across a loop without
+// copies. FIRST starts from a zero accumulator (srcC = 0).
+template <bool FIRST>
+__device__ inline void mfma_agpr(floatx4& c, const bf16x8& w, const bf16x8& a) {
+    if constexpr (FIRST)
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(c) : "v"(w), "v"(a));
+    else
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(w), "v"(a));
+}
+template <bool FIRST>
+__device__ inline void mfma_agpr(floatx4& c, const halfx8& w, const halfx8& a) {
+    if constexpr (FIRST)
+        asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, 0" : "=a"(c) : "v"(w), "v"(a));
+    else
+        asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(c) : "v"(w), "v"(a));
+}
+
+// One dword of a bf16 weight fragment (two values) widened to two float16 values, in
+// inline assembly so that it keeps its place in the interleaved instruction stream.
+__device__ inline uint32_t widen_pair_asm(uint32_t w) {
+    uint32_t out, lo, hi;
+    asm volatile(
+        "v_lshlrev_b32 %1, 16, %3\n\t"
+        "v_and_b32 %2, 0xffff0000, %3\n\t"
+        "v_cvt_pk_f16_f32 %0, %1, %2"
+        : "=v"(out), "=&v"(lo), "=&v"(hi)
+        : "v"(w));
+    return out;
+}
 
 template <class C, int MODE>
-__global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_upper, int nt,
-                                                         int group_n) {
+__global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_upper, int nt,
+                                                        int group_n) {
     extern __shared__ __attribute__((aligned(1024))) char lds[];
     __shared__ int s_tile[3];
     int64_t mt;
     int ntile;
-    // K slice: the grid holds ksplit copies of the tile grid, one per slice
     const int64_t per_slice = gridDim.x / g.ksplit;
     const int kslice = (int)(blockIdx.x / per_slice);
     if (!tile_of(blockIdx.x % per_slice, per_slice, mt_upper, nt, group_n, &mt, &ntile)) return;
     if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
     const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / C::WN, wn = wave % C::WN;
-    const int K = g.K / g.ksplit;                       // this slice's K range
-    const int64_t k_byte0 = (int64_t)kslice * K * 2;    // its first byte within a row
+    const int K = g.K / g.ksplit;
+    const int64_t k_byte0 = (int64_t)kslice * K * 2;
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
 
-    // Source of this lane's 16 bytes in each of the wave's LPW loads per stage, and the
-    // byte step per K step. Load q covers LDS rows [blk*16, blk*16 + 16) of A (q < QA) or B.
     const char* src[C::LPW];
-    int64_t step[C::LPW];
     int dst[C::LPW];
-    const int lrow = lane >> 2;                           // row within the 16-row block
-    const int chunk = (lane & 3) ^ ((lrow >> 1) & 3);     // logical 16-byte chunk it fetches
+    const int lrow = lane >> 2;
+    const int chunk = (lane & 3) ^ ((lrow >> 1) & 3);
 #pragma unroll
     for (int q = 0; q < C::LPW; ++q) {
         if (q < C::QA) {
             const int blk = q * C::NW + wave, lr = blk * 16 + lrow;
             const int64_t srow = a_source_row(g, row0 + lr, row1);
             src[q] = (const char*)g.a + srow * (int64_t)g.K * 2 + k_byte0 + chunk * 16;
-            step[q] = 64;
             dst[q] = blk * 1024;
         } else {
             const int blk = (q - C::QA) * C::NW + wave, lb = blk * 16 + lrow;
             src[q] = (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, lb) + k_byte0 + chunk * 16;
-            step[q] = 64;
             dst[q] = C::A_ROWS * 64 + blk * 1024;
         }
     }
-    auto issue = [&](int kt) {
-        char* base = lds + (kt % C::NS) * C::STAGE;
-#pragma unroll
-        for (int q = 0; q < C::LPW; ++q)
-            __builtin_amdgcn_global_load_lds((const void*)(src[q] + kt * step[q]),
-                                             (PCM_LDS void*)(base + dst[q]), 16, 0, 0);
+    auto load = [&](int q, int ks, char* base) {
+        __builtin_amdgcn_global_load_lds((const void*)(src[q] + (int64_t)ks * 64),
+                                         (PCM_LDS void*)(base + dst[q]), 16, 0, 0);
     };
 
     floatx4 acc[C::NBK][C::MB];
-#pragma unroll
-    for (int nb = 0; nb < C::NBK; ++nb)
-#pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    const int KT_ = K / 32;
-    // Fragment addressing: row (lane & 15) of a 16-row block, logical chunk (lane >> 4).
+    const int KT_ = K / 32;                 // even: K is a multiple of 64
     const int frag_off = (lane & 15) * 64 + (((lane >> 4) ^ (((lane & 15) >> 1) & 3)) * 16);
-    typename Frag<MODE>::T bfr[C::NBK], afr[C::MB];
-    auto read_frags = [&](int kt) {
-        const char* S = lds + (kt % C::NS) * C::STAGE;
-#pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb)
-            afr[mb] = Frag<MODE>::acts(S + (wm * C::WTM + mb * 16) * 64 + frag_off);
-#pragma unroll
-        for (int nb = 0; nb < C::NBK; ++nb)
-            bfr[nb] = Frag<MODE>::weights(S + (C::A_ROWS + wn * C::WTN + nb * 16) * 64 + frag_off);
-    };
-    auto mfmas = [&]() {
-#pragma unroll
-        for (int nb = 0; nb < C::NBK; ++nb)
-#pragma unroll
-            for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = mfma_step(bfr[nb], afr[mb], acc[nb][mb]);
-    };
-    // barrier that the compiler may not move memory accesses or other instructions across
+    using FT = typename Frag<MODE>::T;
+    FT af[2][C::MB], bf[2][C::NBK];
+    bf16x8 braw[C::NBK];
+    uint32_t bw[C::NBK][4];
+    auto b_at = [&](const char* S, int nb) { return S + (C::A_ROWS + wn * C::WTN + nb * 16) * 64 + frag_off; };
+    auto a_at = [&](const char* S, int mb) { return S + (wm * C::WTM + mb * 16) * 64 + frag_off; };
     auto barrier = [&]() {
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("" ::: "memory");
@@ -319,46 +334,71 @@ __global__ __launch_bounds__(C::NT) void gemm_dma_kernel(GemmArgs g, int64_t mt_
         asm volatile("" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
     };
-    // this wave's loads of step kt+1 have landed (later steps may still be in flight)
-    auto wait_next_stage = [&](int kt, bool lds_too) {
-        if (kt + C::NS - 1 < KT_) {
-            if (lds_too) __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, 0));
-            else __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, kNoLgkm));
-        } else {
-            if (lds_too) __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
-            else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, kNoLgkm));
+    constexpr int NM = C::NBK * C::MB;        // MFMAs per k-step
+    constexpr int NR = C::NBK + C::MB;        // fragment reads per k-step
+    constexpr int R_EVERY = 3, L_EVERY = 6, W_FROM = R_EVERY * C::NBK + 2;
+    static_assert(R_EVERY * (NR - 1) < NM && L_EVERY * (C::LPW - 1) + 1 < NM, "slots");
+    static_assert(W_FROM + 4 * C::NBK <= NM, "widen slots");
+    // One k-step. Every step issues LPW loads (past the last step they re-read the last
+    // step's source into a stage nobody reads again), so at the top of step kt steps
+    // 0 .. kt+NS-1 are issued and step kt+1 must have landed: NS-2 newer steps in flight.
+    // MFMA i is followed by fragment read i/R_EVERY (weights first) and load i/L_EVERY;
+    // program order is issue order (the MFMAs are volatile asm, the rest memory accesses).
+    auto body = [&](int kt, auto first, FT (&ca)[C::MB], FT (&cb)[C::NBK], FT (&na)[C::MB],
+                    FT (&nb_)[C::NBK]) {
+        __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, 0));
+        barrier();
+        const int ks = kt + C::NS < KT_ ? kt + C::NS : KT_ - 1;
+        char* lbase = lds + (kt % C::NS) * C::STAGE;          // the stage step kt vacated
+        const char* S = lds + ((kt + 1) % C::NS) * C::STAGE;  // step kt+1 (past the end: unused)
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            mfma_agpr<decltype(first)::value>(acc[i / C::MB][i % C::MB], cb[i / C::MB], ca[i % C::MB]);
+            if (i % R_EVERY == 0 && i / R_EVERY < NR) {
+                const int j = i / R_EVERY;
+                if (j < C::NBK) {
+                    if constexpr (MODE == kExpand) nb_[j] = *(const bf16x8*)b_at(S, j);
+                    else braw[j] = *(const bf16x8*)b_at(S, j);
+                } else {
+                    na[j - C::NBK] = Frag<MODE>::acts(a_at(S, j - C::NBK));
+                }
+            }
+            if (i % L_EVERY == 1 && i / L_EVERY < C::LPW) load(i / L_EVERY, ks, lbase);
+            if constexpr (MODE != kExpand) {
+                // one dword of weight fragment d / 4 per slot, well after its LDS read
+                const int d = i - W_FROM;
+                if (d >= 0 && d < 4 * C::NBK) {
+                    const uint4 q = __builtin_bit_cast(uint4, braw[d / 4]);
+                    const uint32_t wv = (d % 4 == 0) ? q.x : (d % 4 == 1) ? q.y : (d % 4 == 2) ? q.z : q.w;
+                    bw[d / 4][d % 4] = widen_pair_asm(wv);
+                    if (d % 4 == 3)
+                        nb_[d / 4] = __builtin_bit_cast(FT, uint4{bw[d / 4][0], bw[d / 4][1], bw[d / 4][2], bw[d / 4][3]});
+                }
+            }
         }
     };
 
-    // Ping-pong: waves 0..NW/2-1 (group 0) and NW/2..NW-1 (group 1) hold one wave per SIMD
-    // each and run half a step apart. Between two barriers one group issues its LDS
-    // fragment reads and the global->LDS loads of step kt+NS-1 ("M" phase) while the
-    // other issues the MFMAs of its previous step ("C" phase), so every SIMD alternates
-    // between its two waves' MFMA streams. Each step is read by group 0 in interval 2kt
-    // and by group 1 in interval 2kt+1; the stage it lived in is refilled only after both
-    // groups have finished reading it (each wave drains its LDS reads before the barrier
-    // that ends its M phase).
-    const bool g1 = wave >= C::NW / 2;
+    // prologue: NS steps in flight, step 0 landed, its fragments read
 #pragma unroll
-    for (int s = 0; s < C::NS - 1; ++s)
-        if (s < KT_) issue(s);
-    if (C::NS - 2 < KT_) __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, kNoLgkm));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, kNoLgkm));
-    barrier();                 // step 0 is in LDS for everyone
-    if (g1) barrier();         // group 1 starts half a step later
-    for (int kt = 0; kt < KT_; ++kt) {
-        // M phase
-        if (kt + C::NS - 1 < KT_) issue(kt + C::NS - 1);  // into the stage of step kt-1
-        read_frags(kt);
-        if (g1) wait_next_stage(kt, true);              // group 0 reads step kt+1 next
-        else __builtin_amdgcn_s_waitcnt(waitcnt_imm(kNoVm, 0));
-        barrier();
-        // C phase
-        mfmas();
-        if (!g1) wait_next_stage(kt, false);            // own step kt+1 before reading it
-        barrier();
+    for (int s = 0; s < C::NS; ++s)
+#pragma unroll
+        for (int q = 0; q < C::LPW; ++q) load(q, s < KT_ ? s : KT_ - 1, lds + s * C::STAGE);
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 1) * C::LPW, kNoLgkm));
+    barrier();
+#pragma unroll
+    for (int nb = 0; nb < C::NBK; ++nb) bf[0][nb] = Frag<MODE>::weights(b_at(lds, nb));
+#pragma unroll
+    for (int mb = 0; mb < C::MB; ++mb) af[0][mb] = Frag<MODE>::acts(a_at(lds, mb));
+    body(0, std::true_type{}, af[0], bf[0], af[1], bf[1]);
+    body(1, std::false_type{}, af[1], bf[1], af[0], bf[0]);
+    for (int kt = 2; kt < KT_; kt += 2) {
+        body(kt, std::false_type{}, af[0], bf[0], af[1], bf[1]);
+        body(kt + 1, std::false_type{}, af[1], bf[1], af[0], bf[0]);
     }
-    if (!g1) barrier();        // both groups pass the same number of barriers
+    // no load still writing LDS at exit; the MFMA results are complete before VALU reads them
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
     GemmArgs gs = g;
     if (kslice) gs.out = (float*)g.out + (int64_t)kslice * g.rows_total * g.N;
     epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(gs, acc, row0, row1, ntile, wm, wn, lane);
@@ -561,7 +601,7 @@ __global__ __launch_bounds__(SWAVES * 64) void gemm_stream_kernel(GemmArgs g, in
         if (f >= N) return;
         float v[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = acc[0][i] / (1.0f + __expf(-acc[0][i])) * acc[1][i];
+        for (int i = 0; i < 4; ++i) v[i] = silu(acc[0][i]) * acc[1][i];
         *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
     } else {
         const float sc = g.row_scale ? g.row_scale[r] : 1.0f;
@@ -591,11 +631,11 @@ hipError_t launch_stream(const GemmArgs& g, int64_t R, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------- launch
-template <class C, int MODE, bool DMA>
+template <class C, int MODE, bool IL>
 hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     const void* fn;
-    if constexpr (DMA)
-        fn = (const void*)gemm_dma_kernel<C, MODE>;
+    if constexpr (IL)
+        fn = (const void*)gemm_il_kernel<C, MODE>;
     else
         fn = (const void*)gemm_staged_kernel<C, MODE>;
     static bool attr_set = false;  // idempotent; a race only repeats the same call
@@ -614,8 +654,8 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
         const int v = env ? atoi(env) : 4;
         return v > 0 ? v : 4;
     }();
-    if constexpr (DMA)
-        gemm_dma_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
+    if constexpr (IL)
+        gemm_il_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
     else
         gemm_staged_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
     return hipGetLastError();
@@ -638,7 +678,7 @@ int down_ksplit(int64_t R, int n, int H, int F) {
     // only the large-tile kernel slices K; its grid is (R/256 + n) x (H/256) tiles
     if (pick_tile(R, n) != 'L') return 1;
     const int64_t tiles = (ceil_div(R, 256) + n) * ceil_div(H, 256);
-    return (tiles < 4 * 256 && (F / 2) % 32 == 0 && F / 32 >= 128) ? 2 : 1;
+    return (tiles < 4 * 256 && (F / 2) % 64 == 0 && F / 32 >= 128) ? 2 : 1;
 }
 
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStream_t s) {
@@ -650,15 +690,15 @@ hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStr
         case kExpand:
             if (t == 'S') return launch_stream<kExpand>(g, R, s);
             if (t == 'M') return launch_cfg<MediumStaged, kExpand, false>(g, R, s);
-            return launch_cfg<LargeDma, kExpand, true>(g, R, s);
+            return launch_cfg<LargeIl, kExpand, true>(g, R, s);
         case kDownStore:
             if (t == 'S') return launch_stream<kDownStore>(g, R, s);
             if (t == 'M') return launch_cfg<MediumStaged, kDownStore, false>(g, R, s);
-            return launch_cfg<LargeDma, kDownStore, true>(g, R, s);
+            return launch_cfg<LargeIl, kDownStore, true>(g, R, s);
         default:
             if (t == 'S') return launch_stream<kDownAccum>(g, R, s);
             if (t == 'M') return launch_cfg<MediumStaged, kDownAccum, false>(g, R, s);
-            return launch_cfg<LargeDma, kDownAccum, true>(g, R, s);
+            return launch_cfg<LargeIl, kDownAccum, true>(g, R, s);
     }
 }
 
