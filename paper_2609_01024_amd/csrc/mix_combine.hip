@@ -143,6 +143,103 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
     }
 }
 
+// Single-pass form of the float16 mix: each thread keeps its ITER column chunks of every
+// target row in registers (KK >= k targets), so U is read once; then the row maxima are
+// reduced over the workgroup and the scaled rows stored.
+template <int KK, int ITER>
+__global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict__ u,
+                                                        uint16_t* __restrict__ z,
+                                                        float* __restrict__ zscale,
+                                                        const uint64_t* __restrict__ bits,
+                                                        const float* __restrict__ beta,
+                                                        const int32_t* __restrict__ row_of, int k,
+                                                        int F, int64_t R) {
+    const int64_t t = blockIdx.x;
+    const TokenPaths p = token_paths(bits, beta, row_of, t, k, R);
+    float zz[ITER][KK][8];
+    float mx[KK];
+#pragma unroll
+    for (int b = 0; b < KK; ++b) mx[b] = 0.f;
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+#pragma unroll
+        for (int b = 0; b < KK; ++b)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) zz[it][b][i] = 0.f;
+        const int c = (threadIdx.x + it * blockDim.x) * 8;
+        if (c >= F) continue;
+        // sources in ascending order, each row's 8 values added to every target it feeds
+#pragma unroll
+        for (int a = 0; a < KK; ++a) {
+            if (a >= p.k) break;
+            float ua[8];
+            load8(u + p.rows[a] * F + c, ua);
+#pragma unroll
+            for (int b = 0; b < KK; ++b) {
+                if (b < p.k && ((p.bits >> (a * p.k + b)) & 1)) {
+                    const float w = p.beta ? p.beta[a * p.k + b] : 1.0f;
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) zz[it][b][i] = fmaf(w, ua[i], zz[it][b][i]);
+                }
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < KK; ++b)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) mx[b] = fmaxf(mx[b], fabsf(zz[it][b][i]));
+    }
+    __shared__ float red[KK][16];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int b = 0; b < KK; ++b) {
+        float v = mx[b];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+        if (lane == 0) red[b][wave] = v;
+    }
+    __syncthreads();
+    const int nw = (blockDim.x + 63) / 64;
+    float scale[KK];
+#pragma unroll
+    for (int b = 0; b < KK; ++b) {
+        float v = 0.f;
+        for (int w = 0; w < nw; ++w) v = fmaxf(v, red[b][w]);
+        // scale = 2^(kZScaleExp - e) with v < 2^e, so every |z * scale| < 2^kZScaleExp
+        int e = 0;
+        if (v > 0.f) frexpf(v, &e);
+        int sh = kZScaleExp - e;
+        sh = sh > 126 ? 126 : (sh < -126 ? -126 : sh);
+        scale[b] = ldexpf(1.0f, sh);
+        if (threadIdx.x == 0 && b < p.k) zscale[p.rows[b]] = ldexpf(1.0f, -sh);
+    }
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+        const int c = (threadIdx.x + it * blockDim.x) * 8;
+        if (c >= F) continue;
+#pragma unroll
+        for (int b = 0; b < KK; ++b) {
+            if (b >= p.k) break;
+            uint32_t w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const _Float16 lo = (_Float16)(zz[it][b][2 * i] * scale[b]);
+                const _Float16 hi = (_Float16)(zz[it][b][2 * i + 1] * scale[b]);
+                w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) |
+                       ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+            }
+            *(uint4*)(z + p.rows[b] * F + c) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+}
+
+template <int KK, int ITER>
+void launch_mix_regs(unsigned blocks, int threads, const float* u, void* z, float* zscale,
+                     const uint64_t* bits, const float* beta, const int32_t* row_of, int k, int F,
+                     int64_t R, hipStream_t s) {
+    mix_regs_kernel<KK, ITER><<<blocks, threads, 0, s>>>(u, (uint16_t*)z, zscale, bits, beta,
+                                                         row_of, k, F, R);
+}
+
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o, int ksplit,
                                                       const int32_t* __restrict__ row_of, int k,
                                                       int H, int64_t R, float* __restrict__ y,
@@ -181,9 +278,35 @@ hipError_t launch_mix(const float* u, void* z, float* zscale, const uint64_t* bi
     if (T == 0) return hipSuccess;
     const int threads = F / 8 >= 256 ? 256 : ((F / 8 + 63) / 64) * 64;
     const int64_t R = bits ? T * k : T;
-    if (zscale)
+    if (zscale) {
+        // single pass when a thread's share of every target row fits in 64 registers
+        const int chunks = F / 8;
+        const int threads_r = chunks >= 1024 ? 1024 : ((chunks + 63) / 64) * 64;
+        const int iter = (chunks + threads_r - 1) / threads_r;
+        const int kk = k <= 1 ? 1 : (k <= 2 ? 2 : (k <= 4 ? 4 : 8));
+        const int it = iter <= 1 ? 1 : (iter <= 2 ? 2 : (iter <= 4 ? 4 : (iter <= 8 ? 8 : 16)));  // 16: two-pass
+        const unsigned blocks = (unsigned)T;
+        if (kk * it <= 8) {
+            auto go = [&](auto fn) {
+                fn(blocks, threads_r, u, z, zscale, bits, beta, row_of, k, F, R, s);
+                return hipGetLastError();
+            };
+            switch (kk * 100 + it) {
+                case 101: return go(launch_mix_regs<1, 1>);
+                case 102: return go(launch_mix_regs<1, 2>);
+                case 104: return go(launch_mix_regs<1, 4>);
+                case 108: return go(launch_mix_regs<1, 8>);
+                case 201: return go(launch_mix_regs<2, 1>);
+                case 202: return go(launch_mix_regs<2, 2>);
+                case 204: return go(launch_mix_regs<2, 4>);
+                case 401: return go(launch_mix_regs<4, 1>);
+                case 402: return go(launch_mix_regs<4, 2>);
+                case 801: return go(launch_mix_regs<8, 1>);
+                default: break;
+            }
+        }
         mix_kernel<true><<<(unsigned)T, threads, 0, s>>>(u, z, zscale, bits, beta, row_of, k, F, R);
-    else
+    } else
         mix_kernel<false><<<(unsigned)T, threads, 0, s>>>(u, z, zscale, bits, beta, row_of, k, F, R);
     return hipGetLastError();
 }
