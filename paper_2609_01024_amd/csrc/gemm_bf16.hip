@@ -243,7 +243,7 @@ struct ICfg {
     static_assert(NS >= 2 && (NS - 1) * LPW <= 63, "vmcnt range");
 };
 
-using LargeIl = ICfg<256, 256, 2, 2, 4>;
+using LargeIl = ICfg<256, 256, 2, 2, 3>;
 
 // MFMA through inline assembly with the accumulator pinned to AGPRs ("a" constraint):
 // 256 accumulators per lane exceed what the compiler keeps in AGPRs across a loop without
@@ -336,7 +336,7 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
     };
     constexpr int NM = C::NBK * C::MB;        // MFMAs per k-step
     constexpr int NR = C::NBK + C::MB;        // fragment reads per k-step
-    constexpr int R_EVERY = 3, L_EVERY = 6, W_FROM = R_EVERY * C::NBK + 2;
+    constexpr int R_EVERY = 3, L_EVERY = 8, W_FROM = R_EVERY * C::NBK + 2;
     static_assert(R_EVERY * (NR - 1) < NM && L_EVERY * (C::LPW - 1) + 1 < NM, "slots");
     static_assert(W_FROM + 4 * C::NBK <= NM, "widen slots");
     // One k-step. Every step issues LPW loads (past the last step they re-read the last
