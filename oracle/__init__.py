@@ -53,8 +53,16 @@ def lib(path: str = _LIB) -> ctypes.CDLL:
     L.pcmo_expansion_rows.argtypes = [I, P, P, P, I64, I, I, I, P, P, I64, P]
     L.pcmo_dense_swiglu_tokens.argtypes = [I, P, P, P, P, I64, I, I, P, I64, P]
     L.pcmo_set_num_threads.argtypes = [I]
+    Fl = ctypes.c_float
+    L.pcmo_route_scored.argtypes = [P, P, Fl, P, P, I64, I, I, P, P, P, P]
+    L.pcmo_group_scored.argtypes = [P, P, P, I64, I, P, P, P, P, P, P]
+    L.pcmo_permute_var.argtypes = [P, P, I64, I, I, P, P, P, P]
+    L.pcmo_layer_scored_tokens.argtypes = [I, P, P, P, Fl, P, P, P, P, P, I64, I, I, I, I, I, P,
+                                           I64, P]
     for name in ("pcmo_route", "pcmo_paths", "pcmo_permute", "pcmo_layer_tokens",
-                 "pcmo_expansion_rows", "pcmo_dense_swiglu_tokens", "pcmo_num_threads"):
+                 "pcmo_expansion_rows", "pcmo_dense_swiglu_tokens", "pcmo_num_threads",
+                 "pcmo_route_scored", "pcmo_group_scored", "pcmo_permute_var",
+                 "pcmo_layer_scored_tokens"):
         getattr(L, name).restype = I
     if path == _LIB:
         _lib = L
@@ -193,4 +201,86 @@ def layer_inputs(inp, tokens=None, beta_mode: int = BETA_SRC_COND, reuse: bool =
               beta_mode=beta_mode, reuse=reuse, tokens=tokens)
     if inp.s_gate is not None:
         y = y + dense_swiglu(inp.x, inp.s_gate, inp.s_up, inp.s_down, tokens=tokens)
+    return y
+
+
+# ------------------------------------------------------------- scored routing
+def route_scored(g_base, g_tgt, lam: float, bias, mask, K: int, L=None):
+    """Selected paths of every token in selection order: src[T,K], tgt[T,K],
+    score[T,K] (float32) and beta[T,K] (float64, softmax of the selected scores)."""
+    L = L or lib()
+    gb = np.ascontiguousarray(g_base, dtype=np.float32)
+    gt = np.ascontiguousarray(g_tgt, dtype=np.float32)
+    b = np.ascontiguousarray(bias, dtype=np.float32)
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    T, n = gb.shape
+    src = np.empty((T, K), np.int32)
+    tgt = np.empty((T, K), np.int32)
+    score = np.empty((T, K), np.float32)
+    beta = np.empty((T, K), np.float64)
+    _check(L.pcmo_route_scored(_ptr(gb), _ptr(gt), float(lam), _ptr(b), _ptr(m), T, n, K, _ptr(src),
+                               _ptr(tgt), _ptr(score), _ptr(beta)), "route_scored")
+    return src, tgt, score, beta
+
+
+def group_scored(src, tgt, beta, L=None):
+    """Source and target groups: n_src[T], srcs[T,K], n_tgt[T], tgts[T,K] (ascending,
+    -1 padded), bits[T] (bit a*K+b: path srcs[a] -> tgts[b]) and beta_g[T,K,K]."""
+    L = L or lib()
+    src = np.ascontiguousarray(src, np.int32)
+    tgt = np.ascontiguousarray(tgt, np.int32)
+    beta = np.ascontiguousarray(beta, np.float64)
+    T, K = src.shape
+    n_src = np.empty((T,), np.int32)
+    srcs = np.empty((T, K), np.int32)
+    n_tgt = np.empty((T,), np.int32)
+    tgts = np.empty((T, K), np.int32)
+    bits = np.empty((T,), np.uint64)
+    beta_g = np.empty((T, K, K), np.float64)
+    _check(L.pcmo_group_scored(_ptr(src), _ptr(tgt), _ptr(beta), T, K, _ptr(n_src), _ptr(srcs),
+                               _ptr(n_tgt), _ptr(tgts), _ptr(bits), _ptr(beta_g)), "group_scored")
+    return n_src, srcs, n_tgt, tgts, bits, beta_g
+
+
+def permute_var(ids, counts, n: int, L=None):
+    """Dispatch layout for counts[t] <= K entries per token: expert_offsets[n+1],
+    row_token[R], row_slot[R], row_of[T,K] (-1 for unused slots), R = sum(counts)."""
+    L = L or lib()
+    ids = np.ascontiguousarray(ids, np.int32)
+    counts = np.ascontiguousarray(counts, np.int32)
+    T, K = ids.shape
+    R = int(counts.sum())
+    offsets = np.empty((n + 1,), np.int32)
+    row_token = np.empty((max(R, 1),), np.int32)
+    row_slot = np.empty((max(R, 1),), np.int32)
+    row_of = np.empty((T * K,), np.int32)
+    _check(L.pcmo_permute_var(_ptr(ids), _ptr(counts), T, n, K, _ptr(offsets), _ptr(row_token),
+                              _ptr(row_slot), _ptr(row_of)), "permute_var")
+    return offsets, row_token[:R], row_slot[:R], row_of.reshape(T, K)
+
+
+def layer_scored(x, g_base, g_tgt, lam: float, bias, mask, w_gate, w_up, w_down, K: int,
+                 reuse: bool = True, tokens=None, L=None) -> np.ndarray:
+    """y[tokens] of the layer under scored routing, float64; tokens=None: every token."""
+    L = L or lib()
+    xh, dt = _host(x)
+    wg, dtg = _host(w_gate)
+    wu, dtu = _host(w_up)
+    wd, dtd = _host(w_down)
+    if not (dt == dtg == dtu == dtd):
+        raise ValueError("x and the weights must share one dtype")
+    gb = np.ascontiguousarray(g_base, dtype=np.float32)
+    gt = np.ascontiguousarray(g_tgt, dtype=np.float32)
+    b = np.ascontiguousarray(bias, dtype=np.float32)
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    T, H = xh.shape
+    n, F, H2 = wg.shape
+    if H2 != H or wd.shape != (n, H, F) or gb.shape != (T, n) or gt.shape != (T, n) \
+            or b.shape != (n, n) or m.shape != (n, n):
+        raise ValueError("shape mismatch")
+    tok = np.arange(T, dtype=np.int64) if tokens is None else np.ascontiguousarray(tokens, np.int64)
+    y = np.empty((tok.size, H), np.float64)
+    _check(L.pcmo_layer_scored_tokens(dt, _ptr(xh), _ptr(gb), _ptr(gt), float(lam), _ptr(b), _ptr(m),
+                                      _ptr(wg), _ptr(wu), _ptr(wd), T, H, F, n, K, int(bool(reuse)),
+                                      _ptr(tok), tok.size, _ptr(y)), "layer_scored")
     return y

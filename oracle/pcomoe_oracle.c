@@ -310,3 +310,214 @@ int pcmo_dense_swiglu_tokens(int dtype, const void* x, const void* wg, const voi
     }
     return failed ? ORC_NO_MEM : ORC_OK;
 }
+
+/* ---------------------------------------------------------------------------------
+ * Scored compositional routing: the router the paper runs at inference.
+ *
+ *   s_ij = g_base_i + b_ij + lambda g_tgt_j                (Section 4.2, path score)
+ *   Pi   = the K highest s_ij over A = {(i, j) : m_ij = 1}, with m_ii = 1
+ *                                                          (Section 4.3, TopK over A)
+ *   S    = {i : (i, j) in Pi},  T_i = {j : (i, j) in Pi}  (Section 4.3)
+ *   y    = sum_{i in S} sum_{j in T_i} beta_ij D_j(U_i(h)) (Section 4.3)
+ *
+ * Readings where the paper is silent (listed in the design notes):
+ *   - the score is formed in float32 as fmaf(lambda, g_tgt_j, g_base_i + b_ij), so that
+ *     every implementation takes the selection on identical values;
+ *   - equal scores go to the lower flattened index i*n + j;
+ *   - beta is the softmax of the K selected scores;
+ *   - K <= n, which keeps K <= |A| because every diagonal pair is active.
+ * --------------------------------------------------------------------------------- */
+
+static float path_score(const float* gb, const float* gt, const float* bias, float lambda, int n,
+                        int i, int j) {
+    return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)i * n + j]);
+}
+
+/* One token: src[K], tgt[K] and score[K] of the selected paths in selection order
+ * (score descending, ties to the lower i*n + j), beta[K] their softmax weights. */
+static int route_scored_one(const float* gb, const float* gt, float lambda, const float* bias,
+                            const uint8_t* mask, int n, int K, int32_t* src, int32_t* tgt,
+                            float* score, double* beta) {
+    unsigned char* taken = (unsigned char*)calloc((size_t)n * n, 1);
+    if (!taken) return ORC_NO_MEM;
+    for (int r = 0; r < K; ++r) {
+        int bi = -1, bj = -1;
+        float bs = 0.0f;
+        for (int i = 0; i < n; ++i)
+            for (int j = 0; j < n; ++j) {
+                if (i != j && !mask[(int64_t)i * n + j]) continue;   /* outside A */
+                if (taken[(int64_t)i * n + j]) continue;
+                float s = path_score(gb, gt, bias, lambda, n, i, j);
+                if (bi < 0 || s > bs) { bi = i; bj = j; bs = s; }    /* first of equals wins */
+            }
+        src[r] = bi;
+        tgt[r] = bj;
+        score[r] = bs;
+        taken[(int64_t)bi * n + bj] = 1;
+    }
+    free(taken);
+    double top = (double)score[0], sum = 0.0;
+    for (int r = 0; r < K; ++r) sum += exp((double)score[r] - top);
+    for (int r = 0; r < K; ++r) beta[r] = exp((double)score[r] - top) / sum;
+    return ORC_OK;
+}
+
+static int check_scored(int64_t T, int n, int K) {
+    if (T < 0 || n < 1 || K < 1 || K > n || K > ORC_MAX_K) return ORC_BAD_ARG;
+    return ORC_OK;
+}
+
+/* Routing of T tokens: sel_src[T,K], sel_tgt[T,K], sel_score[T,K] (float), beta[T,K].
+ * g_base, g_tgt [T,n]; bias [n,n]; mask [n,n] (row = source i, column = target j). */
+int pcmo_route_scored(const float* g_base, const float* g_tgt, float lambda, const float* bias,
+                      const uint8_t* mask, int64_t T, int n, int K, int32_t* sel_src,
+                      int32_t* sel_tgt, float* sel_score, double* beta) {
+    int st = check_scored(T, n, K);
+    if (st) return st;
+    int failed = 0;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t)
+        if (route_scored_one(g_base + t * n, g_tgt + t * n, lambda, bias, mask, n, K,
+                             sel_src + t * K, sel_tgt + t * K, sel_score + t * K, beta + t * K))
+#pragma omp atomic write
+            failed = 1;
+    return failed ? ORC_NO_MEM : ORC_OK;
+}
+
+/* Source and target groups of each token's selected paths (Section 4.3): the sources S
+ * and the targets, each in ascending expert order (n_src[t], srcs[t, 0..n_src), and
+ * n_tgt[t], tgts[t, 0..n_tgt)); bit a*K + b of bits[t] marks the path (srcs[a], tgts[b])
+ * and beta_g[t, a, b] is its weight (0 off-path). */
+int pcmo_group_scored(const int32_t* sel_src, const int32_t* sel_tgt, const double* beta, int64_t T,
+                      int K, int32_t* n_src, int32_t* srcs, int32_t* n_tgt, int32_t* tgts,
+                      uint64_t* bits, double* beta_g) {
+    if (T < 0 || K < 1 || K > ORC_MAX_K) return ORC_BAD_ARG;
+    for (int64_t t = 0; t < T; ++t) {
+        const int32_t* ps = sel_src + t * K;
+        const int32_t* pt = sel_tgt + t * K;
+        int32_t* S = srcs + t * K;
+        int32_t* G = tgts + t * K;
+        int ns = 0, ng = 0;
+        for (int r = 0; r < K; ++r) {         /* distinct values, kept sorted ascending */
+            int v = ps[r], pos = 0, dup = 0;
+            for (int q = 0; q < ns; ++q) { if (S[q] == v) dup = 1; if (S[q] < v) pos = q + 1; }
+            if (!dup) { for (int q = ns; q > pos; --q) S[q] = S[q - 1]; S[pos] = v; ++ns; }
+            v = pt[r]; pos = 0; dup = 0;
+            for (int q = 0; q < ng; ++q) { if (G[q] == v) dup = 1; if (G[q] < v) pos = q + 1; }
+            if (!dup) { for (int q = ng; q > pos; --q) G[q] = G[q - 1]; G[pos] = v; ++ng; }
+        }
+        for (int q = ns; q < K; ++q) S[q] = -1;
+        for (int q = ng; q < K; ++q) G[q] = -1;
+        n_src[t] = ns;
+        n_tgt[t] = ng;
+        uint64_t b64 = 0;
+        double* bg = beta_g + t * K * K;
+        for (int q = 0; q < K * K; ++q) bg[q] = 0.0;
+        for (int r = 0; r < K; ++r) {
+            int a = 0, b = 0;
+            while (S[a] != ps[r]) ++a;
+            while (G[b] != pt[r]) ++b;
+            b64 |= (uint64_t)1 << (a * K + b);
+            bg[a * K + b] = beta[t * K + r];
+        }
+        bits[t] = b64;
+    }
+    return ORC_OK;
+}
+
+/* Grouped dispatch with a variable number of entries per token: token t contributes
+ * counts[t] <= K entries ids[t, 0..counts[t]) (distinct experts). Rows are ordered by
+ * (expert ascending, token ascending); row_of[t, a] = -1 for a >= counts[t]. */
+int pcmo_permute_var(const int32_t* ids, const int32_t* counts, int64_t T, int n, int K,
+                     int32_t* expert_offsets, int32_t* row_token, int32_t* row_slot,
+                     int32_t* row_of) {
+    if (T < 0 || n < 1 || K < 1) return ORC_BAD_ARG;
+    int64_t* cursor = (int64_t*)calloc((size_t)n + 1, sizeof(int64_t));
+    if (!cursor) return ORC_NO_MEM;
+    for (int64_t t = 0; t < T; ++t) {
+        if (counts[t] < 0 || counts[t] > K) { free(cursor); return ORC_BAD_ARG; }
+        for (int a = 0; a < counts[t]; ++a) {
+            int e = ids[t * K + a];
+            if (e < 0 || e >= n) { free(cursor); return ORC_BAD_ARG; }
+            cursor[e + 1]++;
+        }
+    }
+    for (int e = 0; e < n; ++e) cursor[e + 1] += cursor[e];
+    for (int e = 0; e <= n; ++e) expert_offsets[e] = (int32_t)cursor[e];
+    for (int64_t t = 0; t < T; ++t)
+        for (int a = 0; a < K; ++a) {
+            if (a >= counts[t]) { row_of[t * K + a] = -1; continue; }
+            int64_t r = cursor[ids[t * K + a]]++;
+            row_token[r] = (int32_t)t;
+            row_slot[r] = (int32_t)a;
+            row_of[t * K + a] = (int32_t)r;
+        }
+    free(cursor);
+    return ORC_OK;
+}
+
+/* Layer output of selected tokens under scored routing:
+ * y = sum over the selected paths r of beta_r D_{tgt_r}(U_{src_r}(x_t)), visited in
+ * selection order.
+ *   reuse = 0: U is re-evaluated for every path;
+ *   reuse = 1: U is evaluated once per distinct source and reused (Section 4.3).
+ * Both use the same arithmetic, so their results are bit-identical. */
+int pcmo_layer_scored_tokens(int dtype, const void* x, const float* g_base, const float* g_tgt,
+                             float lambda, const float* bias, const uint8_t* mask,
+                             const void* w_gate, const void* w_up, const void* w_down, int64_t T,
+                             int H, int F, int n, int K, int reuse, const int64_t* tokens,
+                             int64_t ntok, double* y_out) {
+    int st = check_scored(T, n, K);
+    if (st) return st;
+    if (H < 1 || F < 1 || (dtype != ORC_F32 && dtype != ORC_BF16)) return ORC_BAD_ARG;
+    for (int64_t i = 0; i < ntok; ++i)
+        if (tokens[i] < 0 || tokens[i] >= T) return ORC_BAD_ARG;
+    int failed = 0;
+#pragma omp parallel
+    {
+        double* U = (double*)malloc(sizeof(double) * (size_t)F * K);
+        double* P = (double*)malloc(sizeof(double) * (size_t)H);
+        if (!U || !P) {
+#pragma omp atomic write
+            failed = 1;
+        } else {
+#pragma omp for schedule(dynamic, 1)
+            for (int64_t i = 0; i < ntok; ++i) {
+                int64_t t = tokens[i];
+                int32_t src[ORC_MAX_K], tgt[ORC_MAX_K], have[ORC_MAX_K];
+                float score[ORC_MAX_K];
+                double beta[ORC_MAX_K];
+                if (route_scored_one(g_base + t * n, g_tgt + t * n, lambda, bias, mask, n, K, src,
+                                     tgt, score, beta)) {
+#pragma omp atomic write
+                    failed = 1;
+                    continue;
+                }
+                double* y = y_out + i * H;
+                for (int m = 0; m < H; ++m) y[m] = 0.0;
+                int nhave = 0;
+                for (int r = 0; r < K; ++r) {
+                    const double* Ui = U;
+                    if (reuse) {
+                        int slot = -1;
+                        for (int q = 0; q < nhave; ++q) if (have[q] == src[r]) slot = q;
+                        if (slot < 0) {
+                            slot = nhave++;
+                            have[slot] = src[r];
+                            expansion(dtype, x, t * H, w_gate, w_up, (int64_t)src[r] * F * H, H, F,
+                                      U + (int64_t)slot * F);
+                        }
+                        Ui = U + (int64_t)slot * F;
+                    } else {
+                        expansion(dtype, x, t * H, w_gate, w_up, (int64_t)src[r] * F * H, H, F, U);
+                    }
+                    projection(dtype, w_down, (int64_t)tgt[r] * H * F, H, F, Ui, P);
+                    for (int m = 0; m < H; ++m) y[m] += beta[r] * P[m];
+                }
+            }
+        }
+        free(U);
+        free(P);
+    }
+    return failed ? ORC_NO_MEM : ORC_OK;
+}

@@ -299,7 +299,206 @@ def pin_edge_cases(L):
     assert st != 0, "k > 8 must be rejected"
 
 
+# ------------------------------------------------------------ scored routing
+def eq9_bias(n, c=-1.0, noise=0.5, quant=None):
+    """Compatibility bias of Section 4.2's initialisation: b_ii = 0, b_ij = c + eps with
+    bounded uniform noise; quant rounds to a grid (exact float32 ties)."""
+    b = (c + RNG.uniform(-noise, noise, (n, n))).astype(np.float32)
+    if quant:
+        b = (np.round(b / quant) * quant).astype(np.float32)
+    np.fill_diagonal(b, 0.0)
+    return b
+
+
+def bruteforce_scored(gb, gt, lam, bias, mask, K):
+    """Every token: the full n x n score matrix (float32; lam is a power of two so
+    lam * g_tgt is exact and the sum is a single float32 rounding, as in fmaf), inactive
+    pairs at -inf, then a stable sort of the flattened matrix by descending score: the
+    first K entries, ties to the lower i*n + j. Returns src, tgt, score, beta."""
+    T, n = gb.shape
+    active = (mask != 0) | np.eye(n, dtype=bool)
+    src = np.empty((T, K), np.int32); tgt = np.empty((T, K), np.int32)
+    sc = np.empty((T, K), np.float32); beta = np.empty((T, K))
+    for t in range(T):
+        s = (gb[t][:, None] + bias).astype(np.float32) + np.float32(lam) * gt[t][None, :]
+        s = s.astype(np.float32)
+        flat = np.where(active, s, -np.inf).ravel()
+        order = np.argsort(-flat.astype(np.float64), kind="stable")[:K]
+        src[t], tgt[t] = order // n, order % n
+        sc[t] = flat[order]
+        e = np.exp(sc[t].astype(np.float64) - sc[t, 0])
+        beta[t] = e / e.sum()
+    return src, tgt, sc, beta
+
+
+def dense_scored_layer(x, wg, wu, wd, src, tgt, beta):
+    """All U_i and all P_ij per token, then y = sum over the selected paths of beta P_ij."""
+    x = np.asarray(x, np.float64)
+    G = np.einsum("th,nfh->tnf", x, wg)
+    Uall = G / (1.0 + np.exp(-G)) * np.einsum("th,nfh->tnf", x, wu)
+    P = np.einsum("jhf,tif->tijh", wd, Uall)
+    T = x.shape[0]
+    return np.stack([sum(beta[t, r] * P[t, src[t, r], tgt[t, r]] for r in range(src.shape[1]))
+                     for t in range(T)])
+
+
+def pin_scored_bruteforce(L):
+    cases = [(7, 16, 8, 8, 2, 0.5, 0.5), (5, 8, 8, 16, 4, 0.3, 2.0), (6, 8, 16, 6, 6, 0.7, 0.0),
+             (4, 8, 8, 64, 8, 0.25, 0.5), (3, 8, 8, 3, 3, 1.0, 1.0)]
+    for T, H, F, n, K, d, lam in cases:
+        for quant in (None, 0.25):
+            x, _, wg, wu, wd, mask = rand_layer(T, H, F, n, K, d)
+            gb = RNG.standard_normal((T, n)).astype(np.float32)
+            gt = RNG.standard_normal((T, n)).astype(np.float32)
+            if quant:
+                gb = (np.round(gb / quant) * quant).astype(np.float32)
+                gt = (np.round(gt / quant) * quant).astype(np.float32)
+            bias = eq9_bias(n, quant=quant)
+            m0 = mask.copy(); np.fill_diagonal(m0, 0)      # a zero diagonal is overridden
+            src, tgt, sc, beta = oracle.route_scored(gb, gt, lam, bias, m0, K, L=L)
+            rs, rt, rsc, rb = bruteforce_scored(gb, gt, lam, bias, m0, K)
+            what = f"T={T} n={n} K={K} lam={lam} quant={quant}"
+            assert np.array_equal(src, rs) and np.array_equal(tgt, rt), f"selected paths {what}"
+            assert np.array_equal(sc, rsc), f"scores {what}"
+            _close(beta, rb, 1e-14, f"beta {what}")
+            y = oracle.layer_scored(x, gb, gt, lam, bias, m0, wg, wu, wd, K, L=L)
+            ref = dense_scored_layer(x, wg, wu, wd, rs, rt, rb)
+            _close(y, ref, 1e-12, f"layer vs brute force {what}")
+
+
+def pin_scored_reduces_to_vanilla(L):
+    """Only diagonal paths, no target prior: the router is the vanilla top-K with the
+    renormalised softmax, and the layer is the standard top-k MoE (Section 4.1)."""
+    T, H, F, n, K = 9, 32, 16, 8, 3
+    x, l, wg, wu, wd, _ = rand_layer(T, H, F, n, K, 0.0)
+    eye = np.eye(n, dtype=np.uint8)
+    gt = RNG.standard_normal((T, n)).astype(np.float32)
+    bias = eq9_bias(n)
+    src, tgt, _, beta = oracle.route_scored(l, gt, 0.0, bias, eye, K, L=L)
+    ids, p = softmax_renorm_topk(l, K)
+    assert np.array_equal(src, ids) and np.array_equal(tgt, ids), "diagonal top-K"
+    _close(beta, p, 1e-14, "beta = renormalised softmax")
+    y = oracle.layer_scored(x, l, gt, 0.0, bias, eye, wg, wu, wd, K, L=L)
+    f64 = lambda a: a.astype(np.float64)
+    ref = np.stack([sum(p[t, a] * textbook_swiglu(f64(x[t:t + 1]), f64(wg[e]), f64(wu[e]), f64(wd[e]))[0]
+                        for a, e in enumerate(ids[t])) for t in range(T)])
+    _close(y, ref, 1e-12, "scored routing with mask = I is the vanilla MoE")
+    # a very negative off-diagonal bias prunes like the mask
+    full = np.ones((n, n), np.uint8)
+    b2 = np.full((n, n), -1e4, np.float32); np.fill_diagonal(b2, 0.0)
+    src2, tgt2, _, beta2 = oracle.route_scored(l, gt, 0.0, b2, full, K, L=L)
+    assert np.array_equal(src2, ids) and np.array_equal(tgt2, ids), "bias pruning"
+    _close(beta2, p, 1e-14, "bias pruning beta")
+
+
+def pin_scored_single_source(L):
+    """All pairs active, zero bias, no target prior: s_ij = g_i, so the K paths are
+    (i*, 0), ..., (i*, K-1) of the top source, each with weight 1/K:
+    y = (1/K) sum_{j<K} W_down_j U_{i*}."""
+    T, H, F, n, K = 6, 16, 24, 8, 4
+    x, l, wg, wu, wd, _ = rand_layer(T, H, F, n, K, 1.0)
+    full = np.ones((n, n), np.uint8)
+    gt = RNG.standard_normal((T, n)).astype(np.float32)
+    zero = np.zeros((n, n), np.float32)
+    src, tgt, _, beta = oracle.route_scored(l, gt, 0.0, zero, full, K, L=L)
+    top = np.argmax(l, axis=1)
+    assert np.array_equal(src, np.repeat(top[:, None], K, 1)), "single source"
+    assert np.array_equal(tgt, np.tile(np.arange(K, dtype=np.int32), (T, 1))), "targets 0..K-1"
+    _close(beta, np.full((T, K), 1.0 / K), 1e-15, "uniform weights")
+    y = oracle.layer_scored(x, l, gt, 0.0, zero, full, wg, wu, wd, K, L=L)
+    ref = np.zeros((T, H))
+    for t in range(T):
+        xt, i = x[t].astype(np.float64), top[t]
+        g, u = wg[i].astype(np.float64) @ xt, wu[i].astype(np.float64) @ xt
+        U = g / (1 + np.exp(-g)) * u
+        ref[t] = sum(wd[j].astype(np.float64) @ U for j in range(K)) / K
+    _close(y, ref, 1e-12, "single-source closed form")
+
+
+def pin_scored_target_prior(L):
+    """A dominant target prior sends every selected path to its unique best target j*;
+    the sources are then the top-K of g_base_i + b_ij* (ties to the lower id)."""
+    T, n, K = 40, 16, 5
+    gb = RNG.standard_normal((T, n)).astype(np.float32)
+    gt = RNG.standard_normal((T, n)).astype(np.float32)
+    jstar = RNG.integers(0, n, T)
+    gt[np.arange(T), jstar] = 8.0
+    bias = eq9_bias(n)
+    full = np.ones((n, n), np.uint8)
+    src, tgt, _, _ = oracle.route_scored(gb, gt, 64.0, bias, full, K, L=L)
+    assert np.array_equal(tgt, np.repeat(jstar[:, None].astype(np.int32), K, 1)), "one target"
+    for t in range(T):
+        col = (gb[t] + bias[:, jstar[t]]).astype(np.float32)
+        assert list(src[t]) == list(np.argsort(-col.astype(np.float64), kind="stable")[:K]), "sources"
+
+
+def pin_scored_groups_and_dispatch(L):
+    for T, n, K, d in ((50, 8, 2, 0.5), (40, 64, 8, 0.25), (30, 256, 8, 0.2), (20, 6, 6, 1.0)):
+        gb = RNG.standard_normal((T, n)).astype(np.float32)
+        gt = RNG.standard_normal((T, n)).astype(np.float32)
+        mask = (RNG.random((n, n)) < d).astype(np.uint8)
+        bias = eq9_bias(n, noise=1.5)
+        src, tgt, _, beta = oracle.route_scored(gb, gt, 0.5, bias, mask, K, L=L)
+        _close(beta.sum(axis=1), np.ones(T), 1e-14, "weights sum to 1")
+        assert np.all(np.diff(beta, axis=1) <= 0), "weights follow the selection order"
+        n_src, srcs, n_tgt, tgts, bits, bg = oracle.group_scored(src, tgt, beta, L=L)
+        for t in range(T):
+            pairs = list(zip(src[t], tgt[t]))
+            assert len(set(pairs)) == K, "distinct paths"
+            assert all(i == j or mask[i, j] for i, j in pairs), "paths inside A"
+            S, G = sorted(set(src[t])), sorted(set(tgt[t]))
+            assert n_src[t] == len(S) and list(srcs[t, :len(S)]) == S, "sources"
+            assert n_tgt[t] == len(G) and list(tgts[t, :len(G)]) == G, "targets"
+            ref = 0
+            for r, (i, j) in enumerate(pairs):
+                a, b = S.index(i), G.index(j)
+                ref |= 1 << (a * K + b)
+                assert bg[t, a, b] == beta[t, r], "grouped weight"
+            assert int(bits[t]) == ref, "grouped bits"
+            assert abs(bg[t].sum() - 1.0) < 1e-14, "grouped weights sum to 1"
+        for ids, cnt in ((srcs, n_src), (tgts, n_tgt)):
+            off, rt, rs, ro = oracle.permute_var(ids, cnt, n, L=L)
+            entries = sorted((int(ids[t, a]), t, a) for t in range(T) for a in range(cnt[t]))
+            assert list(rt) == [t for _, t, _ in entries] and list(rs) == [a for _, _, a in entries]
+            counts = np.bincount([e for e, _, _ in entries], minlength=n)
+            assert list(off) == [0] + list(np.cumsum(counts)), "offsets"
+            for r, (_, t, a) in enumerate(entries):
+                assert ro[t, a] == r, "row_of"
+            assert all(ro[t, a] == -1 for t in range(T) for a in range(cnt[t], K)), "unused slots"
+    # reuse of U per source changes nothing
+    T, H, F, n, K = 5, 16, 16, 8, 4
+    x, _, wg, wu, wd, mask = rand_layer(T, H, F, n, K, 0.6)
+    gb = RNG.standard_normal((T, n)).astype(np.float32)
+    gt = RNG.standard_normal((T, n)).astype(np.float32)
+    bias = eq9_bias(n, noise=1.0)
+    y1 = oracle.layer_scored(x, gb, gt, 1.0, bias, mask, wg, wu, wd, K, reuse=True, L=L)
+    y0 = oracle.layer_scored(x, gb, gt, 1.0, bias, mask, wg, wu, wd, K, reuse=False, L=L)
+    assert np.array_equal(y0, y1), "reuse must be bit-identical"
+
+
+def pin_scored_relabel_and_edges(L):
+    T, H, F, n, K = 6, 16, 8, 10, 3
+    x, _, wg, wu, wd, mask = rand_layer(T, H, F, n, K, 0.5)
+    gb = RNG.standard_normal((T, n)).astype(np.float32)
+    gt = RNG.standard_normal((T, n)).astype(np.float32)
+    bias = eq9_bias(n, noise=1.0)
+    y = oracle.layer_scored(x, gb, gt, 0.5, bias, mask, wg, wu, wd, K, L=L)
+    perm = RNG.permutation(n)
+    inv = np.argsort(perm)
+    c = np.ascontiguousarray
+    y2 = oracle.layer_scored(x, c(gb[:, inv]), c(gt[:, inv]), 0.5, c(bias[np.ix_(inv, inv)]),
+                             c(mask[np.ix_(inv, inv)]), c(wg[inv]), c(wu[inv]), c(wd[inv]), K, L=L)
+    _close(y2, y, 1e-14, "expert relabelling")
+    src, _, _, _ = oracle.route_scored(np.zeros((0, n), np.float32), np.zeros((0, n), np.float32),
+                                       0.5, bias, mask, K, L=L)
+    assert src.shape == (0, K)
+    assert L.pcmo_route_scored(0, 0, 0.5, 0, 0, 1, 4, 5, 0, 0, 0, 0) != 0, "K > n must be rejected"
+    assert L.pcmo_route_scored(0, 0, 0.5, 0, 0, 1, 16, 9, 0, 0, 0, 0) != 0, "K > 8 must be rejected"
+
+
 ALL_PINS = [pin_topk_bruteforce, pin_path_bits_bruteforce, pin_beta_closed_forms,
             pin_permutation_bruteforce, pin_layer_bruteforce, pin_diagonal_is_vanilla_moe,
             pin_full_mask_closed_form, pin_k1_and_n1, pin_reuse_and_target_mix,
-            pin_expansion_rows, pin_relabel_invariance, pin_bf16_widening, pin_edge_cases]
+            pin_expansion_rows, pin_relabel_invariance, pin_bf16_widening, pin_edge_cases,
+            pin_scored_bruteforce, pin_scored_reduces_to_vanilla, pin_scored_single_source,
+            pin_scored_target_prior, pin_scored_groups_and_dispatch, pin_scored_relabel_and_edges]

@@ -45,6 +45,32 @@ MUTANTS = {
     "x_row_dropped": ("double xv = elem(x, dtype, x_off + h);", "double xv = elem(x, dtype, h);"),
     "reuse_wrong_source": ("const double* Ua = U + (reuse ? (int64_t)a * F : 0);",
                            "const double* Ua = U + (reuse ? (int64_t)b * F : 0);"),
+    # scored routing
+    "score_bias_transposed": ("return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)i * n + j]);",
+                              "return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)j * n + i]);"),
+    "score_target_prior_on_source": ("return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)i * n + j]);",
+                                     "return fmaf(lambda, gt[i], gb[i] + bias[(int64_t)i * n + j]);"),
+    "score_base_on_target": ("return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)i * n + j]);",
+                             "return fmaf(lambda, gt[j], gb[j] + bias[(int64_t)i * n + j]);"),
+    "scored_mask_ignored": ("if (i != j && !mask[(int64_t)i * n + j]) continue;   /* outside A */",
+                            "if (0) continue;"),
+    "scored_diagonal_not_forced": ("if (i != j && !mask[(int64_t)i * n + j]) continue;   /* outside A */",
+                                   "if (!mask[(int64_t)i * n + j]) continue;"),
+    "scored_tie_to_higher": ("if (bi < 0 || s > bs) { bi = i; bj = j; bs = s; }",
+                             "if (bi < 0 || s >= bs) { bi = i; bj = j; bs = s; }"),
+    "scored_beta_unnormalised": ("for (int r = 0; r < K; ++r) beta[r] = exp((double)score[r] - top) / sum;",
+                                 "for (int r = 0; r < K; ++r) beta[r] = exp((double)score[r] - top);"),
+    "scored_beta_linear": ("for (int r = 0; r < K; ++r) beta[r] = exp((double)score[r] - top) / sum;",
+                           "for (int r = 0; r < K; ++r) beta[r] = 1.0 / K;"),
+    "group_bits_transposed": ("b64 |= (uint64_t)1 << (a * K + b);", "b64 |= (uint64_t)1 << (b * K + a);"),
+    "group_targets_unsorted": ("if (G[q] < v) pos = q + 1; }", "pos = q + 1; }"),
+    "scored_down_uses_source": ("projection(dtype, w_down, (int64_t)tgt[r] * H * F, H, F, Ui, P);",
+                                "projection(dtype, w_down, (int64_t)src[r] * H * F, H, F, Ui, P);"),
+    "scored_reuse_wrong_slot": ("Ui = U + (int64_t)slot * F;", "Ui = U;"),
+    "permute_var_offsets_shifted": ("cursor[e + 1]++;", "cursor[e]++;"),
+    "permute_var_slot_reversed": ("row_slot[r] = (int32_t)a;", "row_slot[r] = (int32_t)(K - 1 - a);"),
+    "permute_var_stale_slot": ("if (a >= counts[t]) { row_of[t * K + a] = -1; continue; }",
+                               "if (a >= counts[t]) { row_of[t * K + a] = 0; continue; }"),
 }
 
 

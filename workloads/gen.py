@@ -18,6 +18,13 @@ Distributions ("N(0, s)" means standard deviation s):
                +one_expert: expert 0's logit raised by 100 for every token
   mask         each off-diagonal entry 1 with probability `density`, diagonal 1, uint8 [n, n]
                (row = expansion source i, column = projection target j)
+
+Scored compositional routing (make_scored_inputs) adds:
+  g_tgt        N(0, 1)                                        [T, n] (target-side prior)
+  bias         compatibility bias B: 0 on the diagonal, c + U(-a, a) off it with
+               c = -1, a = 0.5 (the negative-offset, bounded-noise initialisation)   [n, n]
+  lambda       0.5 (weight of the target prior)
+The base routing signal g_base is the layer's logits.
 """
 from __future__ import annotations
 
@@ -34,6 +41,10 @@ from .configs import LayerConfig
 TID_X, TID_LOGITS, TID_ROUTER, TID_BIAS, TID_RANK, TID_MASK = 0, 1, 2, 3, 4, 5
 TID_WG, TID_WU, TID_WD = 10, 11, 12
 TID_SWG, TID_SWU, TID_SWD = 20, 21, 22
+TID_GTGT, TID_COMPAT = 6, 7
+
+SCORED_LAMBDA = 0.5
+COMPAT_C, COMPAT_NOISE = -1.0, 0.5
 
 
 def _rng(seed: int, tid: int, chunk: int = 0) -> np.random.Generator:
@@ -131,3 +142,19 @@ def make_inputs(cfg: LayerConfig, seed: int = 0, workers: Optional[int] = None,
         inp.s_up = _to_dtype(_normal(seed, TID_SWU, (Fs, cfg.H), cfg.w_std), cfg.dtype)
         inp.s_down = _to_dtype(_normal(seed, TID_SWD, (cfg.H, Fs), cfg.w_std), cfg.dtype)
     return inp
+
+
+@dataclass
+class ScoredInputs:
+    g_tgt: np.ndarray               # [T, n]    f32
+    bias: np.ndarray                # [n, n]    f32
+    lam: float
+
+
+def make_scored_inputs(cfg: LayerConfig, seed: int = 0) -> ScoredInputs:
+    """Target prior and compatibility bias of the scored router (host arrays)."""
+    g_tgt = _normal(seed, TID_GTGT, (cfg.T, cfg.n), 1.0)
+    b = _rng(seed, TID_COMPAT).uniform(-COMPAT_NOISE, COMPAT_NOISE, (cfg.n, cfg.n))
+    bias = (np.float64(COMPAT_C) + b).astype(np.float32)
+    np.fill_diagonal(bias, 0.0)
+    return ScoredInputs(np.ascontiguousarray(g_tgt), np.ascontiguousarray(bias), SCORED_LAMBDA)
