@@ -73,7 +73,8 @@ typedef enum pcm_op {
     PCM_OP_BUILD_PATHS = 0,
     PCM_OP_EXPAND = 1,
     PCM_OP_PROJECT_COMBINE = 2,
-    PCM_OP_DENSE_SWIGLU = 3
+    PCM_OP_DENSE_SWIGLU = 3,
+    PCM_OP_ROUTE_SCORED = 4
 } pcm_op;
 
 /* Path table and grouped dispatch layout of T tokens (caller-owned device buffers).
@@ -139,6 +140,78 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
 pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate,
                             const void* w_up, const void* w_down, int64_t T, int H, int Fs,
                             float* y, int accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------- scored routing
+ * The router the paper runs at inference (Section 4.2's compatibility-aware path score
+ * and Section 4.3's TopK over the active path set):
+ *   s_ij = g_base_i + b_ij + lambda g_tgt_j over A = {(i, j) : m_ij = 1}, m_ii = 1;
+ *   Pi = the K best paths (ties to the lower i*n + j), beta = softmax of their scores;
+ *   S = the distinct sources, each expanded once; T_i = the targets of source i;
+ *   y = sum_{i in S} sum_{j in T_i} beta_ij D_j(U_i(h)).
+ * The score is formed in float32 as fmaf(lambda, g_tgt_j, g_base_i + b_ij). K <= min(n, 8). */
+
+/* Active pairs of one layer, materialised once (Section 4.3's offline path layout).
+ * Caller-owned device buffers: count [1] i32; pair [n*n] u32 ((i << 16) | j of each active
+ * pair in ascending i*n + j); bias [n*n] f32 (b_ij of each active pair). */
+typedef struct pcm_path_layout {
+    int32_t* count;
+    uint32_t* pair;
+    float* bias;
+} pcm_path_layout;
+
+/* Selected paths, groups and the two dispatch layouts of T tokens (caller-owned device
+ * buffers). Source slots a < n_src[t] index the token's distinct sources and target slots
+ * b < n_tgt[t] its distinct targets, both in ascending expert order. Expansion rows
+ * (one per (token, source)) and projection rows (one per (token, target)) are each
+ * ordered by (expert ascending, token ascending); at most T*K of each are used. */
+typedef struct pcm_scored_paths {
+    int32_t* sel_pair;         /* [T,K]    i*n + j of each selected path, selection order     */
+    float* sel_score;          /* [T,K]    its score                                           */
+    int32_t* n_src;            /* [T]      distinct sources                                    */
+    int32_t* src_expert;       /* [T,K]    ascending; -1 from n_src on                         */
+    int32_t* n_tgt;            /* [T]      distinct targets                                    */
+    int32_t* tgt_expert;       /* [T,K]    ascending; -1 from n_tgt on                         */
+    uint64_t* path_bits;       /* [T]      bit a*K+b: path src_expert[a] -> tgt_expert[b]      */
+    float* beta;               /* [T,K,K]  weight of path (a, b); 0 where the bit is clear     */
+    int32_t* src_offsets;      /* [n+1]    expansion rows of each expert                       */
+    int32_t* src_row_token;    /* [T*K]    token of each expansion row                         */
+    int32_t* src_row_slot;     /* [T*K]    source slot of each expansion row                   */
+    int32_t* src_row_of;       /* [T*K]    expansion row of (t, a); -1 from n_src on           */
+    int32_t* tgt_offsets;      /* [n+1]    projection rows of each expert                      */
+    int32_t* tgt_row_token;    /* [T*K]                                                         */
+    int32_t* tgt_row_slot;     /* [T*K]                                                         */
+    int32_t* tgt_row_of;       /* [T*K]    projection row of (t, b); -1 from n_tgt on          */
+} pcm_scored_paths;
+
+/* Build the active-pair layout of a layer from mask [n,n] u8 (row = source i, column =
+ * target j; the diagonal is treated as 1) and the compatibility bias [n,n] f32 (device). */
+pcm_status pcm_path_layout_build(const uint8_t* mask, const float* bias, int n,
+                                 const pcm_path_layout* out, void* stream);
+
+/* Route T tokens over the layer's active pairs: selection, source / target groups,
+ * weights and both dispatch layouts in one call (Section 4.3's fused indexing).
+ * g_base, g_tgt [T,n] f32 (device); lambda finite. Deterministic.
+ * ws: pcm_workspace_bytes(PCM_OP_ROUTE_SCORED, T, 0, 0, n, K, 0) bytes. */
+pcm_status pcm_route_scored(const float* g_base, const float* g_tgt, float lambda,
+                            const pcm_path_layout* layout, int64_t T, int n, int K,
+                            const pcm_scored_paths* out, void* ws, size_t ws_bytes, void* stream);
+
+/* pcm_expand over the expansion rows of scored routing: one row per (token, distinct
+ * source). u [T*K,F] f32; rows from src_offsets[n] on are not written. */
+pcm_status pcm_expand_scored(pcm_dtype dtype, const void* x, const void* w_gate,
+                             const void* w_up, const pcm_scored_paths* paths, int64_t T, int H,
+                             int F, int n, int K, void* u, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/* pcm_project_combine for scored routing: z_(t,b) = sum_{a : (a,b) in Pi} beta_ab u_(t,a)
+ * over the token's source and target slots, o_(t,b) = W_down[tgt_expert[b]] z_(t,b),
+ * y_t = [y_t] + sum_{b ascending} o_(t,b); the same float16 projection input as
+ * pcm_project_combine. ws: pcm_workspace_bytes(PCM_OP_PROJECT_COMBINE, T, H, F, n, K,
+ * dtype) bytes. */
+pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void* w_down,
+                                      const pcm_scored_paths* paths, int64_t T, int H, int F,
+                                      int n, int K, float* y, int accumulate, void* ws,
+                                      size_t ws_bytes, void* stream);
 
 /* Device workspace bytes an operation needs (0 if none). Returns 0 for invalid sizes. */
 size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm_dtype dtype);

@@ -19,16 +19,31 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpcomoe.
 
 PCM_F32, PCM_BF16 = 0, 1
 BETA_SRC_COND, BETA_PRODUCT, BETA_GLOBAL = 0, 1, 2
-OP_BUILD_PATHS, OP_EXPAND, OP_PROJECT_COMBINE, OP_DENSE_SWIGLU = 0, 1, 2, 3
+OP_BUILD_PATHS, OP_EXPAND, OP_PROJECT_COMBINE, OP_DENSE_SWIGLU, OP_ROUTE_SCORED = 0, 1, 2, 3, 4
 
 EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
-           "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version")
+           "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version",
+           "pcm_path_layout_build", "pcm_route_scored", "pcm_expand_scored",
+           "pcm_project_combine_scored")
 
 
 class PcmPaths(ctypes.Structure):
     _fields_ = [("path_bits", ctypes.c_void_p), ("beta", ctypes.c_void_p),
                 ("expert_offsets", ctypes.c_void_p), ("row_token", ctypes.c_void_p),
                 ("row_slot", ctypes.c_void_p), ("row_of", ctypes.c_void_p)]
+
+
+class PcmPathLayout(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_void_p), ("pair", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+
+
+_SCORED_FIELDS = ("sel_pair", "sel_score", "n_src", "src_expert", "n_tgt", "tgt_expert",
+                  "path_bits", "beta", "src_offsets", "src_row_token", "src_row_slot", "src_row_of",
+                  "tgt_offsets", "tgt_row_token", "tgt_row_slot", "tgt_row_of")
+
+
+class PcmScoredPaths(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_void_p) for f in _SCORED_FIELDS]
 
 
 _lib = None
@@ -54,8 +69,16 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
     L.pcm_workspace_bytes.restype = SZ
     L.pcm_status_string.argtypes = [I]
     L.pcm_status_string.restype = ctypes.c_char_p
+    L.pcm_path_layout_build.argtypes = [P, P, I, ctypes.POINTER(PcmPathLayout), P]
+    L.pcm_route_scored.argtypes = [P, P, ctypes.c_float, ctypes.POINTER(PcmPathLayout), I64, I, I,
+                                   ctypes.POINTER(PcmScoredPaths), P, SZ, P]
+    L.pcm_expand_scored.argtypes = [I, P, P, P, ctypes.POINTER(PcmScoredPaths), I64, I, I, I, I, P,
+                                    P, SZ, P]
+    L.pcm_project_combine_scored.argtypes = [I, P, P, ctypes.POINTER(PcmScoredPaths), I64, I, I, I,
+                                             I, P, I, P, SZ, P]
     for name in ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
-                 "pcm_dense_swiglu", "pcm_abi_version"):
+                 "pcm_dense_swiglu", "pcm_abi_version", "pcm_path_layout_build",
+                 "pcm_route_scored", "pcm_expand_scored", "pcm_project_combine_scored"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -190,6 +213,143 @@ def pcm_dense_swiglu(x, w_gate, w_up, w_down, y=None, accumulate: bool = False,
                                   _ptr(y), int(bool(accumulate)), _ptr(ws),
                                   ws.numel() if ws is not None else 0, _stream(stream)))
     return y
+
+
+# --------------------------------------------------------------- scored routing
+@dataclass
+class PathLayout:
+    """Device buffers of one layer's active-pair layout (n experts)."""
+    n: int
+    count: torch.Tensor
+    pair: torch.Tensor
+    bias: torch.Tensor
+
+    @classmethod
+    def empty(cls, n: int, device) -> "PathLayout":
+        return cls(n, torch.empty((1,), dtype=torch.int32, device=device),
+                   torch.empty((n * n,), dtype=torch.int32, device=device),
+                   torch.empty((n * n,), dtype=torch.float32, device=device))
+
+    def struct(self) -> PcmPathLayout:
+        return PcmPathLayout(self.count.data_ptr(), self.pair.data_ptr(), self.bias.data_ptr())
+
+
+def pcm_path_layout_build(mask, bias, out: PathLayout = None, stream=None) -> PathLayout:
+    _dev(mask, bias)
+    n = mask.shape[0]
+    if bias.dtype != torch.float32 or bias.shape != (n, n) or mask.dtype != torch.uint8:
+        raise TypeError("mask [n,n] uint8 and bias [n,n] float32")
+    out = out or PathLayout.empty(n, mask.device)
+    st = out.struct()
+    _check(lib().pcm_path_layout_build(_ptr(mask), _ptr(bias), n, ctypes.byref(st), _stream(stream)))
+    return out
+
+
+@dataclass
+class ScoredPathTable:
+    """Device buffers of one pcm_scored_paths for T tokens, n experts, K paths."""
+    T: int
+    n: int
+    K: int
+    sel_pair: torch.Tensor
+    sel_score: torch.Tensor
+    n_src: torch.Tensor
+    src_expert: torch.Tensor
+    n_tgt: torch.Tensor
+    tgt_expert: torch.Tensor
+    path_bits: torch.Tensor
+    beta: torch.Tensor
+    src_offsets: torch.Tensor
+    src_row_token: torch.Tensor
+    src_row_slot: torch.Tensor
+    src_row_of: torch.Tensor
+    tgt_offsets: torch.Tensor
+    tgt_row_token: torch.Tensor
+    tgt_row_slot: torch.Tensor
+    tgt_row_of: torch.Tensor
+
+    @classmethod
+    def empty(cls, T: int, n: int, K: int, device) -> "ScoredPathTable":
+        i32 = dict(dtype=torch.int32, device=device)
+        e = lambda *shape, **kw: torch.empty(shape, **(kw or i32))
+        return cls(T, n, K, e(T, K), e(T, K, dtype=torch.float32, device=device), e(T), e(T, K), e(T),
+                   e(T, K), e(T, dtype=torch.int64, device=device),
+                   e(T, K, K, dtype=torch.float32, device=device),
+                   e(n + 1), e(T * K), e(T * K), e(T, K), e(n + 1), e(T * K), e(T * K), e(T, K))
+
+    def struct(self) -> PcmScoredPaths:
+        return PcmScoredPaths(*[getattr(self, f).data_ptr() for f in _SCORED_FIELDS])
+
+
+def pcm_route_scored(g_base, g_tgt, lam: float, layout: PathLayout, K: int,
+                     out: ScoredPathTable = None, ws: torch.Tensor = None,
+                     stream=None) -> ScoredPathTable:
+    _dev(g_base, g_tgt)
+    T, n = g_base.shape
+    out = out or ScoredPathTable.empty(T, n, K, g_base.device)
+    if ws is None:
+        ws = _workspace(workspace_bytes(OP_ROUTE_SCORED, T, 0, 0, n, K, 0), g_base.device)
+    lst, st = layout.struct(), out.struct()
+    _check(lib().pcm_route_scored(_ptr(g_base), _ptr(g_tgt), float(lam), ctypes.byref(lst), T, n, K,
+                                  ctypes.byref(st), _ptr(ws), ws.numel() if ws is not None else 0,
+                                  _stream(stream)))
+    return out
+
+
+def pcm_expand_scored(x, w_gate, w_up, paths: ScoredPathTable, u=None, stream=None) -> torch.Tensor:
+    _dev(x, w_gate, w_up, u)
+    T, H = x.shape
+    n, F, _ = w_gate.shape
+    u = u if u is not None else torch.empty((T * paths.K, F), dtype=torch.float32, device=x.device)
+    st = paths.struct()
+    _check(lib().pcm_expand_scored(_dtype_code(x), _ptr(x), _ptr(w_gate), _ptr(w_up), ctypes.byref(st),
+                                   T, H, F, n, paths.K, _ptr(u), None, 0, _stream(stream)))
+    return u
+
+
+def pcm_project_combine_scored(u, w_down, paths: ScoredPathTable, y=None, accumulate: bool = False,
+                               ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+    _dev(u, w_down, y)
+    n, H, F = w_down.shape
+    T, K = paths.T, paths.K
+    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
+    dt = _dtype_code(w_down)
+    if ws is None:
+        ws = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, K, dt), u.device)
+    st = paths.struct()
+    _check(lib().pcm_project_combine_scored(dt, _ptr(u), _ptr(w_down), ctypes.byref(st), T, H, F, n,
+                                            K, _ptr(y), int(bool(accumulate)), _ptr(ws),
+                                            ws.numel() if ws is not None else 0, _stream(stream)))
+    return y
+
+
+class ScoredLayerPlan:
+    """Preallocated buffers for the scored-routing layer (forward enqueues kernels only).
+    The active-pair layout is built once per layer (build_layout)."""
+
+    def __init__(self, T, H, F, n, K, dtype: torch.dtype, device, shared_F: int = 0):
+        self.T, self.H, self.F, self.n, self.K, self.shared_F = T, H, F, n, K, shared_F
+        dt = PCM_BF16 if dtype == torch.bfloat16 else PCM_F32
+        self.layout = PathLayout.empty(n, device)
+        self.paths = ScoredPathTable.empty(T, n, K, device)
+        self.ws_route = _workspace(workspace_bytes(OP_ROUTE_SCORED, T, 0, 0, n, K, 0), device)
+        self.u = torch.empty((T * K, F), dtype=torch.float32, device=device)
+        self.ws_proj = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, K, dt), device)
+        self.ws_shared = (_workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, shared_F, 1, 1, dt), device)
+                          if shared_F else None)
+        self.y = torch.empty((T, H), dtype=torch.float32, device=device)
+
+    def build_layout(self, mask, bias, stream=None):
+        pcm_path_layout_build(mask, bias, out=self.layout, stream=stream)
+
+    def forward(self, x, g_base, g_tgt, lam, w_gate, w_up, w_down, shared=None, stream=None):
+        pcm_route_scored(g_base, g_tgt, lam, self.layout, self.K, out=self.paths, ws=self.ws_route,
+                         stream=stream)
+        pcm_expand_scored(x, w_gate, w_up, self.paths, u=self.u, stream=stream)
+        pcm_project_combine_scored(self.u, w_down, self.paths, y=self.y, ws=self.ws_proj, stream=stream)
+        if shared is not None:
+            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=True, ws=self.ws_shared, stream=stream)
+        return self.y
 
 
 class LayerPlan:

@@ -70,12 +70,41 @@ int down_ksplit(int64_t R, int n, int H, int F);
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
 hipError_t launch_gemm_f32(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
 
-// z_(t,b) = sum_a beta_ab u_(t,a); u is f32 [R,F]; z is f16 (scaled rows, inverse scales in
-// zscale) when zscale != NULL, else f32. bits == NULL: identity (k = 1, z_t = u_t).
-hipError_t launch_mix(const float* u, void* z, float* zscale, const uint64_t* bits,
-                      const float* beta, const int32_t* row_of, int64_t T, int k, int F,
+// Per-token path structure read by the mix and the combine. Token t has n_src[t] source
+// slots a (U rows src_row[t*K + a]) and n_tgt[t] target slots b (z and o rows
+// tgt_row[t*K + b]); bit a*K + b of bits[t] marks the path a -> b, weighted by
+// beta[t, a, b]. bits == NULL: identity (one slot, z_t = u_t, weight 1).
+struct MixMap {
+    const uint64_t* bits;
+    const float* beta;
+    const int32_t* src_row;
+    const int32_t* tgt_row;
+    const int32_t* n_src;   // NULL: K
+    const int32_t* n_tgt;   // NULL: K
+    int K;
+    int64_t R_src, R_tgt;   // row counts of U and of z / o (indices are clamped to them)
+};
+
+// z_(t,b) = sum_a beta_ab u_(t,a); u is f32; z is f16 (scaled rows, inverse scales in
+// zscale) when zscale != NULL, else f32.
+hipError_t launch_mix(const float* u, void* z, float* zscale, const MixMap& m, int64_t T, int F,
                       hipStream_t s);
-hipError_t launch_combine(const float* o, int ksplit, const int32_t* row_of, int64_t T, int k,
-                          int H, float* y, int accumulate, hipStream_t s);
+// y_t = [y_t] + sum_b o_(t,b), o holding ksplit slices of R_tgt rows.
+hipError_t launch_combine(const float* o, int ksplit, const MixMap& m, int64_t T, int H, float* y,
+                          int accumulate, hipStream_t s);
+
+// Grouped dispatch of counts[t] <= K distinct experts per token (ids [T,K]).
+hipError_t launch_dispatch(const int32_t* ids, const int32_t* counts, int64_t T, int n, int K,
+                           int32_t* offsets, int32_t* row_token, int32_t* row_slot,
+                           int32_t* row_of, int32_t* block_counts, hipStream_t s);
+
+// Scored compositional routing.
+hipError_t launch_path_layout(const uint8_t* mask, const float* bias, int n, int32_t* count,
+                              uint32_t* pair, float* pair_bias, hipStream_t s);
+hipError_t launch_route_scored(const float* g_base, const float* g_tgt, float lambda,
+                               const int32_t* count, const uint32_t* pair, const float* pair_bias,
+                               int64_t T, int n, int K, int32_t* sel_pair, float* sel_score,
+                               int32_t* n_src, int32_t* src_expert, int32_t* n_tgt,
+                               int32_t* tgt_expert, uint64_t* bits, float* beta, hipStream_t s);
 
 }  // namespace pcm

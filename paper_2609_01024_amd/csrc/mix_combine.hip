@@ -5,6 +5,9 @@
 //            bf16 layers store z as float16 rows scaled by a power of two (largest element
 //            just below 2^14) with the inverse scale kept per row for the down GEMM.
 //   combine: y_t = [y_t] + sum_{b ascending} o_(t,b)
+// The token's source slots a (U rows) and target slots b (z / o rows) are the same k
+// top-k slots for the vanilla-compatible router, and the distinct sources and targets of
+// the selected paths for the scored router.
 // One workgroup per token; each thread owns 8 consecutive columns.
 #include "internal.h"
 
@@ -17,30 +20,36 @@ __device__ inline void load8(const float* p, float* v) {
 }
 
 struct TokenPaths {
-    uint64_t bits;
-    int64_t rows[kMaxK];
-    const float* beta;
-    int k;
+    uint64_t bits;           // bit a*K + b: source slot a feeds target slot b
+    int64_t src[kMaxK];      // U row of each source slot
+    int64_t tgt[kMaxK];      // z / o row of each target slot
+    const float* beta;       // [K,K] (NULL: weight 1)
+    int ns, nt, K;
 };
 
-__device__ inline TokenPaths token_paths(const uint64_t* bits, const float* beta,
-                                         const int32_t* row_of, int64_t t, int k, int64_t R) {
+__device__ inline int64_t clamp_row(int64_t r, int64_t R) { return r < 0 ? 0 : (r >= R ? R - 1 : r); }
+
+__device__ inline TokenPaths token_paths(const MixMap& m, int64_t t) {
     TokenPaths p;
-    if (bits == nullptr) {  // identity: one row per token, weight 1
+    if (m.bits == nullptr) {  // identity: one row per token, weight 1
         p.bits = 1;
-        p.rows[0] = t;
+        p.src[0] = p.tgt[0] = t;
         p.beta = nullptr;
-        p.k = 1;
+        p.ns = p.nt = p.K = 1;
         return p;
     }
-    p.bits = bits[t];
+    p.K = m.K;
+    p.ns = m.n_src ? m.n_src[t] : m.K;
+    p.nt = m.n_tgt ? m.n_tgt[t] : m.K;
+    p.ns = p.ns < 0 ? 0 : (p.ns > m.K ? m.K : p.ns);
+    p.nt = p.nt < 0 ? 0 : (p.nt > m.K ? m.K : p.nt);
+    p.bits = m.bits[t];
 #pragma unroll
     for (int a = 0; a < kMaxK; ++a) {
-        int64_t r = a < k ? row_of[t * k + a] : 0;
-        p.rows[a] = r < 0 ? 0 : (r >= R ? R - 1 : r);
+        p.src[a] = a < p.ns ? clamp_row(m.src_row[t * m.K + a], m.R_src) : 0;
+        p.tgt[a] = a < p.nt ? clamp_row(m.tgt_row[t * m.K + a], m.R_tgt) : 0;
     }
-    p.beta = beta + t * k * k;
-    p.k = k;
+    p.beta = m.beta + t * m.K * m.K;
     return p;
 }
 
@@ -50,16 +59,16 @@ __device__ inline void mix8(const float* __restrict__ u, const TokenPaths& p, in
     float ua[kMaxK][8];
 #pragma unroll
     for (int a = 0; a < kMaxK; ++a)
-        if (a < p.k) load8(u + p.rows[a] * F + c, ua[a]);
+        if (a < p.ns) load8(u + p.src[a] * F + c, ua[a]);
 #pragma unroll
     for (int b = 0; b < kMaxK; ++b) {
-        if (b >= p.k) break;
+        if (b >= p.nt) break;
 #pragma unroll
         for (int i = 0; i < 8; ++i) z[b][i] = 0.f;
 #pragma unroll
         for (int a = 0; a < kMaxK; ++a) {
-            if (a < p.k && ((p.bits >> (a * p.k + b)) & 1)) {
-                const float w = p.beta ? p.beta[a * p.k + b] : 1.0f;
+            if (a < p.ns && ((p.bits >> (a * p.K + b)) & 1)) {
+                const float w = p.beta ? p.beta[a * p.K + b] : 1.0f;
 #pragma unroll
                 for (int i = 0; i < 8; ++i) z[b][i] = fmaf(w, ua[a][i], z[b][i]);
             }
@@ -69,13 +78,9 @@ __device__ inline void mix8(const float* __restrict__ u, const TokenPaths& p, in
 
 template <bool F16>
 __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, void* __restrict__ z,
-                                                  float* __restrict__ zscale,
-                                                  const uint64_t* __restrict__ bits,
-                                                  const float* __restrict__ beta,
-                                                  const int32_t* __restrict__ row_of, int k, int F,
-                                                  int64_t R) {
+                                                  float* __restrict__ zscale, MixMap m, int F) {
     const int64_t t = blockIdx.x;
-    const TokenPaths p = token_paths(bits, beta, row_of, t, k, R);
+    const TokenPaths p = token_paths(m, t);
     float scale[kMaxK];
     if (F16) {
         // pass 1: largest |z| of each target row, reduced over the workgroup
@@ -87,7 +92,7 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
             mix8(u, p, F, c, zz);
 #pragma unroll
             for (int b = 0; b < kMaxK; ++b)
-                if (b < p.k)
+                if (b < p.nt)
 #pragma unroll
                     for (int i = 0; i < 8; ++i) mx[b] = fmaxf(mx[b], fabsf(zz[b][i]));
         }
@@ -95,7 +100,7 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
         const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
         for (int b = 0; b < kMaxK; ++b) {
-            if (b >= p.k) break;
+            if (b >= p.nt) break;
             float v = mx[b];
 #pragma unroll
             for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
@@ -105,7 +110,7 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
         const int nw = (blockDim.x + 63) / 64;
 #pragma unroll
         for (int b = 0; b < kMaxK; ++b) {
-            if (b >= p.k) break;
+            if (b >= p.nt) break;
             float v = 0.f;
             for (int w = 0; w < nw; ++w) v = fmaxf(v, red[b][w]);
             // scale = 2^(kZScaleExp - e) with v < 2^e, so every |z * scale| < 2^kZScaleExp
@@ -114,7 +119,7 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
             int sh = kZScaleExp - e;
             sh = sh > 126 ? 126 : (sh < -126 ? -126 : sh);
             scale[b] = ldexpf(1.0f, sh);
-            if (threadIdx.x == 0) zscale[p.rows[b]] = ldexpf(1.0f, -sh);
+            if (threadIdx.x == 0) zscale[p.tgt[b]] = ldexpf(1.0f, -sh);
         }
     }
     // pass 2 (only pass for float32 layers): store z
@@ -123,7 +128,7 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
         mix8(u, p, F, c, zz);
 #pragma unroll
         for (int b = 0; b < kMaxK; ++b) {
-            if (b >= p.k) break;
+            if (b >= p.nt) break;
             if (F16) {
                 uint32_t w[4];
 #pragma unroll
@@ -133,9 +138,9 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
                     w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) |
                            ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
                 }
-                *(uint4*)((uint16_t*)z + p.rows[b] * F + c) = make_uint4(w[0], w[1], w[2], w[3]);
+                *(uint4*)((uint16_t*)z + p.tgt[b] * F + c) = make_uint4(w[0], w[1], w[2], w[3]);
             } else {
-                float* dst = (float*)z + p.rows[b] * F + c;
+                float* dst = (float*)z + p.tgt[b] * F + c;
                 *(float4*)dst = make_float4(zz[b][0], zz[b][1], zz[b][2], zz[b][3]);
                 *(float4*)(dst + 4) = make_float4(zz[b][4], zz[b][5], zz[b][6], zz[b][7]);
             }
@@ -144,18 +149,15 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
 }
 
 // Single-pass form of the float16 mix: each thread keeps its ITER column chunks of every
-// target row in registers (KK >= k targets), so U is read once; then the row maxima are
+// target row in registers (KK >= the token's target count), so U is read once; then the row maxima are
 // reduced over the workgroup and the scaled rows stored.
 template <int KK, int ITER>
 __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict__ u,
                                                         uint16_t* __restrict__ z,
-                                                        float* __restrict__ zscale,
-                                                        const uint64_t* __restrict__ bits,
-                                                        const float* __restrict__ beta,
-                                                        const int32_t* __restrict__ row_of, int k,
-                                                        int F, int64_t R) {
+                                                        float* __restrict__ zscale, MixMap m,
+                                                        int F) {
     const int64_t t = blockIdx.x;
-    const TokenPaths p = token_paths(bits, beta, row_of, t, k, R);
+    const TokenPaths p = token_paths(m, t);
     float zz[ITER][KK][8];
     float mx[KK];
 #pragma unroll
@@ -171,13 +173,13 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
         // sources in ascending order, each row's 8 values added to every target it feeds
 #pragma unroll
         for (int a = 0; a < KK; ++a) {
-            if (a >= p.k) break;
+            if (a >= p.ns) break;
             float ua[8];
-            load8(u + p.rows[a] * F + c, ua);
+            load8(u + p.src[a] * F + c, ua);
 #pragma unroll
             for (int b = 0; b < KK; ++b) {
-                if (b < p.k && ((p.bits >> (a * p.k + b)) & 1)) {
-                    const float w = p.beta ? p.beta[a * p.k + b] : 1.0f;
+                if (b < p.nt && ((p.bits >> (a * p.K + b)) & 1)) {
+                    const float w = p.beta ? p.beta[a * p.K + b] : 1.0f;
 #pragma unroll
                     for (int i = 0; i < 8; ++i) zz[it][b][i] = fmaf(w, ua[i], zz[it][b][i]);
                 }
@@ -210,7 +212,7 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
         int sh = kZScaleExp - e;
         sh = sh > 126 ? 126 : (sh < -126 ? -126 : sh);
         scale[b] = ldexpf(1.0f, sh);
-        if (threadIdx.x == 0 && b < p.k) zscale[p.rows[b]] = ldexpf(1.0f, -sh);
+        if (threadIdx.x == 0 && b < p.nt) zscale[p.tgt[b]] = ldexpf(1.0f, -sh);
     }
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {
@@ -218,7 +220,7 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
         if (c >= F) continue;
 #pragma unroll
         for (int b = 0; b < KK; ++b) {
-            if (b >= p.k) break;
+            if (b >= p.nt) break;
             uint32_t w[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -227,37 +229,29 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
                 w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) |
                        ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
             }
-            *(uint4*)(z + p.rows[b] * F + c) = make_uint4(w[0], w[1], w[2], w[3]);
+            *(uint4*)(z + p.tgt[b] * F + c) = make_uint4(w[0], w[1], w[2], w[3]);
         }
     }
 }
 
 template <int KK, int ITER>
 void launch_mix_regs(unsigned blocks, int threads, const float* u, void* z, float* zscale,
-                     const uint64_t* bits, const float* beta, const int32_t* row_of, int k, int F,
-                     int64_t R, hipStream_t s) {
-    mix_regs_kernel<KK, ITER><<<blocks, threads, 0, s>>>(u, (uint16_t*)z, zscale, bits, beta,
-                                                         row_of, k, F, R);
+                     const MixMap& m, int F, hipStream_t s) {
+    mix_regs_kernel<KK, ITER><<<blocks, threads, 0, s>>>(u, (uint16_t*)z, zscale, m, F);
 }
 
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o, int ksplit,
-                                                      const int32_t* __restrict__ row_of, int k,
-                                                      int H, int64_t R, float* __restrict__ y,
+                                                      MixMap m, int H, float* __restrict__ y,
                                                       int accumulate) {
     const int64_t t = blockIdx.x;
-    int64_t rows[kMaxK];
-#pragma unroll
-    for (int b = 0; b < kMaxK; ++b) {
-        int64_t r = b < k ? row_of[t * k + b] : 0;
-        rows[b] = r < 0 ? 0 : (r >= R ? R - 1 : r);
-    }
+    const TokenPaths p = token_paths(m, t);
     for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
         float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int b = 0; b < kMaxK; ++b) {
-            if (b >= k) break;
+            if (b >= p.nt) break;
             for (int q = 0; q < ksplit; ++q) {  // K slices of the projection, in order
-                const float4 v = *(const float4*)(o + (q * R + rows[b]) * H + c);
+                const float4 v = *(const float4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c);
                 s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
             }
         }
@@ -272,23 +266,22 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 
 }  // namespace
 
-hipError_t launch_mix(const float* u, void* z, float* zscale, const uint64_t* bits,
-                      const float* beta, const int32_t* row_of, int64_t T, int k, int F,
+hipError_t launch_mix(const float* u, void* z, float* zscale, const MixMap& m, int64_t T, int F,
                       hipStream_t s) {
     if (T == 0) return hipSuccess;
     const int threads = F / 8 >= 256 ? 256 : ((F / 8 + 63) / 64) * 64;
-    const int64_t R = bits ? T * k : T;
+    const int kslots = m.bits ? m.K : 1;
     if (zscale) {
         // single pass when a thread's share of every target row fits in 64 registers
         const int chunks = F / 8;
         const int threads_r = chunks >= 1024 ? 1024 : ((chunks + 63) / 64) * 64;
         const int iter = (chunks + threads_r - 1) / threads_r;
-        const int kk = k <= 1 ? 1 : (k <= 2 ? 2 : (k <= 4 ? 4 : 8));
+        const int kk = kslots <= 1 ? 1 : (kslots <= 2 ? 2 : (kslots <= 4 ? 4 : 8));
         const int it = iter <= 1 ? 1 : (iter <= 2 ? 2 : (iter <= 4 ? 4 : (iter <= 8 ? 8 : 16)));  // 16: two-pass
         const unsigned blocks = (unsigned)T;
         if (kk * it <= 8) {
             auto go = [&](auto fn) {
-                fn(blocks, threads_r, u, z, zscale, bits, beta, row_of, k, F, R, s);
+                fn(blocks, threads_r, u, z, zscale, m, F, s);
                 return hipGetLastError();
             };
             switch (kk * 100 + it) {
@@ -305,17 +298,17 @@ hipError_t launch_mix(const float* u, void* z, float* zscale, const uint64_t* bi
                 default: break;
             }
         }
-        mix_kernel<true><<<(unsigned)T, threads, 0, s>>>(u, z, zscale, bits, beta, row_of, k, F, R);
+        mix_kernel<true><<<(unsigned)T, threads, 0, s>>>(u, z, zscale, m, F);
     } else
-        mix_kernel<false><<<(unsigned)T, threads, 0, s>>>(u, z, zscale, bits, beta, row_of, k, F, R);
+        mix_kernel<false><<<(unsigned)T, threads, 0, s>>>(u, z, zscale, m, F);
     return hipGetLastError();
 }
 
-hipError_t launch_combine(const float* o, int ksplit, const int32_t* row_of, int64_t T, int k,
-                          int H, float* y, int accumulate, hipStream_t s) {
+hipError_t launch_combine(const float* o, int ksplit, const MixMap& m, int64_t T, int H, float* y,
+                          int accumulate, hipStream_t s) {
     if (T == 0) return hipSuccess;
     const int threads = H / 4 >= 256 ? 256 : ((H / 4 + 63) / 64) * 64;
-    combine_kernel<<<(unsigned)T, threads, 0, s>>>(o, ksplit, row_of, k, H, T * k, y, accumulate);
+    combine_kernel<<<(unsigned)T, threads, 0, s>>>(o, ksplit, m, H, y, accumulate);
     return hipGetLastError();
 }
 

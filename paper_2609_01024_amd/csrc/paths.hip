@@ -198,6 +198,79 @@ __global__ __launch_bounds__(kMaxN) void paths_scan_kernel(int32_t* __restrict__
     if (x == kMaxN - 1) offsets[n] = scan[x];
 }
 
+// Grouped dispatch with a variable number of entries per token: token t contributes
+// counts[t] <= K distinct experts ids[t, 0..counts[t]) (scored routing: the distinct
+// sources, or the distinct targets, of its selected paths). Rows are ordered by
+// (expert, token) with the same OR-bitset ranks as paths_kernel; row_of[t, a] = -1 for
+// a >= counts[t].
+template <int PH>
+__global__ __launch_bounds__(kPathBlock) void dispatch_kernel(
+    const int32_t* __restrict__ ids, const int32_t* __restrict__ counts, int64_t T, int n, int K,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ row_token, int32_t* __restrict__ row_slot,
+    int32_t* __restrict__ row_of, int32_t* __restrict__ block_counts) {
+    __shared__ PathSmem sm;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    for (int i = tid; i < kWaves * kMaxN; i += kPathBlock) (&sm.words[0][0])[i] = 0ull;
+    __syncthreads();
+
+    const int64_t t = (int64_t)blockIdx.x * kPathBlock + tid;
+    const bool valid = t < T;
+    int c = valid ? counts[t] : 0;
+    c = c < 0 ? 0 : (c > K ? K : c);
+    int e[kMaxK];
+#pragma unroll
+    for (int a = 0; a < kMaxK; ++a) {
+        int v = (a < c) ? ids[t * K + a] : 0;
+        e[a] = v < 0 ? 0 : (v >= n ? n - 1 : v);
+    }
+#pragma unroll
+    for (int a = 0; a < kMaxK; ++a)
+        if (a < c) atomicOr(&sm.words[wave][e[a]], 1ull << lane);
+    __syncthreads();
+
+    for (int x = tid; x < kMaxN; x += kPathBlock) {
+        int run = 0;
+        if (x < n) {
+#pragma unroll
+            for (int v = 0; v < kWaves; ++v) {
+                sm.prefix[v][x] = run;
+                run += __popcll(sm.words[v][x]);
+            }
+        }
+        sm.scan[x] = run;
+    }
+    __syncthreads();
+
+    if (PH == kCount) {
+        for (int x = tid; x < n; x += kPathBlock) block_counts[(int64_t)blockIdx.x * n + x] = sm.scan[x];
+        return;
+    }
+    if (PH == kFused) {
+        const int total = block_exclusive_scan(sm.scan, n);
+        for (int x = tid; x < n; x += kPathBlock) offsets[x] = sm.scan[x];
+        if (tid == 0) offsets[n] = total;
+    } else {
+        for (int x = tid; x < n; x += kPathBlock) sm.scan[x] = block_counts[(int64_t)blockIdx.x * n + x];
+        __syncthreads();
+    }
+    if (valid) {
+        const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+        for (int a = 0; a < kMaxK; ++a) {
+            if (a >= K) break;
+            if (a >= c) {
+                row_of[t * K + a] = -1;
+                continue;
+            }
+            const int x = e[a];
+            const int pos = sm.scan[x] + sm.prefix[wave][x] + __popcll(sm.words[wave][x] & below);
+            row_token[pos] = (int32_t)t;
+            row_slot[pos] = a;
+            row_of[t * K + a] = pos;
+        }
+    }
+}
+
 }  // namespace
 
 size_t build_paths_ws_bytes(int64_t T, int n) {
@@ -222,6 +295,29 @@ hipError_t launch_build_paths(const int32_t* ids, const float* w, const uint8_t*
     paths_kernel<kScatter><<<(unsigned)NB, kPathBlock, 0, s>>>(ids, w, mask, T, n, k, beta_mode,
                                                                bits, beta, offsets, row_token,
                                                                row_slot, row_of, block_counts);
+    return hipGetLastError();
+}
+
+}  // namespace pcm
+
+namespace pcm {
+
+hipError_t launch_dispatch(const int32_t* ids, const int32_t* counts, int64_t T, int n, int K,
+                           int32_t* offsets, int32_t* row_token, int32_t* row_slot,
+                           int32_t* row_of, int32_t* block_counts, hipStream_t s) {
+    const int64_t NB = ceil_div(T, kPathBlock);
+    if (NB <= 1) {
+        dispatch_kernel<kFused><<<1, kPathBlock, 0, s>>>(ids, counts, T, n, K, offsets, row_token,
+                                                        row_slot, row_of, nullptr);
+        return hipGetLastError();
+    }
+    dispatch_kernel<kCount><<<(unsigned)NB, kPathBlock, 0, s>>>(ids, counts, T, n, K, offsets,
+                                                               row_token, row_slot, row_of,
+                                                               block_counts);
+    paths_scan_kernel<<<1, kMaxN, 0, s>>>(block_counts, NB, n, offsets);
+    dispatch_kernel<kScatter><<<(unsigned)NB, kPathBlock, 0, s>>>(ids, counts, T, n, K, offsets,
+                                                                 row_token, row_slot, row_of,
+                                                                 block_counts);
     return hipGetLastError();
 }
 

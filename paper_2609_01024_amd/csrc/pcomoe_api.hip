@@ -33,6 +33,20 @@ pcm_status check_paths(const pcm_paths* p) {
 
 pcm_status from_hip(hipError_t e) { return e == hipSuccess ? PCM_OK : PCM_ERR_HIP; }
 
+pcm_status check_scored(const pcm_scored_paths* p) {
+    if (!p || !p->sel_pair || !p->sel_score || !p->n_src || !p->src_expert || !p->n_tgt ||
+        !p->tgt_expert || !p->path_bits || !p->beta || !p->src_offsets || !p->src_row_token ||
+        !p->src_row_slot || !p->src_row_of || !p->tgt_offsets || !p->tgt_row_token ||
+        !p->tgt_row_slot || !p->tgt_row_of)
+        return PCM_ERR_ARG;
+    return PCM_OK;
+}
+
+pcm_status check_layout(const pcm_path_layout* l) {
+    if (!l || !l->count || !l->pair || !l->bias) return PCM_ERR_ARG;
+    return PCM_OK;
+}
+
 // Workspace of the projection of R rows of n groups: z [R,F] (f16 for bf16 layers, f32
 // otherwise), the per-row inverse scales [R] f32 (bf16 layers), then, when `with_o`, the
 // projected rows o [ksplit, R, H] f32 (K slices of the projection); parts 256-byte aligned.
@@ -54,7 +68,7 @@ ProjWs proj_ws(size_t R, int n, int H, int F, pcm_dtype dt, bool with_o) {
 
 extern "C" {
 
-int pcm_abi_version(void) { return 100; }
+int pcm_abi_version(void) { return 110; }
 
 const char* pcm_status_string(pcm_status s) {
     switch (s) {
@@ -75,6 +89,8 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
         case PCM_OP_PROJECT_COMBINE:
             if (H < 1 || F < 1) return 0;
             return proj_ws((size_t)T * k, n, H, F, dtype, true).total;
+        case PCM_OP_ROUTE_SCORED:  // block counts of the source and the target dispatch
+            return 2 * build_paths_ws_bytes(T, n);
         case PCM_OP_DENSE_SWIGLU:  // the SwiGLU output u [T,F] f32, then a projection input
             if (H < 1 || F < 1) return 0;
             return align_up((size_t)T * F * sizeof(float), 256) +
@@ -157,8 +173,13 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
     float* zscale = bf16 ? (float*)((char*)ws + w.zscale_off) : nullptr;
     float* o = (float*)((char*)ws + w.o_off);
     hipStream_t s = (hipStream_t)stream;
-    hipError_t e = launch_mix((const float*)u, z, zscale, paths->path_bits, paths->beta,
-                              paths->row_of, T, k, F, s);
+    MixMap m{};
+    m.bits = paths->path_bits;
+    m.beta = paths->beta;
+    m.src_row = m.tgt_row = paths->row_of;
+    m.K = k;
+    m.R_src = m.R_tgt = R;
+    hipError_t e = launch_mix((const float*)u, z, zscale, m, T, F, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     GemmArgs g{};
     g.a = z;
@@ -174,7 +195,7 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
     g.rows_total = R;
     e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s) : launch_gemm_f32(kDownStore, g, R, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
-    return from_hip(launch_combine(o, w.ksplit, paths->row_of, T, k, H, y, accumulate, s));
+    return from_hip(launch_combine(o, w.ksplit, m, T, H, y, accumulate, s));
 }
 
 pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
@@ -215,7 +236,10 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     if (bf16) {  // row-scaled float16 projection input
         z = (char*)ws + u_bytes;
         zscale = (float*)((char*)z + w.zscale_off);
-        e = launch_mix(u, z, zscale, nullptr, nullptr, nullptr, T, 1, Fs, s);
+        MixMap id{};  // identity: z_t = u_t
+        id.K = 1;
+        id.R_src = id.R_tgt = T;
+        e = launch_mix(u, z, zscale, id, T, Fs, s);
         if (e != hipSuccess) return PCM_ERR_HIP;
     }
     GemmArgs d{};
@@ -231,6 +255,118 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     d.accumulate = accumulate;
     e = bf16 ? launch_gemm_bf16(kDownAccum, d, T, s) : launch_gemm_f32(kDownAccum, d, T, s);
     return from_hip(e);
+}
+
+pcm_status pcm_path_layout_build(const uint8_t* mask, const float* bias, int n,
+                                 const pcm_path_layout* out, void* stream) {
+    if (n < 1) return PCM_ERR_ARG;
+    if (n > kMaxN) return PCM_ERR_UNSUPPORTED;
+    if (!mask || !bias || check_layout(out) != PCM_OK) return PCM_ERR_ARG;
+    return from_hip(launch_path_layout(mask, bias, n, out->count, out->pair, out->bias,
+                                       (hipStream_t)stream));
+}
+
+pcm_status pcm_route_scored(const float* g_base, const float* g_tgt, float lambda,
+                            const pcm_path_layout* layout, int64_t T, int n, int K,
+                            const pcm_scored_paths* out, void* ws, size_t ws_bytes, void* stream) {
+    pcm_status st = check_shape(T, n, K);
+    if (st != PCM_OK) return st;
+    if (!(lambda == lambda) || lambda - lambda != 0.0f) return PCM_ERR_ARG;  // NaN or inf
+    if (T == 0) return PCM_OK;
+    if (!g_base || !g_tgt || check_layout(layout) != PCM_OK || check_scored(out) != PCM_OK)
+        return PCM_ERR_ARG;
+    const size_t one = build_paths_ws_bytes(T, n);
+    if (ws_bytes < 2 * one || (one && !ws)) return PCM_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = launch_route_scored(g_base, g_tgt, lambda, layout->count, layout->pair,
+                                       layout->bias, T, n, K, out->sel_pair, out->sel_score,
+                                       out->n_src, out->src_expert, out->n_tgt, out->tgt_expert,
+                                       out->path_bits, out->beta, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    int32_t* bc = (int32_t*)ws;
+    e = launch_dispatch(out->src_expert, out->n_src, T, n, K, out->src_offsets, out->src_row_token,
+                        out->src_row_slot, out->src_row_of, bc, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    return from_hip(launch_dispatch(out->tgt_expert, out->n_tgt, T, n, K, out->tgt_offsets,
+                                    out->tgt_row_token, out->tgt_row_slot, out->tgt_row_of,
+                                    one ? (int32_t*)((char*)ws + one) : nullptr, s));
+}
+
+pcm_status pcm_expand_scored(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                             const pcm_scored_paths* paths, int64_t T, int H, int F, int n, int K,
+                             void* u, void* ws, size_t ws_bytes, void* stream) {
+    (void)ws;
+    (void)ws_bytes;
+    pcm_status st = check_shape(T, n, K);
+    if (st != PCM_OK) return st;
+    if ((st = check_dims(H, F)) != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!x || !w_gate || !w_up || !u || check_scored(paths) != PCM_OK) return PCM_ERR_ARG;
+    if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(u)) return PCM_ERR_ARG;
+    GemmArgs g{};
+    g.a = x;
+    g.b0 = w_gate;
+    g.b1 = w_up;
+    g.out = u;
+    g.offsets = paths->src_offsets;
+    g.gather = paths->src_row_token;
+    g.a_rows = T;
+    g.n = n;
+    g.K = H;
+    g.N = F;
+    const int64_t R = T * K;  // upper bound: the rows in use are src_offsets[n]
+    hipStream_t s = (hipStream_t)stream;
+    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s)
+                                      : launch_gemm_f32(kExpand, g, R, s));
+}
+
+pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void* w_down,
+                                      const pcm_scored_paths* paths, int64_t T, int H, int F, int n,
+                                      int K, float* y, int accumulate, void* ws, size_t ws_bytes,
+                                      void* stream) {
+    pcm_status st = check_shape(T, n, K);
+    if (st != PCM_OK) return st;
+    if ((st = check_dims(H, F)) != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!u || !w_down || !y || check_scored(paths) != PCM_OK) return PCM_ERR_ARG;
+    if (!aligned16(u) || !aligned16(w_down) || !aligned16(y)) return PCM_ERR_ARG;
+    const int64_t R = T * K;  // row bound of U, z and o
+    const ProjWs w = proj_ws((size_t)R, n, H, F, dtype, true);
+    if (!ws || ws_bytes < w.total) return PCM_ERR_WORKSPACE;
+    if (!aligned16(ws)) return PCM_ERR_ARG;
+    void* z = ws;
+    const bool bf16 = dtype == PCM_BF16;
+    float* zscale = bf16 ? (float*)((char*)ws + w.zscale_off) : nullptr;
+    float* o = (float*)((char*)ws + w.o_off);
+    hipStream_t s = (hipStream_t)stream;
+    MixMap m{};
+    m.bits = paths->path_bits;
+    m.beta = paths->beta;
+    m.src_row = paths->src_row_of;
+    m.tgt_row = paths->tgt_row_of;
+    m.n_src = paths->n_src;
+    m.n_tgt = paths->n_tgt;
+    m.K = K;
+    m.R_src = m.R_tgt = R;
+    hipError_t e = launch_mix((const float*)u, z, zscale, m, T, F, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    GemmArgs g{};
+    g.a = z;
+    g.b0 = w_down;
+    g.out = o;
+    g.row_scale = zscale;
+    g.offsets = paths->tgt_offsets;
+    g.a_rows = R;
+    g.n = n;
+    g.K = F;
+    g.N = H;
+    g.ksplit = w.ksplit;
+    g.rows_total = R;
+    e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s) : launch_gemm_f32(kDownStore, g, R, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    return from_hip(launch_combine(o, w.ksplit, m, T, H, y, accumulate, s));
 }
 
 }  // extern "C"

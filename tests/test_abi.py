@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert L.pcm_abi_version() == 100
+    assert L.pcm_abi_version() == 110
     for s in (OK, ARG, UNSUP, WS, HIP):
         assert L.pcm_status_string(s).decode().startswith("PCM_")
     assert L.pcm_status_string(77) == b"unknown pcm_status"
@@ -107,3 +107,36 @@ def test_workspace_bytes_invalid(L):
     assert L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, -1, 128, 128, 8, 2, 1) == 0
     assert L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 256, 0, 0, 8, 2, 0) == 0  # one block
     assert L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 257, 0, 0, 8, 2, 0) == 256  # 2 blocks x 8
+
+
+def test_scored_validation(L):
+    lay = binding.PcmPathLayout(0x10000, 0x10000, 0x10000)
+    assert L.pcm_path_layout_build(FAKE, FAKE, 300, ctypes.byref(lay), None) == UNSUP   # n > 256
+    assert L.pcm_path_layout_build(FAKE, FAKE, 0, ctypes.byref(lay), None) == ARG       # n < 1
+    assert L.pcm_path_layout_build(None, FAKE, 8, ctypes.byref(lay), None) == ARG       # null
+    bad = binding.PcmPathLayout(0x10000, 0, 0x10000)
+    assert L.pcm_path_layout_build(FAKE, FAKE, 8, ctypes.byref(bad), None) == ARG
+    sp = binding.PcmScoredPaths(*([0x10000] * len(binding._SCORED_FIELDS)))
+    spp = ctypes.byref(sp)
+    assert L.pcm_route_scored(FAKE, FAKE, 0.5, ctypes.byref(lay), 4, 8, 9, spp, None, 0, None) == ARG    # K > n
+    assert L.pcm_route_scored(FAKE, FAKE, 0.5, ctypes.byref(lay), 4, 16, 9, spp, None, 0, None) == UNSUP  # K > 8
+    assert L.pcm_route_scored(FAKE, FAKE, float("nan"), ctypes.byref(lay), 4, 8, 2, spp, None, 0, None) == ARG
+    assert L.pcm_route_scored(FAKE, FAKE, float("inf"), ctypes.byref(lay), 4, 8, 2, spp, None, 0, None) == ARG
+    assert L.pcm_route_scored(None, None, 0.5, None, 0, 8, 2, None, None, 0, None) == OK   # T = 0
+    for f in range(len(binding._SCORED_FIELDS)):                  # every field is required
+        vals = [0x10000] * len(binding._SCORED_FIELDS)
+        vals[f] = 0
+        q = binding.PcmScoredPaths(*vals)
+        assert L.pcm_route_scored(FAKE, FAKE, 0.5, ctypes.byref(lay), 4, 8, 2, ctypes.byref(q), None,
+                                  0, None) == ARG, binding._SCORED_FIELDS[f]
+    need = L.pcm_workspace_bytes(binding.OP_ROUTE_SCORED, 5000, 0, 0, 64, 8, 0)
+    assert need == 2 * L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 5000, 0, 0, 64, 8, 0) > 0
+    assert L.pcm_route_scored(FAKE, FAKE, 0.5, ctypes.byref(lay), 5000, 64, 8, spp, FAKE, need - 1,
+                              None) == WS
+    assert L.pcm_expand_scored(1, FAKE, FAKE, FAKE, spp, 4, 100, 128, 8, 2, FAKE, None, 0, None) == UNSUP
+    assert L.pcm_expand_scored(1, FAKE, FAKE, FAKE, None, 4, 128, 128, 8, 2, FAKE, None, 0, None) == ARG
+    needp = L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, 4, 128, 128, 8, 2, 1)
+    assert L.pcm_project_combine_scored(1, FAKE, FAKE, spp, 4, 128, 128, 8, 2, FAKE, 0, FAKE,
+                                        needp - 1, None) == WS
+    assert L.pcm_project_combine_scored(1, FAKE, FAKE, spp, 4, 128, 128, 8, 9, FAKE, 0, FAKE,
+                                        needp, None) == ARG
