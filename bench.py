@@ -4,7 +4,8 @@ A step is one forward pass of the whole layer (route, build paths, expand, proje
 and combine, plus the shared expert when the workload has one) over one batch of
 synthetic, seeded inputs already resident in HBM. Prints ONE JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--config NAME] [--router topk|scored]
+                  [--no-cpu-baseline]
 
 The dominant kernel's roofline figure uses its average launch duration, measured
 with HIP events recorded on the stream the kernel runs on, over the timed steps.
@@ -32,6 +33,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default=None)
+    ap.add_argument("--router", choices=("topk", "scored"), default="topk",
+                    help="topk: top-k experts, paths among them allowed by the mask; "
+                         "scored: scored compositional routing over the active paths")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -116,27 +120,44 @@ def main():
     wg, wu, wd = inp.w_gate.to(dev), inp.w_up.to(dev), inp.w_down.to(dev)
     shared = (inp.s_gate.to(dev), inp.s_up.to(dev), inp.s_down.to(dev)) if cfg.shared_F else None
     dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-    plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
     stream = torch.cuda.current_stream()
-
-    stages = ["route", "build_paths", "expand", "project_combine"] + (["shared"] if shared else [])
+    scored = args.router == "scored"
+    if scored:
+        from workloads import make_scored_inputs
+        sinp = make_scored_inputs(cfg, seed=args.seed)
+        g_tgt = torch.from_numpy(sinp.g_tgt).to(dev)
+        plan = pcm.ScoredLayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
+        plan.build_layout(mask, torch.from_numpy(sinp.bias).to(dev))   # once per layer
+        stages = ["route", "expand", "project_combine"] + (["shared"] if shared else [])
+    else:
+        plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
+        stages = ["route", "build_paths", "expand", "project_combine"] + (["shared"] if shared else [])
 
     def step(events=None):
         def mark(i):
             if events is not None:
                 events[i].record(stream)
         mark(0)
-        pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
-        mark(1)
-        pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
-        mark(2)
-        pcm.pcm_expand(x, wg, wu, plan.paths, u=plan.u)
-        mark(3)
-        pcm.pcm_project_combine(plan.u, wd, plan.paths, y=plan.y, ws=plan.ws_proj)
-        mark(4)
+        if scored:
+            pcm.pcm_route_scored(logits, g_tgt, sinp.lam, plan.layout, cfg.k, out=plan.paths,
+                                 ws=plan.ws_route)
+            mark(1)
+            pcm.pcm_expand_scored(x, wg, wu, plan.paths, u=plan.u)
+            mark(2)
+            pcm.pcm_project_combine_scored(plan.u, wd, plan.paths, y=plan.y, ws=plan.ws_proj)
+            mark(3)
+        else:
+            pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
+            mark(1)
+            pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
+            mark(2)
+            pcm.pcm_expand(x, wg, wu, plan.paths, u=plan.u)
+            mark(3)
+            pcm.pcm_project_combine(plan.u, wd, plan.paths, y=plan.y, ws=plan.ws_proj)
+            mark(4)
         if shared:
             pcm.pcm_dense_swiglu(x, *shared, y=plan.y, accumulate=True, ws=plan.ws_shared)
-            mark(5)
+            mark(len(stages))
 
     for _ in range(args.warmup):
         step()
@@ -153,10 +174,18 @@ def main():
                 for i, st in enumerate(stages)}
     ms = wall * 1e3 / args.steps
 
-    offsets = plan.paths.expert_offsets.cpu().numpy()
-    touched = int(np.count_nonzero(np.diff(offsets)))
-    R = cfg.R
-    fl = acc.gemm_flops(R, cfg.H, cfg.F, cfg.T, cfg.shared_F)
+    if scored:
+        src_off = plan.paths.src_offsets.cpu().numpy()
+        tgt_off = plan.paths.tgt_offsets.cpu().numpy()
+        R, R_tgt = int(src_off[-1]), int(tgt_off[-1])
+        touched = int(np.count_nonzero(np.diff(src_off) + np.diff(tgt_off)))
+        touched_src = int(np.count_nonzero(np.diff(src_off)))
+        touched_tgt = int(np.count_nonzero(np.diff(tgt_off)))
+    else:
+        offsets = plan.paths.expert_offsets.cpu().numpy()
+        touched = touched_src = touched_tgt = int(np.count_nonzero(np.diff(offsets)))
+        R = R_tgt = cfg.R
+    fl = acc.gemm_flops(R, cfg.H, cfg.F, cfg.T, cfg.shared_F, R_tgt)
     gemm_ms = stage_ms["expand"] + stage_ms["project_combine"] + stage_ms.get("shared", 0.0)
     gemm_tflops = fl["total"] / (gemm_ms * 1e-3) / 1e12
     bf16 = cfg.dtype == "bf16"
@@ -166,13 +195,14 @@ def main():
 
     if name == "decode":
         # weight streaming: every touched expert's three matrices are read once per step
-        wbytes = acc.decode_weight_bytes(touched, cfg.H, cfg.F, 2, cfg.shared_F)
-        exp_bytes = touched * 2 * cfg.H * cfg.F * 2
+        wbytes = (touched_src * 2 + touched_tgt) * cfg.H * cfg.F * 2 + \
+            (3 * cfg.H * cfg.shared_F * 2 if cfg.shared_F else 0)
+        exp_bytes = touched_src * 2 * cfg.H * cfg.F * 2
         achieved = exp_bytes / (stage_ms["expand"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": acc.HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / acc.HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "expand (grouped gate/up GEMM + SwiGLU)",
-                "per_launch": f"{touched} touched experts x 2*H*F*2 B of gate/up weights"}
+                "per_launch": f"{touched_src} source experts x 2*H*F*2 B of gate/up weights"}
         extra = {"layer_weight_GBps": round(wbytes / (ms * 1e-3) / 1e9, 1)}
     else:
         achieved = fl["expand"] / (stage_ms["expand"] * 1e-3) / 1e12
@@ -190,7 +220,9 @@ def main():
         "config": {"workload": f"{name}: T={cfg.T} H={cfg.H} n={cfg.n} F={cfg.F} k={cfg.k} "
                                f"mask density {cfg.density}"
                                + (f" shared F={cfg.shared_F}" if cfg.shared_F else ""),
-                   "tokens": cfg.T, "rows": R, "touched_experts": touched},
+                   "tokens": cfg.T, "rows": R, "touched_experts": touched,
+                   "router": args.router,
+                   **({"projection_rows": R_tgt, "lambda": sinp.lam} if scored else {})},
         "gemm_tflops": round(gemm_tflops, 1), "gemm_frac_peak": round(gemm_tflops / peak, 4),
         "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "roofline": roof, **extra,

@@ -27,10 +27,13 @@ def expert_flops(H: int, F: int) -> int:
     return expansion_flops_per_row(H, F) + projection_flops_per_row(H, F)
 
 
-def gemm_flops(R: int, H: int, F: int, T: int = 0, shared_F: int = 0) -> dict:
-    """Executed MFMA work of the grouped GEMMs for R = T*k rows (+ a shared expert)."""
+def gemm_flops(R: int, H: int, F: int, T: int = 0, shared_F: int = 0, R_tgt: int = None) -> dict:
+    """Executed MFMA work of the grouped GEMMs for R expansion rows and R_tgt projection rows
+    (both T*k for the top-k router; the distinct sources and targets for the scored router),
+    plus a shared expert."""
+    R_tgt = R if R_tgt is None else R_tgt
     exp = R * expansion_flops_per_row(H, F)
-    proj = R * projection_flops_per_row(H, F)
+    proj = R_tgt * projection_flops_per_row(H, F)
     sh_exp = T * expansion_flops_per_row(H, shared_F) if shared_F else 0
     sh_proj = T * projection_flops_per_row(H, shared_F) if shared_F else 0
     return {"expand": exp, "project": proj, "shared_expand": sh_exp, "shared_project": sh_proj,

@@ -9,8 +9,9 @@
 // only walks the active pairs. The score is formed as fmaf(lambda, g_tgt_j,
 // g_base_i + b_ij) in float32.
 //
-// route_scored_kernel: one wavefront per token. Each lane keeps the 8 best keys of the
-// pairs it visits; K rounds of a wave-wide maximum then pick the winners in order. A key
+// route_scored_kernel: W waves per token. Each lane keeps the 8 best keys of the pairs it
+// visits; K rounds of a wave-wide maximum give each wave's winners, and the token's first
+// wave merges the waves' winners the same way. A key
 // is (orderable score) << 32 | (~(i*n + j)), so a larger key is a larger score or, for an
 // equal score, a lower flattened index. The token's distinct sources and targets
 // (ascending expert order), the path bits over (source slot, target slot) and the
@@ -20,7 +21,6 @@
 namespace pcm {
 namespace {
 
-constexpr int kRouteWaves = 4;
 
 // float -> unsigned key with the same order (inputs finite; -0 is folded into +0 first)
 __device__ inline uint32_t orderable(float f) {
@@ -74,66 +74,111 @@ __global__ __launch_bounds__(256) void layout_kernel(const uint8_t* __restrict__
     if (tid == 0) *count = base;
 }
 
-__global__ __launch_bounds__(kRouteWaves * 64) void route_scored_kernel(
+// Insert key into a descending list of N keys (static indices only).
+template <int N>
+__device__ inline void insert_key(uint64_t (&best)[N], uint64_t key) {
+    if (key > best[N - 1]) {
+        best[N - 1] = key;
+#pragma unroll
+        for (int q = N - 1; q > 0; --q)
+            if (best[q] > best[q - 1]) {
+                const uint64_t tmp = best[q];
+                best[q] = best[q - 1];
+                best[q - 1] = tmp;
+            }
+    }
+}
+
+// K rounds of a wave-wide maximum over the lanes' descending lists; the lane holding the
+// winner pops it. Returns the winners in out[0..K) (the same on every lane).
+template <int N>
+__device__ inline void wave_topk(uint64_t (&best)[N], int K, uint64_t (&out)[kMaxK]) {
+#pragma unroll
+    for (int r = 0; r < kMaxK; ++r) {
+        out[r] = 0;
+        if (r >= K) continue;
+        const uint64_t m = wave_max_u64(best[0]);
+        if (best[0] == m) {
+#pragma unroll
+            for (int q = 0; q < N - 1; ++q) best[q] = best[q + 1];
+            best[N - 1] = 0;
+        }
+        out[r] = m;
+    }
+}
+
+// TPB tokens per workgroup, W waves per token: the waves of a token split its active
+// pairs, each keeps its K best, and the token's first wave merges the W*K candidates and
+// writes the token's outputs.
+template <int W, int TPB>
+__global__ __launch_bounds__(W * TPB * 64) void route_scored_kernel(
     const float* __restrict__ g_base, const float* __restrict__ g_tgt, float lambda,
     const int32_t* __restrict__ count_p, const uint32_t* __restrict__ pair,
     const float* __restrict__ pair_bias, int64_t T, int n, int K, int32_t* __restrict__ sel_pair,
     float* __restrict__ sel_score, int32_t* __restrict__ n_src_out, int32_t* __restrict__ src_out,
     int32_t* __restrict__ n_tgt_out, int32_t* __restrict__ tgt_out, uint64_t* __restrict__ bits_out,
     float* __restrict__ beta_out) {
-    __shared__ float gb_s[kRouteWaves][kMaxN], gt_s[kRouteWaves][kMaxN];
+    __shared__ float gb_s[TPB][kMaxN], gt_s[TPB][kMaxN];
+    __shared__ uint64_t cand[TPB][W * kMaxK];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t t = (int64_t)blockIdx.x * kRouteWaves + wave;
+    const int slot = wave / W, wt = wave % W, tt = wt * 64 + lane;  // token slot, thread in token
+    const int64_t t = (int64_t)blockIdx.x * TPB + slot;
     const bool active = t < T;
-    for (int x = lane; x < n; x += 64) {
-        gb_s[wave][x] = active ? g_base[t * n + x] : 0.0f;
-        gt_s[wave][x] = active ? g_tgt[t * n + x] : 0.0f;
+    for (int x = tt; x < n; x += W * 64) {
+        gb_s[slot][x] = active ? g_base[t * n + x] : 0.0f;
+        gt_s[slot][x] = active ? g_tgt[t * n + x] : 0.0f;
     }
     __syncthreads();
-    if (!active) return;  // wave-uniform; no barrier follows
 
     // this lane's 8 best keys over its share of the active pairs, descending
     uint64_t best[kMaxK];
 #pragma unroll
     for (int q = 0; q < kMaxK; ++q) best[q] = 0;  // below every real key
-    const int count = *count_p;
-    for (int p = lane; p < count; p += 64) {
+    const int count = active ? *count_p : 0;
+    for (int p = tt; p < count; p += W * 64) {
         const uint32_t pr = pair[p];
         const int i = (int)(pr >> 16), j = (int)(pr & 0xFFFFu);
-        float s = __builtin_fmaf(lambda, gt_s[wave][j], gb_s[wave][i] + pair_bias[p]);
+        float s = __builtin_fmaf(lambda, gt_s[slot][j], gb_s[slot][i] + pair_bias[p]);
         s = (s == 0.0f) ? 0.0f : s;
-        const uint64_t key =
-            ((uint64_t)orderable(s) << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)(i * n + j));
-        if (key > best[kMaxK - 1]) {
-            best[kMaxK - 1] = key;
-#pragma unroll
-            for (int q = kMaxK - 1; q > 0; --q)
-                if (best[q] > best[q - 1]) {
-                    const uint64_t tmp = best[q];
-                    best[q] = best[q - 1];
-                    best[q - 1] = tmp;
-                }
-        }
+        insert_key(best, ((uint64_t)orderable(s) << 32) |
+                             (uint32_t)(0xFFFFFFFFu - (uint32_t)(i * n + j)));
     }
-
-    // K rounds of a wave maximum over the lanes' heads; the winning lane pops its head
+    uint64_t win[kMaxK];
+    wave_topk(best, K, win);
+    if (W > 1) {
+#pragma unroll
+        for (int r = 0; r < kMaxK; ++r)
+            if (lane == r) cand[slot][wt * kMaxK + r] = win[r];
+        __syncthreads();
+        if (wt != 0) return;  // no barrier follows
+        // the token's first wave merges the W*8 candidates, (W*8 + 63) / 64 per lane
+        constexpr int PER = (W * kMaxK + 63) / 64;
+        uint64_t c[PER];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int idx = lane + 64 * q;
+            c[q] = idx < W * kMaxK ? cand[slot][idx] : 0;
+        }
+#pragma unroll
+        for (int q = 1; q < PER; ++q)   // keep each lane's list descending
+#pragma unroll
+            for (int v = q; v > 0; --v)
+                if (c[v] > c[v - 1]) {
+                    const uint64_t tmp = c[v];
+                    c[v] = c[v - 1];
+                    c[v - 1] = tmp;
+                }
+        wave_topk(c, K, win);
+    }
+    if (!active) return;
     int src[kMaxK], tgt[kMaxK];
     float score[kMaxK];
 #pragma unroll
     for (int r = 0; r < kMaxK; ++r) {
-        src[r] = tgt[r] = 0;
-        score[r] = 0.0f;
-        if (r >= K) continue;
-        const uint64_t m = wave_max_u64(best[0]);
-        if (best[0] == m) {
-#pragma unroll
-            for (int q = 0; q < kMaxK - 1; ++q) best[q] = best[q + 1];
-            best[kMaxK - 1] = 0;
-        }
-        const uint32_t flat = 0xFFFFFFFFu - (uint32_t)m;
-        src[r] = (int)(flat / (uint32_t)n);
-        tgt[r] = (int)(flat % (uint32_t)n);
-        score[r] = from_orderable((uint32_t)(m >> 32));
+        const uint32_t flat = 0xFFFFFFFFu - (uint32_t)win[r];
+        src[r] = r < K ? (int)(flat / (uint32_t)n) : 0;
+        tgt[r] = r < K ? (int)(flat % (uint32_t)n) : 0;
+        score[r] = r < K ? from_orderable((uint32_t)(win[r] >> 32)) : 0.0f;
     }
 
     // weights: softmax of the selected scores (the first is the largest)
@@ -221,10 +266,15 @@ hipError_t launch_route_scored(const float* g_base, const float* g_tgt, float la
                                int32_t* n_src, int32_t* src_expert, int32_t* n_tgt,
                                int32_t* tgt_expert, uint64_t* bits, float* beta, hipStream_t s) {
     if (T == 0) return hipSuccess;
-    const int64_t blocks = ceil_div(T, kRouteWaves);
-    route_scored_kernel<<<(unsigned)blocks, kRouteWaves * 64, 0, s>>>(
-        g_base, g_tgt, lambda, count, pair, pair_bias, T, n, K, sel_pair, sel_score, n_src,
-        src_expert, n_tgt, tgt_expert, bits, beta);
+    // few tokens: 16 waves share each token's active pairs; many: one wave per token
+    if (T <= 512)
+        route_scored_kernel<16, 1><<<(unsigned)T, 16 * 64, 0, s>>>(
+            g_base, g_tgt, lambda, count, pair, pair_bias, T, n, K, sel_pair, sel_score, n_src,
+            src_expert, n_tgt, tgt_expert, bits, beta);
+    else
+        route_scored_kernel<1, 4><<<(unsigned)ceil_div(T, 4), 4 * 64, 0, s>>>(
+            g_base, g_tgt, lambda, count, pair, pair_bias, T, n, K, sel_pair, sel_score, n_src,
+            src_expert, n_tgt, tgt_expert, bits, beta);
     return hipGetLastError();
 }
 
