@@ -38,6 +38,9 @@ def parse():
                          "scored: scored compositional routing over the active paths")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ablation", action="store_true",
+                    help="also time the same layer executed per path (with and without source "
+                         "reuse) and the vanilla top-k layer (diagonal-only mask)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -90,6 +93,53 @@ def cpu_baseline(inp, target_s: float) -> dict:
     return {"value": round(toks.size / spent, 3), "unit": "tokens/s", "cores": nt, "kind": "oracle",
             "sample": f"{toks.size} of {cfg.T} tokens of the same workload (route, paths, per-path "
                       f"float64 evaluation), {spent:.1f} s wall on {nt} threads"}
+
+
+def ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args):
+    """Layer time of the same routing and paths executed three other ways (Table 3's
+    question on this hardware): one projection per path reusing U per source; one expansion
+    and one projection per path; and the vanilla top-k layer (diagonal-only mask)."""
+    import torch
+    n_paths = int(np.unpackbits(plan.paths.path_bits.cpu().numpy().view(np.uint8)).sum())
+
+    def timed(fn):
+        for _ in range(max(1, args.warmup)):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / args.steps
+
+    ws = torch.empty((pcm.workspace_bytes(5, cfg.T, cfg.H, cfg.F, cfg.n, cfg.k,
+                                          1 if cfg.dtype == "bf16" else 0),), dtype=torch.uint8,
+                     device=x.device)
+    y = torch.empty_like(plan.y)
+
+    def per_path(reuse):
+        def fn():
+            pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
+            pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
+            pcm.pcm_layer_per_path(x, wg, wu, wd, plan.paths, reuse=reuse, y=y, ws=ws)
+            if shared:
+                pcm.pcm_dense_swiglu(x, *shared, y=y, accumulate=True, ws=plan.ws_shared)
+        return fn
+
+    eye = torch.eye(cfg.n, dtype=torch.uint8, device=x.device)
+
+    def mixed(m):
+        def fn():
+            plan.forward(x, logits, m, wg, wu, wd, shared)
+        return fn
+
+    out = {"paths": n_paths, "expansion_rows_reused": cfg.R,
+           "ms_target_mix": round(timed(mixed(mask)), 4),
+           "ms_per_path_reuse": round(timed(per_path(True)), 4),
+           "ms_per_path_no_reuse": round(timed(per_path(False)), 4),
+           "ms_vanilla_topk": round(timed(mixed(eye)), 4)}
+    del ws
+    return out
 
 
 def main():
@@ -227,6 +277,8 @@ def main():
         "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "roofline": roof, **extra,
     }
+    if args.ablation and not scored:
+        line["ablation"] = ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)

@@ -74,7 +74,8 @@ typedef enum pcm_op {
     PCM_OP_EXPAND = 1,
     PCM_OP_PROJECT_COMBINE = 2,
     PCM_OP_DENSE_SWIGLU = 3,
-    PCM_OP_ROUTE_SCORED = 4
+    PCM_OP_ROUTE_SCORED = 4,
+    PCM_OP_LAYER_PER_PATH = 5
 } pcm_op;
 
 /* Path table and grouped dispatch layout of T tokens (caller-owned device buffers).
@@ -140,6 +141,21 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
 pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate,
                             const void* w_up, const void* w_down, int64_t T, int H, int Fs,
                             float* y, int accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/* Per-path execution of the layer, a baseline for the target-mixed projection above: the
+ * path-level aggregation of Section 4.1 evaluated one projection per path, as in Section
+ * 4.3's source-grouped form, with no mixing of paths that share a target:
+ *   reuse = 1: U_(t,a) once per (token, source) (Section 4.3's reuse);
+ *   reuse = 0: U recomputed for every path (no reuse at all);
+ *   o_(t,a,b) = W_down[e_b] U_(t,a) for every (a, b) in Pi,
+ *   y_t = [y_t if accumulate] + sum_{(a,b) in Pi, a-major} beta_ab o_(t,a,b).
+ * Same inputs, path table and result (to rounding) as pcm_expand + pcm_project_combine; bf16
+ * layers project row-scaled float16 U rows. Sized for at most T*k*k paths.
+ * ws: pcm_workspace_bytes(PCM_OP_LAYER_PER_PATH, T, H, F, n, k, dtype) bytes. */
+pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate,
+                              const void* w_up, const void* w_down, const pcm_paths* paths,
+                              int64_t T, int H, int F, int n, int k, int reuse, float* y,
+                              int accumulate, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------- scored routing
  * The router the paper runs at inference (Section 4.2's compatibility-aware path score

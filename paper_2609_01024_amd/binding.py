@@ -20,11 +20,12 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpcomoe.
 PCM_F32, PCM_BF16 = 0, 1
 BETA_SRC_COND, BETA_PRODUCT, BETA_GLOBAL = 0, 1, 2
 OP_BUILD_PATHS, OP_EXPAND, OP_PROJECT_COMBINE, OP_DENSE_SWIGLU, OP_ROUTE_SCORED = 0, 1, 2, 3, 4
+OP_LAYER_PER_PATH = 5
 
 EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version",
            "pcm_path_layout_build", "pcm_route_scored", "pcm_expand_scored",
-           "pcm_project_combine_scored")
+           "pcm_project_combine_scored", "pcm_layer_per_path")
 
 
 class PcmPaths(ctypes.Structure):
@@ -76,9 +77,12 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
                                     P, SZ, P]
     L.pcm_project_combine_scored.argtypes = [I, P, P, ctypes.POINTER(PcmScoredPaths), I64, I, I, I,
                                              I, P, I, P, SZ, P]
+    L.pcm_layer_per_path.argtypes = [I, P, P, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, I, P,
+                                     I, P, SZ, P]
     for name in ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
                  "pcm_dense_swiglu", "pcm_abi_version", "pcm_path_layout_build",
-                 "pcm_route_scored", "pcm_expand_scored", "pcm_project_combine_scored"):
+                 "pcm_route_scored", "pcm_expand_scored", "pcm_project_combine_scored",
+                 "pcm_layer_per_path"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -212,6 +216,26 @@ def pcm_dense_swiglu(x, w_gate, w_up, w_down, y=None, accumulate: bool = False,
     _check(lib().pcm_dense_swiglu(dt, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down), T, H, Fs,
                                   _ptr(y), int(bool(accumulate)), _ptr(ws),
                                   ws.numel() if ws is not None else 0, _stream(stream)))
+    return y
+
+
+def pcm_layer_per_path(x, w_gate, w_up, w_down, paths: PathTable, reuse: bool = True, y=None,
+                       accumulate: bool = False, ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """Per-path execution (baseline): one projection per path; reuse=False also expands
+    once per path."""
+    _dev(x, w_gate, w_up, w_down, y)
+    T, H = x.shape
+    n, F, _ = w_gate.shape
+    k = paths.k
+    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
+    dt = _dtype_code(x)
+    if ws is None:
+        ws = _workspace(workspace_bytes(OP_LAYER_PER_PATH, T, H, F, n, k, dt), x.device)
+    st = paths.struct()
+    _check(lib().pcm_layer_per_path(dt, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down),
+                                    ctypes.byref(st), T, H, F, n, k, int(bool(reuse)), _ptr(y),
+                                    int(bool(accumulate)), _ptr(ws),
+                                    ws.numel() if ws is not None else 0, _stream(stream)))
     return y
 
 

@@ -15,7 +15,7 @@ LIB = os.path.join(PKG, "libpcomoe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["pcomoe_api.hip", "route.hip", "paths.hip", "gemm_bf16.hip", "gemm_f32.hip",
-           "mix_combine.hip", "scored.hip"]
+           "mix_combine.hip", "scored.hip", "baselines.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", INCLUDE, "-I", CSRC]

@@ -4,7 +4,8 @@
 //            one row per (token, source) pair, rows of expert e contiguous (Section 4.3),
 //            x rows gathered through row_token; SwiGLU fused into the epilogue; U kept in
 //            float32. bf16 x bf16 MFMA (v_mfma_f32_16x16x32_bf16).
-//   down:    O[r, h] = row_scale[r] * (Z[r] . W_down[e][h])   (store, or accumulate into y
+//   down:    O[r, h] = row_scale[r'] * (Z[r'] . W_down[e][h]), r' = gather[r] or r
+//                                                  (store, or accumulate into y
 //                                                  for a dense FFN whose rows are tokens)
 //            Z arrives as row-scaled float16; each bf16 W_down fragment is widened to
 //            float16 in registers after its LDS read (exact in float16's normal range), and
@@ -146,6 +147,13 @@ __device__ inline const uint16_t* b_source_row(const GemmArgs& g, int e, int nti
     return (const uint16_t*)g.b0 + ((int64_t)e * g.N + h) * g.K;
 }
 
+// Row of `a` (and of row_scale) behind output row r.
+__device__ inline int64_t scale_row(const GemmArgs& g, int r) {
+    if (!g.gather) return r;
+    const int64_t s = g.gather[r];
+    return s < 0 ? 0 : (s >= g.a_rows ? g.a_rows - 1 : s);
+}
+
 // SiLU(g) = g / (1 + e^-g) with the hardware reciprocal (about 1 ulp) instead of an IEEE
 // division; for g below about -88, e^-g is +inf and the result is -0.
 __device__ inline float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
@@ -172,7 +180,7 @@ __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB]
             }
         } else {
             float* O = (float*)g.out;
-            const float sc = g.row_scale ? g.row_scale[r] : 1.0f;
+            const float sc = g.row_scale ? g.row_scale[scale_row(g, r)] : 1.0f;
 #pragma unroll
             for (int nb = 0; nb < NBK; ++nb) {
                 const int h = ntile * OUT_COLS + wn * WTN + nb * 16 + (lane >> 4) * 4;
@@ -604,7 +612,7 @@ __global__ __launch_bounds__(SWAVES * 64) void gemm_stream_kernel(GemmArgs g, in
         for (int i = 0; i < 4; ++i) v[i] = silu(acc[0][i]) * acc[1][i];
         *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
     } else {
-        const float sc = g.row_scale ? g.row_scale[r] : 1.0f;
+        const float sc = g.row_scale ? g.row_scale[scale_row(g, r)] : 1.0f;
 #pragma unroll
         for (int blk = 0; blk < 2; ++blk) {
             const int h = col0 + blk * 16 + 4 * kg;

@@ -52,7 +52,8 @@ struct GemmArgs {
                                 // down-accum: y [R,H] f32
     const float* row_scale;     // down (bf16 layers): inverse scale of each z row
     const int32_t* offsets;     // [n+1] rows of each group (NULL: one group of a_rows rows)
-    const int32_t* gather;      // expand: row_token [R] (NULL: identity); down: unused
+    const int32_t* gather;      // row of `a` behind each output row (NULL: identity); the
+                                // down modes' row_scale follows the gathered row
     int64_t a_rows;             // rows of `a` (gathered indices are clamped to it)
     int n;                      // groups
     int K;                      // contraction length (H for expand, F for down)
@@ -83,6 +84,7 @@ struct MixMap {
     const int32_t* n_tgt;   // NULL: K
     int K;
     int64_t R_src, R_tgt;   // row counts of U and of z / o (indices are clamped to them)
+    const int32_t* live;    // identity only: rows from *live on are skipped (NULL: none)
 };
 
 // z_(t,b) = sum_a beta_ab u_(t,a); u is f32; z is f16 (scaled rows, inverse scales in
@@ -97,6 +99,18 @@ hipError_t launch_combine(const float* o, int ksplit, const MixMap& m, int64_t T
 hipError_t launch_dispatch(const int32_t* ids, const int32_t* counts, int64_t T, int n, int K,
                            int32_t* offsets, int32_t* row_token, int32_t* row_slot,
                            int32_t* row_of, int32_t* block_counts, hipStream_t s);
+
+// Per-path execution (baselines): path rows keyed by the target (key_is_target = 1) or the
+// source slot of each path, expanded in place from the top-k dispatch rows.
+hipError_t launch_path_rows(const uint64_t* bits, const int32_t* expert_offsets,
+                            const int32_t* row_token, const int32_t* row_slot,
+                            const int32_t* row_of, int64_t R, int n, int k, int key_is_target,
+                            const int32_t* gather_src, int32_t* c, int32_t* start,
+                            int32_t* path_offsets, int32_t* path_token, int32_t* path_row_of,
+                            int32_t* path_gather, hipStream_t s);
+hipError_t launch_combine_paths(const float* o, const uint64_t* bits, const float* beta,
+                                const int32_t* path_row_of, int64_t T, int k, int H, int64_t P,
+                                float* y, int accumulate, hipStream_t s);
 
 // Scored compositional routing.
 hipError_t launch_path_layout(const uint8_t* mask, const float* bias, int n, int32_t* count,

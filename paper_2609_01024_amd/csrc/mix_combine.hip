@@ -80,6 +80,7 @@ template <bool F16>
 __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, void* __restrict__ z,
                                                   float* __restrict__ zscale, MixMap m, int F) {
     const int64_t t = blockIdx.x;
+    if (m.live && t >= *m.live) return;  // whole workgroup
     const TokenPaths p = token_paths(m, t);
     float scale[kMaxK];
     if (F16) {
@@ -157,6 +158,7 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
                                                         float* __restrict__ zscale, MixMap m,
                                                         int F) {
     const int64_t t = blockIdx.x;
+    if (m.live && t >= *m.live) return;  // whole workgroup
     const TokenPaths p = token_paths(m, t);
     float zz[ITER][KK][8];
     float mx[KK];

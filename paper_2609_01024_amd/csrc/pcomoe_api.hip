@@ -64,6 +64,34 @@ ProjWs proj_ws(size_t R, int n, int H, int F, pcm_dtype dt, bool with_o) {
     return w;
 }
 
+// Workspace of the per-path execution (baseline), P = T*k*k rows at most:
+//   c, start [R] i32; path offsets [n+1] x2; path_token [P] x2; path_row_of [T*k*k] x2;
+//   path_gather [P]; U [P or R, F] f32; z [P or R, F] (f16 + scales [P] for bf16); o [P, H] f32.
+struct PathWs {
+    size_t c, start, off_t, off_s, tok_t, tok_s, rof_t, rof_s, gather, u, z, zscale, o, total;
+};
+PathWs path_ws(int64_t T, int H, int F, int n, int k, pcm_dtype dt) {
+    PathWs w{};
+    const size_t R = (size_t)T * k, P = (size_t)T * k * k;
+    size_t at = 0;
+    auto take = [&](size_t bytes) { const size_t o = at; at += align_up(bytes, 256); return o; };
+    w.c = take(R * 4);
+    w.start = take(R * 4);
+    w.off_t = take((size_t)(n + 1) * 4);
+    w.off_s = take((size_t)(n + 1) * 4);
+    w.tok_t = take(P * 4);
+    w.tok_s = take(P * 4);
+    w.rof_t = take(P * 4);
+    w.rof_s = take(P * 4);
+    w.gather = take(P * 4);
+    w.u = take(P * F * 4);
+    w.z = take(P * F * (dt == PCM_BF16 ? 2 : 4));
+    w.zscale = take(dt == PCM_BF16 ? P * 4 : 0);
+    w.o = take(P * H * 4);
+    w.total = at;
+    return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -89,6 +117,9 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
         case PCM_OP_PROJECT_COMBINE:
             if (H < 1 || F < 1) return 0;
             return proj_ws((size_t)T * k, n, H, F, dtype, true).total;
+        case PCM_OP_LAYER_PER_PATH:
+            if (H < 1 || F < 1) return 0;
+            return path_ws(T, H, F, n, k, dtype).total;
         case PCM_OP_ROUTE_SCORED:  // block counts of the source and the target dispatch
             return 2 * build_paths_ws_bytes(T, n);
         case PCM_OP_DENSE_SWIGLU:  // the SwiGLU output u [T,F] f32, then a projection input
@@ -255,6 +286,93 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     d.accumulate = accumulate;
     e = bf16 ? launch_gemm_bf16(kDownAccum, d, T, s) : launch_gemm_f32(kDownAccum, d, T, s);
     return from_hip(e);
+}
+
+pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate,
+                              const void* w_up, const void* w_down, const pcm_paths* paths,
+                              int64_t T, int H, int F, int n, int k, int reuse, float* y,
+                              int accumulate, void* ws, size_t ws_bytes, void* stream) {
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if ((st = check_dims(H, F)) != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T * (int64_t)k * k >= ((int64_t)1 << 31)) return PCM_ERR_UNSUPPORTED;
+    if (T == 0) return PCM_OK;
+    if (!x || !w_gate || !w_up || !w_down || !y || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
+    if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y))
+        return PCM_ERR_ARG;
+    const PathWs w = path_ws(T, H, F, n, k, dtype);
+    if (!ws || ws_bytes < w.total) return PCM_ERR_WORKSPACE;
+    if (!aligned16(ws)) return PCM_ERR_ARG;
+    char* b = (char*)ws;
+    auto i32 = [&](size_t off) { return (int32_t*)(b + off); };
+    const int64_t R = T * k, P = T * (int64_t)k * k;
+    const bool bf16 = dtype == PCM_BF16;
+    hipStream_t s = (hipStream_t)stream;
+    float* u = (float*)(b + w.u);
+    void* z = b + w.z;
+    float* zscale = bf16 ? (float*)(b + w.zscale) : nullptr;
+    float* o = (float*)(b + w.o);
+    hipError_t e;
+    GemmArgs g{};
+    g.a = x;
+    g.b0 = w_gate;
+    g.b1 = w_up;
+    g.out = u;
+    g.a_rows = T;
+    g.n = n;
+    g.K = H;
+    g.N = F;
+    int64_t u_rows;
+    const int32_t* gather_src = nullptr;
+    if (reuse) {  // one expansion row per (token, source): the top-k dispatch itself
+        g.offsets = paths->expert_offsets;
+        g.gather = paths->row_token;
+        u_rows = R;
+    } else {      // one expansion row per path, keyed by its source
+        e = launch_path_rows(paths->path_bits, paths->expert_offsets, paths->row_token,
+                             paths->row_slot, paths->row_of, R, n, k, 0, nullptr, i32(w.c),
+                             i32(w.start), i32(w.off_s), i32(w.tok_s), i32(w.rof_s), nullptr, s);
+        if (e != hipSuccess) return PCM_ERR_HIP;
+        g.offsets = i32(w.off_s);
+        g.gather = i32(w.tok_s);
+        u_rows = P;
+        gather_src = i32(w.rof_s);
+    }
+    e = bf16 ? launch_gemm_bf16(kExpand, g, u_rows, s) : launch_gemm_f32(kExpand, g, u_rows, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    if (bf16) {  // U rows as row-scaled float16, no mixing
+        MixMap id{};
+        id.K = 1;
+        id.R_src = id.R_tgt = u_rows;
+        id.live = reuse ? nullptr : i32(w.off_s) + n;
+        e = launch_mix(u, z, zscale, id, u_rows, F, s);
+        if (e != hipSuccess) return PCM_ERR_HIP;
+    } else {
+        z = u;
+    }
+    // one projection row per path, keyed by its target, gathering its source's z row
+    e = launch_path_rows(paths->path_bits, paths->expert_offsets, paths->row_token,
+                         paths->row_slot, paths->row_of, R, n, k, 1, gather_src, i32(w.c),
+                         i32(w.start), i32(w.off_t), i32(w.tok_t), i32(w.rof_t), i32(w.gather), s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    GemmArgs d{};
+    d.a = z;
+    d.b0 = w_down;
+    d.out = o;
+    d.row_scale = zscale;
+    d.offsets = i32(w.off_t);
+    d.gather = i32(w.gather);
+    d.a_rows = u_rows;
+    d.n = n;
+    d.K = F;
+    d.N = H;
+    d.ksplit = 1;
+    d.rows_total = P;
+    e = bf16 ? launch_gemm_bf16(kDownStore, d, P, s) : launch_gemm_f32(kDownStore, d, P, s);
+    if (e != hipSuccess) return PCM_ERR_HIP;
+    return from_hip(launch_combine_paths(o, paths->path_bits, paths->beta, i32(w.rof_t), T, k, H, P,
+                                         y, accumulate, s));
 }
 
 pcm_status pcm_path_layout_build(const uint8_t* mask, const float* bias, int n,

@@ -140,3 +140,18 @@ def test_scored_validation(L):
                                         needp - 1, None) == WS
     assert L.pcm_project_combine_scored(1, FAKE, FAKE, spp, 4, 128, 128, 8, 9, FAKE, 0, FAKE,
                                         needp, None) == ARG
+
+
+def test_per_path_validation(L):
+    bp = binding.PcmPaths(0x10000, 0x10000, 0x10000, 0x10000, 0x10000, 0x10000)
+    need = L.pcm_workspace_bytes(binding.OP_LAYER_PER_PATH, 4, 128, 128, 8, 2, 1)
+    assert need > 4 * 2 * 2 * (128 * 4 + 128 * 2 + 128 * 4)   # U, z and o for T*k*k paths
+    args = (1, FAKE, FAKE, FAKE, FAKE, ctypes.byref(bp), 4, 128, 128, 8, 2, 1, FAKE, 0)
+    assert L.pcm_layer_per_path(*args, FAKE, need - 1, None) == WS
+    assert L.pcm_layer_per_path(*args, None, need, None) == WS
+    assert L.pcm_layer_per_path(1, FAKE, FAKE, FAKE, FAKE, None, 4, 128, 128, 8, 2, 1, FAKE, 0,
+                                FAKE, need, None) == ARG
+    assert L.pcm_layer_per_path(1, FAKE, FAKE, FAKE, FAKE, ctypes.byref(bp), 1 << 26, 128, 128, 64,
+                                8, 1, FAKE, 0, FAKE, need, None) == UNSUP       # T*k*k >= 2^31
+    assert L.pcm_layer_per_path(1, None, None, None, None, None, 0, 128, 128, 8, 2, 0, None, 0,
+                                None, 0, None) == OK

@@ -272,3 +272,34 @@ def test_layer_full_size(name):
     ref = oracle.layer_inputs(inp, tokens=tokens)
     assert_y_close(y[tokens], ref, cfg.dtype, name)
     assert np.isfinite(y).all()
+
+
+# ------------------------------------------- per-path execution (ablation baselines)
+@pytest.mark.parametrize("reuse", [1, 0])
+@pytest.mark.parametrize("name", ["tiny", "mixtral_s", "olmoe_s", "fine_s", "decode_s"])
+def test_layer_per_path(name, reuse):
+    """One projection per path (and, without reuse, one expansion per path): the same layer
+    as the target-mixed path, against the oracle."""
+    cfg = SMALL[name]
+    say(f"per-path {name} reuse {reuse}")
+    inp = make_inputs(cfg, seed=8)
+    d = dev(inp)
+    ids, w = pcm.pcm_route(d["logits"], cfg.k)
+    p = pcm.pcm_build_paths(ids, w, d["mask"])
+    y = pcm.pcm_layer_per_path(d["x"], d["w_gate"], d["w_up"], d["w_down"], p, reuse=bool(reuse))
+    if "shared" in d:
+        pcm.pcm_dense_swiglu(d["x"], *d["shared"], y=y, accumulate=True)
+    torch.cuda.synchronize()
+    assert_y_close(y.cpu().numpy(), oracle.layer_inputs(inp), cfg.dtype, f"per-path {name}")
+
+
+def test_layer_per_path_reuse_is_bit_identical():
+    """Recomputing U per path gives the same U rows, hence the same output bits."""
+    cfg = SMALL["olmoe_s"]
+    d = dev(make_inputs(cfg, seed=9))
+    ids, w = pcm.pcm_route(d["logits"], cfg.k)
+    p = pcm.pcm_build_paths(ids, w, d["mask"])
+    a = pcm.pcm_layer_per_path(d["x"], d["w_gate"], d["w_up"], d["w_down"], p, reuse=True)
+    b = pcm.pcm_layer_per_path(d["x"], d["w_gate"], d["w_up"], d["w_down"], p, reuse=False)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
