@@ -59,7 +59,8 @@ def lib(path: str = _LIB) -> ctypes.CDLL:
     L.pcmo_permute_var.argtypes = [P, P, I64, I, I, P, P, P, P]
     L.pcmo_layer_scored_tokens.argtypes = [I, P, P, P, Fl, P, P, P, P, P, I64, I, I, I, I, I, P,
                                            I64, P]
-    for name in ("pcmo_route", "pcmo_paths", "pcmo_permute", "pcmo_layer_tokens",
+    L.pcmo_router_logits.argtypes = [I, P, P, I64, I, I, P]
+    for name in ("pcmo_route", "pcmo_paths", "pcmo_permute", "pcmo_layer_tokens", "pcmo_router_logits",
                  "pcmo_expansion_rows", "pcmo_dense_swiglu_tokens", "pcmo_num_threads",
                  "pcmo_route_scored", "pcmo_group_scored", "pcmo_permute_var",
                  "pcmo_layer_scored_tokens"):
@@ -284,3 +285,17 @@ def layer_scored(x, g_base, g_tgt, lam: float, bias, mask, w_gate, w_up, w_down,
                                       _ptr(wg), _ptr(wu), _ptr(wd), T, H, F, n, K, int(bool(reuse)),
                                       _ptr(tok), tok.size, _ptr(y)), "layer_scored")
     return y
+
+
+def router_logits(x, w_router, L=None) -> np.ndarray:
+    """logits[t, e] = x_t . W_r[e] in float64."""
+    L = L or lib()
+    xh, dt = _host(x)
+    wr, dtw = _host(w_router)
+    if dt != dtw:
+        raise ValueError("x and the router weights must share one dtype")
+    T, H = xh.shape
+    n = wr.shape[0]
+    out = np.empty((T, n), np.float64)
+    _check(L.pcmo_router_logits(dt, _ptr(xh), _ptr(wr), T, H, n, _ptr(out)), "router_logits")
+    return out

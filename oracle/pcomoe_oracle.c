@@ -521,3 +521,20 @@ int pcmo_layer_scored_tokens(int dtype, const void* x, const float* g_base, cons
     }
     return failed ? ORC_NO_MEM : ORC_OK;
 }
+
+/* Router scores (Section 2: the router scores each expert from the hidden state h):
+ * logits[t][e] = sum_h x[t][h] W_r[e][h], double precision, h ascending.
+ * x [T,H] and w_router [n,H] float32 or bfloat16 (widened exactly). */
+int pcmo_router_logits(int dtype, const void* x, const void* w_router, int64_t T, int H, int n,
+                       double* logits) {
+    if (T < 0 || H < 1 || n < 1 || (dtype != ORC_F32 && dtype != ORC_BF16)) return ORC_BAD_ARG;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t)
+        for (int e = 0; e < n; ++e) {
+            double s = 0.0;
+            for (int h = 0; h < H; ++h)
+                s += elem(x, dtype, t * H + h) * elem(w_router, dtype, (int64_t)e * H + h);
+            logits[t * n + e] = s;
+        }
+    return ORC_OK;
+}

@@ -496,9 +496,33 @@ def pin_scored_relabel_and_edges(L):
     assert L.pcmo_route_scored(0, 0, 0.5, 0, 0, 1, 16, 9, 0, 0, 0, 0) != 0, "K > 8 must be rejected"
 
 
+def pin_router_logits(L):
+    """Router scores: one-hot router rows read single features; a scaled row scales its
+    score; a brute-force sum over h on small integers is exact; bf16 widening is exact."""
+    T, H, n = 9, 64, 6
+    x = RNG.standard_normal((T, H)).astype(np.float32)
+    hsel = RNG.choice(H, n, replace=False)
+    onehot = np.zeros((n, H), np.float32)
+    onehot[np.arange(n), hsel] = 1.0
+    _close(oracle.router_logits(x, onehot, L=L), x[:, hsel].astype(np.float64), 0.0, "one-hot rows")
+    onehot[2] *= 3.0
+    _close(oracle.router_logits(x, onehot, L=L)[:, 2], 3.0 * x[:, hsel[2]].astype(np.float64), 1e-15,
+           "scaled row")
+    xi = RNG.integers(-8, 9, (T, H)).astype(np.float32)
+    wi = RNG.integers(-8, 9, (n, H)).astype(np.float32)
+    ref = np.array([[sum(int(xi[t, h]) * int(wi[e, h]) for h in range(H)) for e in range(n)]
+                    for t in range(T)], np.float64)
+    assert np.array_equal(oracle.router_logits(xi, wi, L=L), ref), "integer brute force"
+    import torch
+    xb, wb = torch.from_numpy(x).to(torch.bfloat16), torch.from_numpy(wi).to(torch.bfloat16)
+    assert np.array_equal(oracle.router_logits(xb, wb, L=L),
+                          oracle.router_logits(xb.float(), wb.float(), L=L)), "bf16 widening"
+
+
 ALL_PINS = [pin_topk_bruteforce, pin_path_bits_bruteforce, pin_beta_closed_forms,
             pin_permutation_bruteforce, pin_layer_bruteforce, pin_diagonal_is_vanilla_moe,
             pin_full_mask_closed_form, pin_k1_and_n1, pin_reuse_and_target_mix,
             pin_expansion_rows, pin_relabel_invariance, pin_bf16_widening, pin_edge_cases,
             pin_scored_bruteforce, pin_scored_reduces_to_vanilla, pin_scored_single_source,
-            pin_scored_target_prior, pin_scored_groups_and_dispatch, pin_scored_relabel_and_edges]
+            pin_scored_target_prior, pin_scored_groups_and_dispatch, pin_scored_relabel_and_edges,
+            pin_router_logits]

@@ -69,6 +69,10 @@ MUTANTS = {
     "scored_reuse_wrong_slot": ("Ui = U + (int64_t)slot * F;", "Ui = U;"),
     "permute_var_offsets_shifted": ("cursor[e + 1]++;", "cursor[e]++;"),
     "permute_var_slot_reversed": ("row_slot[r] = (int32_t)a;", "row_slot[r] = (int32_t)(K - 1 - a);"),
+    "router_weight_transposed": ("s += elem(x, dtype, t * H + h) * elem(w_router, dtype, (int64_t)e * H + h);",
+                                 "s += elem(x, dtype, t * H + h) * elem(w_router, dtype, (int64_t)h * n + e);"),
+    "router_drops_last_feature": ("            for (int h = 0; h < H; ++h)\n                s += elem(x, dtype, t * H + h)",
+                                  "            for (int h = 0; h < H - 1; ++h)\n                s += elem(x, dtype, t * H + h)"),
     "permute_var_stale_slot": ("if (a >= counts[t]) { row_of[t * K + a] = -1; continue; }",
                                "if (a >= counts[t]) { row_of[t * K + a] = 0; continue; }"),
 }
