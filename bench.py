@@ -95,6 +95,32 @@ def cpu_baseline(inp, target_s: float) -> dict:
                       f"float64 evaluation), {spent:.1f} s wall on {nt} threads"}
 
 
+def router_gemm(pcm, cfg, x, args):
+    """The router's own GEMM fused with the top-k (pcm_route_logits) on this workload's x and
+    a seeded router matrix of shape [n, H]; reported beside the layer, not inside it (the
+    workloads' logits are drawn directly)."""
+    import torch
+    from workloads import make_router_weights
+    wr = make_router_weights(cfg, seed=args.seed).to(x.device)
+    ids = torch.empty((cfg.T, cfg.k), dtype=torch.int32, device=x.device)
+    w = torch.empty((cfg.T, cfg.k), dtype=torch.float32, device=x.device)
+    nws = pcm.workspace_bytes(6, cfg.T, cfg.H, 0, cfg.n, cfg.k, 1 if cfg.dtype == "bf16" else 0)
+    ws = torch.empty((max(nws, 1),), dtype=torch.uint8, device=x.device) if nws else None
+    for _ in range(max(1, args.warmup)):
+        pcm.pcm_route_logits(x, wr, cfg.k, topk_ids=ids, topk_w=w, ws=ws)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        pcm.pcm_route_logits(x, wr, cfg.k, topk_ids=ids, topk_w=w, ws=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    elem = 2 if cfg.dtype == "bf16" else 4
+    nbytes = (cfg.T * cfg.H + cfg.n * cfg.H) * elem + cfg.T * cfg.k * 8
+    return {"ms": round(ms, 4), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "TFLOPs": round(2 * cfg.T * cfg.H * cfg.n / (ms * 1e-3) / 1e12, 2)}
+
+
 def ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args):
     """Layer time of the same routing and paths executed three other ways (Table 3's
     question on this hardware): one projection per path reusing U per source; one expansion
@@ -277,6 +303,7 @@ def main():
         "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "roofline": roof, **extra,
     }
+    line["router_gemm"] = router_gemm(pcm, cfg, x, args)
     if args.ablation and not scored:
         line["ablation"] = ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args)
     if not args.no_cpu_baseline:

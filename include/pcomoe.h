@@ -75,7 +75,8 @@ typedef enum pcm_op {
     PCM_OP_PROJECT_COMBINE = 2,
     PCM_OP_DENSE_SWIGLU = 3,
     PCM_OP_ROUTE_SCORED = 4,
-    PCM_OP_LAYER_PER_PATH = 5
+    PCM_OP_LAYER_PER_PATH = 5,
+    PCM_OP_ROUTE_LOGITS = 6
 } pcm_op;
 
 /* Path table and grouped dispatch layout of T tokens (caller-owned device buffers).
@@ -96,6 +97,17 @@ typedef struct pcm_paths {
  * topk_w [T,k] f32, softmax over the k selected logits. */
 pcm_status pcm_route(const float* logits, int64_t T, int n, int k, int32_t* topk_ids,
                      float* topk_w, void* stream);
+
+/* The router's own GEMM fused with the routing above: logits[t, e] = x_t . W_r[e]
+ * (the scores the router computes from the hidden state, Section 2), float32 accumulation
+ * (bf16: products on the matrix cores), then pcm_route's top-k and softmax on those float32
+ * values. x [T,H] and w_router [n,H] of `dtype` (device); logits [T,n] f32 is written when
+ * not NULL; topk_ids / topk_w as pcm_route. H must be a multiple of 64. The bf16 path splits
+ * K into slices whose partial sums are added in a fixed order (deterministic).
+ * ws: pcm_workspace_bytes(PCM_OP_ROUTE_LOGITS, T, H, 0, n, k, dtype) bytes. */
+pcm_status pcm_route_logits(pcm_dtype dtype, const void* x, const void* w_router, int64_t T,
+                            int H, int n, int k, float* logits, int32_t* topk_ids, float* topk_w,
+                            void* ws, size_t ws_bytes, void* stream);
 
 /* Build the path table and dispatch layout (Section 4.2's mask with m_ii = 1, applied
  * before any weighting; Section 4.3's source-grouped dispatch metadata).

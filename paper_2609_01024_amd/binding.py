@@ -20,12 +20,12 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpcomoe.
 PCM_F32, PCM_BF16 = 0, 1
 BETA_SRC_COND, BETA_PRODUCT, BETA_GLOBAL = 0, 1, 2
 OP_BUILD_PATHS, OP_EXPAND, OP_PROJECT_COMBINE, OP_DENSE_SWIGLU, OP_ROUTE_SCORED = 0, 1, 2, 3, 4
-OP_LAYER_PER_PATH = 5
+OP_LAYER_PER_PATH, OP_ROUTE_LOGITS = 5, 6
 
 EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version",
            "pcm_path_layout_build", "pcm_route_scored", "pcm_expand_scored",
-           "pcm_project_combine_scored", "pcm_layer_per_path")
+           "pcm_project_combine_scored", "pcm_layer_per_path", "pcm_route_logits")
 
 
 class PcmPaths(ctypes.Structure):
@@ -77,12 +77,13 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
                                     P, SZ, P]
     L.pcm_project_combine_scored.argtypes = [I, P, P, ctypes.POINTER(PcmScoredPaths), I64, I, I, I,
                                              I, P, I, P, SZ, P]
+    L.pcm_route_logits.argtypes = [I, P, P, I64, I, I, I, P, P, P, P, SZ, P]
     L.pcm_layer_per_path.argtypes = [I, P, P, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, I, P,
                                      I, P, SZ, P]
     for name in ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
                  "pcm_dense_swiglu", "pcm_abi_version", "pcm_path_layout_build",
                  "pcm_route_scored", "pcm_expand_scored", "pcm_project_combine_scored",
-                 "pcm_layer_per_path"):
+                 "pcm_layer_per_path", "pcm_route_logits"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -133,6 +134,27 @@ def pcm_route(logits: torch.Tensor, k: int, topk_ids=None, topk_w=None, stream=N
     _dev(ids, w)
     _check(lib().pcm_route(_ptr(logits), T, n, k, _ptr(ids), _ptr(w), _stream(stream)))
     return ids, w
+
+
+def pcm_route_logits(x, w_router, k: int, logits=None, topk_ids=None, topk_w=None,
+                     want_logits: bool = False, ws: torch.Tensor = None, stream=None):
+    """Router GEMM fused with the top-k: returns (ids, w) or (ids, w, logits)."""
+    _dev(x, w_router)
+    T, H = x.shape
+    n = w_router.shape[0]
+    dev = x.device
+    ids = topk_ids if topk_ids is not None else torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=dev)
+    if want_logits and logits is None:
+        logits = torch.empty((T, n), dtype=torch.float32, device=dev)
+    _dev(ids, w, logits)
+    dt = _dtype_code(x)
+    if ws is None:
+        ws = _workspace(workspace_bytes(OP_ROUTE_LOGITS, T, H, 0, n, k, dt), dev)
+    _check(lib().pcm_route_logits(dt, _ptr(x), _ptr(w_router), T, H, n, k, _ptr(logits), _ptr(ids),
+                                  _ptr(w), _ptr(ws), ws.numel() if ws is not None else 0,
+                                  _stream(stream)))
+    return (ids, w, logits) if want_logits else (ids, w)
 
 
 @dataclass

@@ -27,6 +27,11 @@ __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b 
 // Launchers (each returns hipGetLastError() of its launches).
 hipError_t launch_route(const float* logits, int64_t T, int n, int k, int32_t* ids, float* w,
                         hipStream_t s);
+// logits = x W_r^T (float32 accumulate; written when logits != NULL) fused with the top-k;
+// bf16 uses `part` (router_ws_bytes) for the K-split partial sums.
+hipError_t launch_router(bool bf16, const void* x, const void* wr, int64_t T, int H, int n, int k,
+                         float* logits, int32_t* ids, float* w, float* part, hipStream_t s);
+size_t router_ws_bytes(int64_t T, int H, int n);
 hipError_t launch_build_paths(const int32_t* ids, const float* w, const uint8_t* mask, int64_t T,
                               int n, int k, int beta_mode, uint64_t* bits, float* beta,
                               int32_t* offsets, int32_t* row_token, int32_t* row_slot,

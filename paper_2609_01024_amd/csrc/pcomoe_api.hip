@@ -117,6 +117,9 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
         case PCM_OP_PROJECT_COMBINE:
             if (H < 1 || F < 1) return 0;
             return proj_ws((size_t)T * k, n, H, F, dtype, true).total;
+        case PCM_OP_ROUTE_LOGITS:
+            if (H < 1 || H % 64) return 0;
+            return dtype == PCM_BF16 ? router_ws_bytes(T, H, n) : 0;
         case PCM_OP_LAYER_PER_PATH:
             if (H < 1 || F < 1) return 0;
             return path_ws(T, H, F, n, k, dtype).total;
@@ -138,6 +141,26 @@ pcm_status pcm_route(const float* logits, int64_t T, int n, int k, int32_t* topk
     if (!logits || !topk_ids || !topk_w) return PCM_ERR_ARG;
     if (!aligned16(logits) || !aligned16(topk_ids) || !aligned16(topk_w)) return PCM_ERR_ARG;
     return from_hip(launch_route(logits, T, n, k, topk_ids, topk_w, (hipStream_t)stream));
+}
+
+pcm_status pcm_route_logits(pcm_dtype dtype, const void* x, const void* w_router, int64_t T,
+                            int H, int n, int k, float* logits, int32_t* topk_ids, float* topk_w,
+                            void* ws, size_t ws_bytes, void* stream) {
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if (H < 1) return PCM_ERR_ARG;
+    if (H % 64) return PCM_ERR_UNSUPPORTED;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!x || !w_router || !topk_ids || !topk_w) return PCM_ERR_ARG;
+    if (!aligned16(x) || !aligned16(w_router) || !aligned16(topk_ids) || !aligned16(topk_w) ||
+        (logits && !aligned16(logits)))
+        return PCM_ERR_ARG;
+    const size_t need = dtype == PCM_BF16 ? router_ws_bytes(T, H, n) : 0;
+    if (ws_bytes < need || (need && !ws)) return PCM_ERR_WORKSPACE;
+    if (need && !aligned16(ws)) return PCM_ERR_ARG;
+    return from_hip(launch_router(dtype == PCM_BF16, x, w_router, T, H, n, k, logits, topk_ids,
+                                  topk_w, (float*)ws, (hipStream_t)stream));
 }
 
 pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const uint8_t* mask,

@@ -155,3 +155,18 @@ def test_per_path_validation(L):
                                 8, 1, FAKE, 0, FAKE, need, None) == UNSUP       # T*k*k >= 2^31
     assert L.pcm_layer_per_path(1, None, None, None, None, None, 0, 128, 128, 8, 2, 0, None, 0,
                                 None, 0, None) == OK
+
+
+def test_route_logits_validation(L):
+    need = L.pcm_workspace_bytes(binding.OP_ROUTE_LOGITS, 4, 128, 0, 8, 2, 1)
+    assert need > 0 and L.pcm_workspace_bytes(binding.OP_ROUTE_LOGITS, 4, 128, 0, 8, 2, 0) == 0
+    args = (FAKE, FAKE, 4, 128, 8, 2, None, FAKE, FAKE, FAKE, need, None)
+    assert L.pcm_route_logits(7, *args) == ARG                                   # dtype
+    assert L.pcm_route_logits(1, FAKE, FAKE, 4, 100, 8, 2, None, FAKE, FAKE, FAKE, need, None) == UNSUP
+    assert L.pcm_route_logits(1, FAKE, FAKE, 4, 128, 8, 9, None, FAKE, FAKE, FAKE, need, None) == ARG
+    assert L.pcm_route_logits(1, None, FAKE, 4, 128, 8, 2, None, FAKE, FAKE, FAKE, need, None) == ARG
+    assert L.pcm_route_logits(1, FAKE, FAKE, 4, 128, 8, 2, ctypes.c_void_p(0x10004), FAKE, FAKE,
+                              FAKE, need, None) == ARG                           # misaligned logits
+    assert L.pcm_route_logits(1, FAKE, FAKE, 4, 128, 8, 2, None, FAKE, FAKE, FAKE, need - 1,
+                              None) == WS
+    assert L.pcm_route_logits(1, None, None, 0, 128, 8, 2, None, None, None, None, 0, None) == OK

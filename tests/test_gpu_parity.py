@@ -303,3 +303,43 @@ def test_layer_per_path_reuse_is_bit_identical():
     b = pcm.pcm_layer_per_path(d["x"], d["w_gate"], d["w_up"], d["w_down"], p, reuse=False)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+# ------------------------------------------------------- router GEMM fused with top-k
+def check_route_logits(x, wr, k, what):
+    ids, w, lg = pcm.pcm_route_logits(x.to(DEV), wr.to(DEV), k, want_logits=True)
+    torch.cuda.synchronize()
+    lg = lg.cpu().numpy()
+    ref = oracle.router_logits(x, wr)
+    xa = np.abs(x.float().numpy().astype(np.float64))
+    wa = np.abs(wr.float().numpy().astype(np.float64))
+    bound = 1e-5 * (xa @ wa.T) + FLT_MIN          # float32 accumulation of exact products
+    assert np.all(np.abs(lg - ref) <= bound), f"router logits {what}"
+    # the top-k decision is taken on the kernel's own float32 logits
+    ids_ref, w_ref = oracle.route(lg, k)
+    assert np.array_equal(ids.cpu().numpy(), ids_ref), f"router ids {what}"
+    np.testing.assert_allclose(w.cpu().numpy(), w_ref, rtol=1e-5, atol=FLT_MIN, err_msg=what)
+    return lg
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+def test_route_logits_full_size(name):
+    from workloads import make_router_weights
+    cfg = CONFIGS[name]
+    inp = make_inputs(cfg, seed=0, with_weights=False)
+    wr = make_router_weights(cfg, seed=0)
+    lg = check_route_logits(inp.x, wr, cfg.k, name)
+    if name == "tiny":   # the tiny workload's logits are x W_r^T of the same matrix
+        np.testing.assert_allclose(lg, inp.logits, rtol=1e-4, atol=1e-6)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("T,H,n,k", [(1, 64, 1, 1), (63, 128, 8, 2), (64, 256, 60, 4),
+                                     (65, 192, 64, 8), (1000, 512, 256, 8), (130, 64, 17, 3)])
+def test_route_logits_shapes(T, H, n, k, dtype):
+    g = torch.Generator().manual_seed(T * 7 + n)
+    x = torch.randn((T, H), generator=g)
+    wr = torch.randn((n, H), generator=g) * 0.1
+    if dtype == "bf16":
+        x, wr = x.to(torch.bfloat16), wr.to(torch.bfloat16)
+    check_route_logits(x, wr, k, f"T={T} H={H} n={n} k={k} {dtype}")

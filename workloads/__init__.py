@@ -7,4 +7,4 @@ construction, no SwiGLU), so neither side of a parity check can borrow the
 other's math through it.
 """
 from .configs import LayerConfig, CONFIGS, HEADLINE, scaled, stress_config  # noqa: F401
-from .gen import LayerInputs, ScoredInputs, make_inputs, make_scored_inputs, quantise_logits  # noqa: F401
+from .gen import LayerInputs, ScoredInputs, make_inputs, make_router_weights, make_scored_inputs, quantise_logits  # noqa: F401

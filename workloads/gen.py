@@ -158,3 +158,9 @@ def make_scored_inputs(cfg: LayerConfig, seed: int = 0) -> ScoredInputs:
     bias = (np.float64(COMPAT_C) + b).astype(np.float32)
     np.fill_diagonal(bias, 0.0)
     return ScoredInputs(np.ascontiguousarray(g_tgt), np.ascontiguousarray(bias), SCORED_LAMBDA)
+
+
+def make_router_weights(cfg: LayerConfig, seed: int = 0) -> torch.Tensor:
+    """Router matrix W_r [n, H], N(0, w_std), in the layer's dtype (the tiny workload's
+    logits are x W_r^T of this same matrix)."""
+    return _to_dtype(_normal(seed, TID_ROUTER, (cfg.n, cfg.H), cfg.w_std), cfg.dtype)
