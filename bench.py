@@ -38,6 +38,10 @@ def parse():
                          "scored: scored compositional routing over the active paths")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stack", type=int, default=0, metavar="L",
+                    help="time a decode step through L layers of the workload's shape (router GEMM, "
+                         "paths, experts, residual; the first two layers diagonal-only); "
+                         "reported as a separate JSON line")
     ap.add_argument("--ablation", action="store_true",
                     help="also time the same layer executed per path (with and without source "
                          "reuse) and the vanilla top-k layer (diagonal-only mask)")
@@ -93,6 +97,49 @@ def cpu_baseline(inp, target_s: float) -> dict:
     return {"value": round(toks.size / spent, 3), "unit": "tokens/s", "cores": nt, "kind": "oracle",
             "sample": f"{toks.size} of {cfg.T} tokens of the same workload (route, paths, per-path "
                       f"float64 evaluation), {spent:.1f} s wall on {nt} threads"}
+
+
+def stack_bench(args):
+    """A decode step through a stack of L MoE layers of the workload's shape, weights drawn
+    on the device (resident in HBM before timing)."""
+    import torch
+    from paper_2609_01024_amd.stack import random_stack
+    from workloads import CONFIGS
+    name = args.config or "decode"
+    cfg = CONFIGS[name]
+    dev = "cuda:0"
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    t0 = time.time()
+    st = random_stack(args.stack, cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, cfg.density, args.seed, dev,
+                      dtype, w_std=cfg.w_std)
+    g = torch.Generator(device=dev).manual_seed(args.seed + 1)
+    x0 = (torch.randn((cfg.T, cfg.H), generator=g, device=dev) * cfg.x_std).to(dtype)
+    h = x0.clone()
+    torch.cuda.synchronize()
+    print(f"[bench] stack of {args.stack}: weights in {time.time() - t0:.1f} s", file=sys.stderr,
+          flush=True)
+    for _ in range(args.warmup):
+        h.copy_(x0)
+        st.forward(h)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        h.copy_(x0)
+        st.forward(h)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    wbytes = args.stack * 3 * cfg.n * cfg.H * cfg.F * (2 if dtype == torch.bfloat16 else 4)
+    line = {"metric": "decode step through a stack of path-MoE layers, tokens/sec, 1 GPU",
+            "value": round(cfg.T / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16" if dtype == torch.bfloat16 else "f32", "data": "synthetic",
+            "config": {"workload": f"{args.stack} x {name}: T={cfg.T} H={cfg.H} n={cfg.n} "
+                                   f"F={cfg.F} k={cfg.k}, layers 0-1 diagonal-only, then mask "
+                                   f"density {cfg.density}", "layers": args.stack},
+            "ms_per_layer": round(ms / args.stack, 4),
+            "all_expert_weight_GB": round(wbytes / 1e9, 1)}
+    print(json.dumps(line), flush=True)
 
 
 def router_gemm(pcm, cfg, x, args):
@@ -172,6 +219,12 @@ def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.stack:
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        stack_bench(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "

@@ -154,6 +154,12 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate,
                             const void* w_up, const void* w_down, int64_t T, int H, int Fs,
                             float* y, int accumulate, void* ws, size_t ws_bytes, void* stream);
 
+/* Residual connection around the layer in a stack of layers (each MoE layer's output is
+ * added to the hidden state it read): h = h + y elementwise, rounded to h's dtype (bf16:
+ * round to nearest even). h [T,H] of `dtype`, y [T,H] f32 (device); H a multiple of 64. */
+pcm_status pcm_residual_add(pcm_dtype dtype, void* h, const float* y, int64_t T, int H,
+                            void* stream);
+
 /* Per-path execution of the layer, a baseline for the target-mixed projection above: the
  * path-level aggregation of Section 4.1 evaluated one projection per path, as in Section
  * 4.3's source-grouped form, with no mixing of paths that share a target:

@@ -25,7 +25,8 @@ OP_LAYER_PER_PATH, OP_ROUTE_LOGITS = 5, 6
 EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version",
            "pcm_path_layout_build", "pcm_route_scored", "pcm_expand_scored",
-           "pcm_project_combine_scored", "pcm_layer_per_path", "pcm_route_logits")
+           "pcm_project_combine_scored", "pcm_layer_per_path", "pcm_route_logits",
+           "pcm_residual_add")
 
 
 class PcmPaths(ctypes.Structure):
@@ -78,12 +79,13 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
     L.pcm_project_combine_scored.argtypes = [I, P, P, ctypes.POINTER(PcmScoredPaths), I64, I, I, I,
                                              I, P, I, P, SZ, P]
     L.pcm_route_logits.argtypes = [I, P, P, I64, I, I, I, P, P, P, P, SZ, P]
+    L.pcm_residual_add.argtypes = [I, P, P, I64, I, P]
     L.pcm_layer_per_path.argtypes = [I, P, P, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, I, P,
                                      I, P, SZ, P]
     for name in ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
                  "pcm_dense_swiglu", "pcm_abi_version", "pcm_path_layout_build",
                  "pcm_route_scored", "pcm_expand_scored", "pcm_project_combine_scored",
-                 "pcm_layer_per_path", "pcm_route_logits"):
+                 "pcm_layer_per_path", "pcm_route_logits", "pcm_residual_add"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -155,6 +157,14 @@ def pcm_route_logits(x, w_router, k: int, logits=None, topk_ids=None, topk_w=Non
                                   _ptr(w), _ptr(ws), ws.numel() if ws is not None else 0,
                                   _stream(stream)))
     return (ids, w, logits) if want_logits else (ids, w)
+
+
+def pcm_residual_add(h: torch.Tensor, y: torch.Tensor, stream=None) -> torch.Tensor:
+    """h += y in place (rounded to h's dtype)."""
+    _dev(h, y)
+    T, H = h.shape
+    _check(lib().pcm_residual_add(_dtype_code(h), _ptr(h), _ptr(y), T, H, _stream(stream)))
+    return h
 
 
 @dataclass

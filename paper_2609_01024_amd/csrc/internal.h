@@ -100,6 +100,9 @@ hipError_t launch_mix(const float* u, void* z, float* zscale, const MixMap& m, i
 hipError_t launch_combine(const float* o, int ksplit, const MixMap& m, int64_t T, int H, float* y,
                           int accumulate, hipStream_t s);
 
+// h = round(h + y) over N elements (N a multiple of 4; h bf16 or f32).
+hipError_t launch_residual(void* h, const float* y, int64_t N, bool bf16, hipStream_t s);
+
 // Grouped dispatch of counts[t] <= K distinct experts per token (ids [T,K]).
 hipError_t launch_dispatch(const int32_t* ids, const int32_t* counts, int64_t T, int n, int K,
                            int32_t* offsets, int32_t* row_token, int32_t* row_slot,

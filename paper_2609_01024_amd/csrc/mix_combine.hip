@@ -266,7 +266,36 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     }
 }
 
+// h = round(h + y) elementwise (h bf16, round to nearest even, or f32)
+__global__ __launch_bounds__(256) void residual_kernel(void* __restrict__ h,
+                                                       const float* __restrict__ y, int64_t N,
+                                                       int bf16) {
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (i >= N) return;
+    const float4 v = *(const float4*)(y + i);
+    if (bf16) {
+        uint16_t* hb = (uint16_t*)h + i;
+        const uint2 q = *(const uint2*)hb;
+        const float a0 = bf16_bits_to_f32(q.x & 0xFFFFu), a1 = bf16_bits_to_f32(q.x >> 16);
+        const float a2 = bf16_bits_to_f32(q.y & 0xFFFFu), a3 = bf16_bits_to_f32(q.y >> 16);
+        uint2 r;
+        r.x = (uint32_t)f32_to_bf16_rne(a0 + v.x) | ((uint32_t)f32_to_bf16_rne(a1 + v.y) << 16);
+        r.y = (uint32_t)f32_to_bf16_rne(a2 + v.z) | ((uint32_t)f32_to_bf16_rne(a3 + v.w) << 16);
+        *(uint2*)hb = r;
+    } else {
+        float4* hf = (float4*)((float*)h + i);
+        const float4 a = *hf;
+        *hf = make_float4(a.x + v.x, a.y + v.y, a.z + v.z, a.w + v.w);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_residual(void* h, const float* y, int64_t N, bool bf16, hipStream_t s) {
+    if (N == 0) return hipSuccess;
+    residual_kernel<<<(unsigned)ceil_div(N / 4, 256), 256, 0, s>>>(h, y, N, bf16 ? 1 : 0);
+    return hipGetLastError();
+}
 
 hipError_t launch_mix(const float* u, void* z, float* zscale, const MixMap& m, int64_t T, int F,
                       hipStream_t s) {

@@ -163,6 +163,16 @@ pcm_status pcm_route_logits(pcm_dtype dtype, const void* x, const void* w_router
                                   topk_w, (float*)ws, (hipStream_t)stream));
 }
 
+pcm_status pcm_residual_add(pcm_dtype dtype, void* h, const float* y, int64_t T, int H,
+                            void* stream) {
+    if (T < 0 || H < 1) return PCM_ERR_ARG;
+    if (H % 64) return PCM_ERR_UNSUPPORTED;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!h || !y || !aligned16(h) || !aligned16(y)) return PCM_ERR_ARG;
+    return from_hip(launch_residual(h, y, T * (int64_t)H, dtype == PCM_BF16, (hipStream_t)stream));
+}
+
 pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const uint8_t* mask,
                            int64_t T, int n, int k, pcm_beta_mode beta_mode, const pcm_paths* out,
                            void* ws, size_t ws_bytes, void* stream) {
