@@ -425,6 +425,7 @@ struct SCfg {
     static constexpr int LDS_BYTES = 2 * STAGE;
     static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+    static_assert(A_CHUNKS % NT == 0 && B_CHUNKS % NT == 0, "every thread owns whole chunks");
 };
 
 using MediumStaged = SCfg<128, 128, 2, 2>;
@@ -446,49 +447,38 @@ __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t 
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
 
     // chunk i of a stage: LDS row i / 8, logical chunk i % 8 (16 bytes), stored at position
-    // (i % 8) ^ ((row >> 1) & 7)
+    // (i % 8) ^ ((row >> 1) & 7); every thread owns A_PER_T + B_PER_T chunks
     const char* aptr[C::A_PER_T];
     const char* bptr[C::B_PER_T];
+    int aoff[C::A_PER_T], boff[C::B_PER_T];
 #pragma unroll
     for (int i = 0; i < C::A_PER_T; ++i) {
         const int c = tid + i * C::NT, lr = c / 8, kc = c % 8;
-        aptr[i] = nullptr;
-        if (c < C::A_CHUNKS) {
-            const int64_t srow = a_source_row(g, row0 + lr, row1);
-            aptr[i] = (const char*)g.a + srow * (int64_t)K * 2 + kc * 16;
-        }
+        const int64_t srow = a_source_row(g, row0 + lr, row1);
+        aptr[i] = (const char*)g.a + srow * (int64_t)K * 2 + kc * 16;
+        aoff[i] = lr * 128 + ((kc ^ ((lr >> 1) & 7)) * 16);
     }
 #pragma unroll
     for (int i = 0; i < C::B_PER_T; ++i) {
         const int c = tid + i * C::NT, j = c / 8, kc = c % 8;
-        bptr[i] = c < C::B_CHUNKS
-                      ? (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, j) + kc * 16
-                      : nullptr;
+        bptr[i] = (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, j) + kc * 16;
+        boff[i] = (C::A_ROWS + j) * 128 + ((kc ^ ((j >> 1) & 7)) * 16);
     }
-    const int a_step = 128;
 
     uint4 ra[C::A_PER_T], rb[C::B_PER_T];
-    auto gload = [&](int kt) {
-#pragma unroll
-        for (int i = 0; i < C::A_PER_T; ++i)
-            if (aptr[i]) ra[i] = *(const uint4*)(aptr[i] + (int64_t)kt * a_step);
-#pragma unroll
-        for (int i = 0; i < C::B_PER_T; ++i)
-            if (bptr[i]) rb[i] = *(const uint4*)(bptr[i] + (int64_t)kt * 128);
-    };
-    auto lstore = [&](int buf) {
-        char* S = lds + buf * C::STAGE;
-#pragma unroll
-        for (int i = 0; i < C::A_PER_T; ++i) {
-            const int c = tid + i * C::NT, lr = c / 8, kc = c % 8;
-            if (c < C::A_CHUNKS) *(uint4*)(S + lr * 128 + ((kc ^ ((lr >> 1) & 7)) * 16)) = ra[i];
-        }
-#pragma unroll
-        for (int i = 0; i < C::B_PER_T; ++i) {
-            const int c = tid + i * C::NT, j = c / 8, kc = c % 8;
-            if (c < C::B_CHUNKS) *(uint4*)(S + (C::A_ROWS + j) * 128 + ((kc ^ ((j >> 1) & 7)) * 16)) = rb[i];
-        }
-    };
+#define PCM_STAGED_GLOAD(kt)                                                              \
+    do {                                                                                  \
+        _Pragma("unroll") for (int i = 0; i < C::A_PER_T; ++i)                            \
+            ra[i] = *(const uint4*)(aptr[i] + (int64_t)(kt) * 128);                       \
+        _Pragma("unroll") for (int i = 0; i < C::B_PER_T; ++i)                            \
+            rb[i] = *(const uint4*)(bptr[i] + (int64_t)(kt) * 128);                       \
+    } while (0)
+#define PCM_STAGED_LSTORE(buf)                                                            \
+    do {                                                                                  \
+        char* S_ = lds + (buf) * C::STAGE;                                                \
+        _Pragma("unroll") for (int i = 0; i < C::A_PER_T; ++i) *(uint4*)(S_ + aoff[i]) = ra[i]; \
+        _Pragma("unroll") for (int i = 0; i < C::B_PER_T; ++i) *(uint4*)(S_ + boff[i]) = rb[i]; \
+    } while (0)
 
     floatx4 acc[C::NBK][C::MB];
 #pragma unroll
@@ -497,12 +487,14 @@ __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t 
         for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     const int KT = K / 64;
-    gload(0);
-    lstore(0);
+    PCM_STAGED_GLOAD(0);
+    PCM_STAGED_LSTORE(0);
     __syncthreads();
     for (int kt = 0; kt < KT; ++kt) {
         const int cur = kt & 1;
-        if (kt + 1 < KT) gload(kt + 1);
+        // unconditional (the last step re-reads itself into the idle stage): a conditional
+        // load keeps the staging registers out of SROA and in scratch memory
+        PCM_STAGED_GLOAD(kt + 1 < KT ? kt + 1 : kt);
         const char* S = lds + cur * C::STAGE;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
@@ -520,9 +512,11 @@ __global__ __launch_bounds__(C::NT) void gemm_staged_kernel(GemmArgs g, int64_t 
 #pragma unroll
                 for (int mb = 0; mb < C::MB; ++mb) acc[nb][mb] = mfma_step(bfr[nb], afr[mb], acc[nb][mb]);
         }
-        if (kt + 1 < KT) lstore(cur ^ 1);
+        PCM_STAGED_LSTORE(cur ^ 1);
         __syncthreads();
     }
+#undef PCM_STAGED_GLOAD
+#undef PCM_STAGED_LSTORE
     epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(g, acc, row0, row1, ntile, wm, wn, lane);
 }
 
