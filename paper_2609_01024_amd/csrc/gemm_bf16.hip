@@ -16,12 +16,12 @@
 // Three kernel shapes share the epilogue and the work decomposition:
 //  * "interleaved" (large tiles, 256 x 256): four waves, one per SIMD, each owning a 128 x 128
 //    block of C in 256 accumulation registers. Global -> LDS direct loads
-//    (global_load_lds_dwordx4, no register staging), 32-wide K steps in NS LDS stages
-//    issued NS steps ahead, one workgroup barrier per step; within a step each wave issues
-//    its 64 MFMAs interleaved with the fragment reads of the next step and the loads of a
-//    later one. LDS rows are 64 bytes; the 16-byte chunk c of row r sits at position
-//    c ^ ((r >> 1) & 3), which keeps the fragment reads (16 rows x 4 chunks per
-//    instruction) free of bank conflicts.
+//    (global_load_lds_dwordx4, no register staging) of 64-wide K stages, double-buffered,
+//    each load covering 8 whole 128-byte rows; one workgroup barrier per 32-wide substep,
+//    within which each wave issues its 64 MFMAs interleaved with the fragment reads of the
+//    next substep (and, once per stage, the loads of the stage after next). LDS rows are
+//    128 bytes; the 16-byte chunk c of row r sits at position c ^ ((r >> 1) & 7), which
+//    keeps the fragment reads (16 rows x 4 chunks per instruction) free of bank conflicts.
 //  * "staged" (medium tiles): loads through registers into two LDS stages of 64-wide K
 //    steps; rows of 128 bytes with chunk c of row r at position c ^ ((r >> 1) & 7).
 //  * "stream" (a few rows per group, decode): no LDS, fragments loaded straight into a
@@ -231,27 +231,30 @@ __device__ inline floatx4 mfma_step(const halfx8& w, const halfx8& a, floatx4 c)
 }
 
 // ---------------------------------------------------------- interleaved kernel
-// One wave per SIMD, each owning a 128 x 128 block of C (256 accumulator registers). Every
-// k-step is one barrier; between two barriers a wave issues the 64 MFMAs of step kt from
-// registers, interleaved with the LDS fragment reads of step kt+1 (into the other register
-// set) and the global->LDS loads of step kt+NS (into the stage step kt just vacated).
-template <int BM_, int BNB_, int WM_, int WN_, int NS_>
+// One wave per SIMD, each owning a 128 x 128 block of C (256 accumulator registers). K runs
+// in 64-wide stages, two of them in LDS (double buffering); a stage is two 32-wide MFMA
+// substeps, and every substep starts at a workgroup barrier. Between two barriers a wave
+// issues the 64 MFMAs of one substep from registers, interleaved with the LDS fragment
+// reads of the next substep (into the other register set); the first substep of a stage
+// also issues every global->LDS load of the stage after next (into the stage just freed).
+// A load covers 8 whole 128-byte rows, so each fetched cache line is used in full.
+template <int BM_, int BNB_, int WM_, int WN_>
 struct ICfg {
-    static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_, NS = NS_;
+    static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_, NS = 2;
     static constexpr int NW = WM * WN, NT = NW * 64;
     static constexpr int WTM = BM / WM, WTN = BNB / WN, MB = WTM / 16, NBK = WTN / 16;
     static constexpr int A_ROWS = BM;
-    static constexpr int A_INSTR = A_ROWS / 16, B_INSTR = BNB / 16;
+    static constexpr int A_INSTR = A_ROWS / 8, B_INSTR = BNB / 8;
     static constexpr int QA = A_INSTR / NW, QB = B_INSTR / NW, LPW = QA + QB;
-    static constexpr int STAGE = (A_ROWS + BNB) * 64;
+    static constexpr int STAGE = (A_ROWS + BNB) * 128;
     static constexpr int LDS_BYTES = NS * STAGE;
     static_assert(A_INSTR % NW == 0 && B_INSTR % NW == 0, "every wave issues the same loads");
     static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
-    static_assert(LDS_BYTES <= 160 * 1024 - 64, "LDS budget");
-    static_assert(NS >= 2 && (NS - 1) * LPW <= 63, "vmcnt range");
+    static_assert(LDS_BYTES <= 160 * 1024 - 1024, "LDS budget");
+    static_assert(LPW <= 63, "vmcnt range");
 };
 
-using LargeIl = ICfg<256, 256, 2, 2, 3>;
+using LargeIl = ICfg<256, 256, 2, 2>;
 
 // MFMA through inline assembly with the accumulator pinned to AGPRs ("a" constraint):
 // 256 accumulators per lane exceed what the compiler keeps in AGPRs across a loop without
@@ -286,7 +289,7 @@ __device__ inline uint32_t widen_pair_asm(uint32_t w) {
 
 template <class C, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_upper, int nt,
-                                                        int group_n) {
+                                                         int group_n) {
     extern __shared__ __attribute__((aligned(1024))) char lds[];
     __shared__ int s_tile[3];
     int64_t mt;
@@ -304,37 +307,43 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
     const int64_t k_byte0 = (int64_t)kslice * K * 2;
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
 
+    // load q of a lane: LDS row blk * 8 + lane / 8 of the A or B region, 16-byte position
+    // lane % 8, holding chunk (lane % 8) ^ ((row >> 1) & 7) of that row
     const char* src[C::LPW];
     int dst[C::LPW];
-    const int lrow = lane >> 2;
-    const int chunk = (lane & 3) ^ ((lrow >> 1) & 3);
+    const int lrow = lane >> 3;
 #pragma unroll
     for (int q = 0; q < C::LPW; ++q) {
         if (q < C::QA) {
-            const int blk = q * C::NW + wave, lr = blk * 16 + lrow;
+            const int blk = q * C::NW + wave, lr = blk * 8 + lrow;
+            const int chunk = (lane & 7) ^ ((lr >> 1) & 7);
             const int64_t srow = a_source_row(g, row0 + lr, row1);
             src[q] = (const char*)g.a + srow * (int64_t)g.K * 2 + k_byte0 + chunk * 16;
             dst[q] = blk * 1024;
         } else {
-            const int blk = (q - C::QA) * C::NW + wave, lb = blk * 16 + lrow;
+            const int blk = (q - C::QA) * C::NW + wave, lb = blk * 8 + lrow;
+            const int chunk = (lane & 7) ^ ((lb >> 1) & 7);
             src[q] = (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, lb) + k_byte0 + chunk * 16;
-            dst[q] = C::A_ROWS * 64 + blk * 1024;
+            dst[q] = C::A_ROWS * 128 + blk * 1024;
         }
     }
     auto load = [&](int q, int ks, char* base) {
-        __builtin_amdgcn_global_load_lds((const void*)(src[q] + (int64_t)ks * 64),
+        __builtin_amdgcn_global_load_lds((const void*)(src[q] + (int64_t)ks * 128),
                                          (PCM_LDS void*)(base + dst[q]), 16, 0, 0);
     };
 
     floatx4 acc[C::NBK][C::MB];
-    const int KT_ = K / 32;                 // even: K is a multiple of 64
-    const int frag_off = (lane & 15) * 64 + (((lane >> 4) ^ (((lane & 15) >> 1) & 3)) * 16);
+    const int KT2 = K / 64;
+    // fragment of row (lane & 15), chunk 4 * sub + (lane >> 4) of a 16-row block
+    const int fr = lane & 15;
+    const int foff0 = fr * 128 + (((lane >> 4) ^ (fr >> 1)) * 16);
+    const int foff1 = fr * 128 + (((4 + (lane >> 4)) ^ (fr >> 1)) * 16);
     using FT = typename Frag<MODE>::T;
     FT af[2][C::MB], bf[2][C::NBK];
     bf16x8 braw[C::NBK];
     uint32_t bw[C::NBK][4];
-    auto b_at = [&](const char* S, int nb) { return S + (C::A_ROWS + wn * C::WTN + nb * 16) * 64 + frag_off; };
-    auto a_at = [&](const char* S, int mb) { return S + (wm * C::WTM + mb * 16) * 64 + frag_off; };
+    auto b_at = [&](const char* S, int nb, int fo) { return S + (C::A_ROWS + wn * C::WTN + nb * 16) * 128 + fo; };
+    auto a_at = [&](const char* S, int mb, int fo) { return S + (wm * C::WTM + mb * 16) * 128 + fo; };
     auto barrier = [&]() {
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("" ::: "memory");
@@ -342,42 +351,42 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
         asm volatile("" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
     };
-    constexpr int NM = C::NBK * C::MB;        // MFMAs per k-step
-    constexpr int NR = C::NBK + C::MB;        // fragment reads per k-step
-    constexpr int R_EVERY = 3, L_EVERY = 8, W_FROM = R_EVERY * C::NBK + 2;
+    constexpr int NM = C::NBK * C::MB;
+    constexpr int NR = C::NBK + C::MB;
+    constexpr int R_EVERY = 3, L_EVERY = NM / C::LPW, W_FROM = R_EVERY * C::NBK + 2;
     static_assert(R_EVERY * (NR - 1) < NM && L_EVERY * (C::LPW - 1) + 1 < NM, "slots");
     static_assert(W_FROM + 4 * C::NBK <= NM, "widen slots");
-    // One k-step. Every step issues LPW loads (past the last step they re-read the last
-    // step's source into a stage nobody reads again), so at the top of step kt steps
-    // 0 .. kt+NS-1 are issued and step kt+1 must have landed: NS-2 newer steps in flight.
-    // MFMA i is followed by fragment read i/R_EVERY (weights first) and load i/L_EVERY;
-    // program order is issue order (the MFMAs are volatile asm, the rest memory accesses).
-    auto body = [&](int kt, auto first, FT (&ca)[C::MB], FT (&cb)[C::NBK], FT (&na)[C::MB],
-                    FT (&nb_)[C::NBK]) {
-        __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 2) * C::LPW, 0));
+    // One 32-wide substep: the MFMAs of (ca, cb), the fragment reads of the next substep
+    // from stage S at chunk offset fo, and (LOADS, the first substep of a stage) every load
+    // of stage ks into slot lbase. It starts with this wave's fragment reads complete and a
+    // barrier; a LOADS substep first also waits until no load is in flight, so the stage
+    // its reads need has landed and the slot it loads has been read by every wave.
+    // The barrier also keeps VALU writes of fragment registers (the prologue's widening)
+    // at least two wait states ahead of the MFMAs that read them: the MFMAs are inline
+    // assembly, which the compiler's hazard checks do not see.
+    auto sub = [&](auto first, auto loads, FT (&ca)[C::MB], FT (&cb)[C::NBK],
+                   FT (&na)[C::MB], FT (&nb_)[C::NBK], const char* S, int fo, int ks, char* lbase) {
+        __builtin_amdgcn_s_waitcnt(waitcnt_imm(decltype(loads)::value ? 0 : kNoVm, 0));
         barrier();
-        const int ks = kt + C::NS < KT_ ? kt + C::NS : KT_ - 1;
-        char* lbase = lds + (kt % C::NS) * C::STAGE;          // the stage step kt vacated
-        const char* S = lds + ((kt + 1) % C::NS) * C::STAGE;  // step kt+1 (past the end: unused)
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             mfma_agpr<decltype(first)::value>(acc[i / C::MB][i % C::MB], cb[i / C::MB], ca[i % C::MB]);
             if (i % R_EVERY == 0 && i / R_EVERY < NR) {
                 const int j = i / R_EVERY;
                 if (j < C::NBK) {
-                    if constexpr (MODE == kExpand) nb_[j] = *(const bf16x8*)b_at(S, j);
-                    else braw[j] = *(const bf16x8*)b_at(S, j);
+                    if constexpr (MODE == kExpand) nb_[j] = *(const bf16x8*)b_at(S, j, fo);
+                    else braw[j] = *(const bf16x8*)b_at(S, j, fo);
                 } else {
-                    na[j - C::NBK] = Frag<MODE>::acts(a_at(S, j - C::NBK));
+                    na[j - C::NBK] = Frag<MODE>::acts(a_at(S, j - C::NBK, fo));
                 }
             }
-            if (i % L_EVERY == 1 && i / L_EVERY < C::LPW) load(i / L_EVERY, ks, lbase);
+            if constexpr (decltype(loads)::value)
+                if (i % L_EVERY == 1 && i / L_EVERY < C::LPW) load(i / L_EVERY, ks, lbase);
             if constexpr (MODE != kExpand) {
-                // one dword of weight fragment d / 4 per slot, well after its LDS read
                 const int d = i - W_FROM;
                 if (d >= 0 && d < 4 * C::NBK) {
-                    const uint4 q = __builtin_bit_cast(uint4, braw[d / 4]);
-                    const uint32_t wv = (d % 4 == 0) ? q.x : (d % 4 == 1) ? q.y : (d % 4 == 2) ? q.z : q.w;
+                    const uint4 q4 = __builtin_bit_cast(uint4, braw[d / 4]);
+                    const uint32_t wv = (d % 4 == 0) ? q4.x : (d % 4 == 1) ? q4.y : (d % 4 == 2) ? q4.z : q4.w;
                     bw[d / 4][d % 4] = widen_pair_asm(wv);
                     if (d % 4 == 3)
                         nb_[d / 4] = __builtin_bit_cast(FT, uint4{bw[d / 4][0], bw[d / 4][1], bw[d / 4][2], bw[d / 4][3]});
@@ -385,25 +394,38 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
             }
         }
     };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
 
-    // prologue: NS steps in flight, step 0 landed, its fragments read
+    // prologue: stages 0 and 1 in flight, stage 0 landed, the fragments of substep 0 read
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s)
+    for (int q = 0; q < C::LPW; ++q) load(q, 0, lds);
 #pragma unroll
-        for (int q = 0; q < C::LPW; ++q) load(q, s < KT_ ? s : KT_ - 1, lds + s * C::STAGE);
-    __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::NS - 1) * C::LPW, kNoLgkm));
+    for (int q = 0; q < C::LPW; ++q) load(q, KT2 > 1 ? 1 : 0, lds + C::STAGE);
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(C::LPW, kNoLgkm));
     barrier();
 #pragma unroll
-    for (int nb = 0; nb < C::NBK; ++nb) bf[0][nb] = Frag<MODE>::weights(b_at(lds, nb));
+    for (int nb = 0; nb < C::NBK; ++nb) bf[0][nb] = Frag<MODE>::weights(b_at(lds, nb, foff0));
 #pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb) af[0][mb] = Frag<MODE>::acts(a_at(lds, mb));
-    body(0, std::true_type{}, af[0], bf[0], af[1], bf[1]);
-    body(1, std::false_type{}, af[1], bf[1], af[0], bf[0]);
-    for (int kt = 2; kt < KT_; kt += 2) {
-        body(kt, std::false_type{}, af[0], bf[0], af[1], bf[1]);
-        body(kt + 1, std::false_type{}, af[1], bf[1], af[0], bf[0]);
+    for (int mb = 0; mb < C::MB; ++mb) af[0][mb] = Frag<MODE>::acts(a_at(lds, mb, foff0));
+    // substep 0: stage 0, first half; reads its second half
+    sub(T_{}, F_{}, af[0], bf[0], af[1], bf[1], lds, foff1, 0, lds);
+    for (int kt = 0; kt + 1 < KT2; ++kt) {
+        char* cur = lds + (kt & 1) * C::STAGE;          // stage kt: free after the barrier
+        const char* nxt = lds + ((kt + 1) & 1) * C::STAGE;
+        const int ks = kt + 2 < KT2 ? kt + 2 : KT2 - 1;  // past the end: re-read, never used
+        // second half of stage kt; reads the first half of stage kt+1; loads stage kt+2
+        sub(F_{}, T_{}, af[1], bf[1], af[0], bf[0], nxt, foff0, ks, cur);
+        // first half of stage kt+1; reads its second half
+        sub(F_{}, F_{}, af[0], bf[0], af[1], bf[1], nxt, foff1, ks, cur);
     }
-    // no load still writing LDS at exit; the MFMA results are complete before VALU reads them
+    // second half of the last stage: MFMAs only (after the two wait states its fragments'
+    // last VALU writes need)
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 1" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NM; ++i) mfma_agpr<false>(acc[i / C::MB][i % C::MB], bf[1][i / C::MB], af[1][i % C::MB]);
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
