@@ -248,13 +248,25 @@ struct ICfg {
     static constexpr int QA = A_INSTR / NW, QB = B_INSTR / NW, LPW = QA + QB;
     static constexpr int STAGE = (A_ROWS + BNB) * 128;
     static constexpr int LDS_BYTES = NS * STAGE;
+    // schedule of a substep: MFMA i is followed by fragment read i / R_EVERY (weights
+    // first), load i / L_EVERY and, from slot W_FROM on, WPS dwords of weight widening
+    static constexpr int NM = NBK * MB, NR = NBK + MB;
+    static constexpr int R_EVERY = 3 * (NR - 1) < NM ? 3 : 2;
+    static constexpr int L_EVERY = NM / LPW;
+    static constexpr int W_FROM = R_EVERY * NBK + 2;
+    static constexpr int WPS = (4 * NBK + (NM - W_FROM) - 1) / (NM - W_FROM);
     static_assert(A_INSTR % NW == 0 && B_INSTR % NW == 0, "every wave issues the same loads");
     static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
     static_assert(LDS_BYTES <= 160 * 1024 - 1024, "LDS budget");
     static_assert(LPW <= 63, "vmcnt range");
+    static_assert(R_EVERY * (NR - 1) < NM && L_EVERY >= 1 && L_EVERY * (LPW - 1) + 1 < NM, "slots");
+    static_assert(W_FROM < NM && (NM - W_FROM) * WPS >= 4 * NBK, "widen slots");
 };
 
+// 256 x 256 tiles; an expert's last tile with at most 128 rows runs as a 128 x 256 tile
+// (each wave 64 x 128), which halves the MFMA work spent on padding rows.
 using LargeIl = ICfg<256, 256, 2, 2>;
+using LargeIlTail = ICfg<128, 256, 2, 2>;
 
 // MFMA through inline assembly with the accumulator pinned to AGPRs ("a" constraint):
 // 256 accumulators per lane exceed what the compiler keeps in AGPRs across a loop without
@@ -287,19 +299,10 @@ __device__ inline uint32_t widen_pair_asm(uint32_t w) {
     return out;
 }
 
+// One tile of configuration C: rows [row0, row1) of group e, N tile ntile, K slice kslice.
 template <class C, int MODE>
-__global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_upper, int nt,
-                                                         int group_n) {
-    extern __shared__ __attribute__((aligned(1024))) char lds[];
-    __shared__ int s_tile[3];
-    int64_t mt;
-    int ntile;
-    const int64_t per_slice = gridDim.x / g.ksplit;
-    const int kslice = (int)(blockIdx.x / per_slice);
-    if (!tile_of(blockIdx.x % per_slice, per_slice, mt_upper, nt, group_n, &mt, &ntile)) return;
-    if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
-    const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
-
+__device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int row0, int row1,
+                                        int ntile, int kslice) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / C::WN, wn = wave % C::WN;
@@ -351,11 +354,8 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
         asm volatile("" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
     };
-    constexpr int NM = C::NBK * C::MB;
-    constexpr int NR = C::NBK + C::MB;
-    constexpr int R_EVERY = 3, L_EVERY = NM / C::LPW, W_FROM = R_EVERY * C::NBK + 2;
-    static_assert(R_EVERY * (NR - 1) < NM && L_EVERY * (C::LPW - 1) + 1 < NM, "slots");
-    static_assert(W_FROM + 4 * C::NBK <= NM, "widen slots");
+    constexpr int NM = C::NM, NR = C::NR, R_EVERY = C::R_EVERY, L_EVERY = C::L_EVERY;
+    constexpr int W_FROM = C::W_FROM, WPS = C::WPS;
     // One 32-wide substep: the MFMAs of (ca, cb), the fragment reads of the next substep
     // from stage S at chunk offset fo, and (LOADS, the first substep of a stage) every load
     // of stage ks into slot lbase. It starts with this wave's fragment reads complete and a
@@ -383,13 +383,16 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
             if constexpr (decltype(loads)::value)
                 if (i % L_EVERY == 1 && i / L_EVERY < C::LPW) load(i / L_EVERY, ks, lbase);
             if constexpr (MODE != kExpand) {
-                const int d = i - W_FROM;
-                if (d >= 0 && d < 4 * C::NBK) {
-                    const uint4 q4 = __builtin_bit_cast(uint4, braw[d / 4]);
-                    const uint32_t wv = (d % 4 == 0) ? q4.x : (d % 4 == 1) ? q4.y : (d % 4 == 2) ? q4.z : q4.w;
-                    bw[d / 4][d % 4] = widen_pair_asm(wv);
-                    if (d % 4 == 3)
-                        nb_[d / 4] = __builtin_bit_cast(FT, uint4{bw[d / 4][0], bw[d / 4][1], bw[d / 4][2], bw[d / 4][3]});
+#pragma unroll
+                for (int w = 0; w < WPS; ++w) {
+                    const int d = (i - W_FROM) * WPS + w;
+                    if (i >= W_FROM && d < 4 * C::NBK) {
+                        const uint4 q4 = __builtin_bit_cast(uint4, braw[d / 4]);
+                        const uint32_t wv = (d % 4 == 0) ? q4.x : (d % 4 == 1) ? q4.y : (d % 4 == 2) ? q4.z : q4.w;
+                        bw[d / 4][d % 4] = widen_pair_asm(wv);
+                        if (d % 4 == 3)
+                            nb_[d / 4] = __builtin_bit_cast(FT, uint4{bw[d / 4][0], bw[d / 4][1], bw[d / 4][2], bw[d / 4][3]});
+                    }
                 }
             }
         }
@@ -432,6 +435,26 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
     GemmArgs gs = g;
     if (kslice) gs.out = (float*)g.out + (int64_t)kslice * g.rows_total * g.N;
     epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(gs, acc, row0, row1, ntile, wm, wn, lane);
+}
+
+template <class C, class CT, int MODE>
+__global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_upper, int nt,
+                                                         int group_n) {
+    static_assert(CT::NT == C::NT && CT::BNB == C::BNB && CT::BM <= C::BM && CT::WTN == C::WTN,
+                  "the tail tile runs on the same workgroup and N tiling");
+    extern __shared__ __attribute__((aligned(1024))) char lds[];
+    __shared__ int s_tile[3];
+    int64_t mt;
+    int ntile;
+    const int64_t per_slice = gridDim.x / g.ksplit;
+    const int kslice = (int)(blockIdx.x / per_slice);
+    if (!tile_of(blockIdx.x % per_slice, per_slice, mt_upper, nt, group_n, &mt, &ntile)) return;
+    if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
+    const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
+    if (row1 - row0 <= CT::BM)   // workgroup-uniform
+        il_tile<CT, MODE>(g, lds, e, row0, row1, ntile, kslice);
+    else
+        il_tile<C, MODE>(g, lds, e, row0, row1, ntile, kslice);
 }
 
 // --------------------------------------------------------------- staged kernel
@@ -659,7 +682,7 @@ template <class C, int MODE, bool IL>
 hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     const void* fn;
     if constexpr (IL)
-        fn = (const void*)gemm_il_kernel<C, MODE>;
+        fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE>;
     else
         fn = (const void*)gemm_staged_kernel<C, MODE>;
     static bool attr_set = false;  // idempotent; a race only repeats the same call
@@ -679,7 +702,7 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
         return v > 0 ? v : 4;
     }();
     if constexpr (IL)
-        gemm_il_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
+        gemm_il_kernel<C, LargeIlTail, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
     else
         gemm_staged_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
     return hipGetLastError();

@@ -245,6 +245,21 @@ def test_dense_swiglu_accumulate():
     assert torch.equal(y, base + y0), "accumulate must add the same values"
 
 
+@pytest.mark.parametrize("T", [513, 640, 641, 767, 768])
+def test_dense_swiglu_large_tile_tails(T, monkeypatch):
+    """One group of T rows on the 256 x 256 tiles: the last tile holds T mod 256 rows, and
+    runs on the 128-row tail shape when that remainder is at most 128."""
+    monkeypatch.setenv("PCM_GEMM_TILE", "L")
+    cfg = scaled(CONFIGS["finegrained_shared"], T=T, H=256, F=64, shared_F=512, name=f"dense{T}")
+    say(f"dense swiglu T={T}")
+    inp = make_inputs(cfg, seed=8)
+    d = dev(inp)
+    y = pcm.pcm_dense_swiglu(d["x"], *d["shared"])
+    torch.cuda.synchronize()
+    ref = oracle.dense_swiglu(inp.x, inp.s_gate, inp.s_up, inp.s_down)
+    assert_y_close(y.cpu().numpy(), ref, cfg.dtype, f"dense T={T}")
+
+
 def test_layer_is_deterministic():
     cfg = SMALL["olmoe_s"]
     d = dev(make_inputs(cfg, seed=7))
