@@ -134,6 +134,37 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
     route_token<EPL>(lg[wave], n, k, lane, ids + t * k, w + t * k);
 }
 
+// The same for many K slices (large H, few tokens): one workgroup per token, thread e
+// sums expert e's slices (independent loads, several in flight), then wave 0 runs the
+// top-k. The sum over slices runs in the same order as in router_topk_kernel.
+template <int EPL>
+__global__ __launch_bounds__(256) void router_topk_wide_kernel(const float* __restrict__ part,
+                                                               int64_t T, int n, int npad, int ks,
+                                                               int k, float* __restrict__ logits,
+                                                               int32_t* __restrict__ ids,
+                                                               float* __restrict__ w) {
+    __shared__ float lg[kMaxN];
+    const int64_t t = blockIdx.x;
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+        const float* p = part + t * npad + e;
+        const int64_t stride = T * npad;
+        float v = 0.0f;
+        int s = 0;
+        for (; s + 8 <= ks; s += 8) {
+            float q[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) q[j] = p[(s + j) * stride];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v += q[j];
+        }
+        for (; s < ks; ++s) v += p[s * stride];
+        lg[e] = v;
+        if (logits) logits[t * n + e] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) route_token<EPL>(lg, n, k, threadIdx.x, ids + t * k, w + t * k);
+}
+
 // float32: one wavefront per token; lane e (+64 j) forms x_t . W_r[e] with h ascending.
 __global__ __launch_bounds__(256) void router_f32_kernel(const float* __restrict__ x,
                                                          const float* __restrict__ wr, int64_t T,
@@ -207,6 +238,16 @@ hipError_t launch_router(bool bf16, const void* x, const void* wr, int64_t T, in
         (const uint16_t*)x, (const uint16_t*)wr, T, H, n, et, tt, ks, steps, part);
     const dim3 grid((unsigned)ceil_div(T, 4)), block(256);
     const int npad = et * 16;
+    if (ks * ceil_div(n, 64) > 16) {   // long serial sums per lane: spread them over a workgroup
+        const dim3 wgrid((unsigned)T);
+        switch (ceil_div(n, 64)) {
+            case 1: router_topk_wide_kernel<1><<<wgrid, block, 0, s>>>(part, T, n, npad, ks, k, logits, ids, w); break;
+            case 2: router_topk_wide_kernel<2><<<wgrid, block, 0, s>>>(part, T, n, npad, ks, k, logits, ids, w); break;
+            case 3: router_topk_wide_kernel<3><<<wgrid, block, 0, s>>>(part, T, n, npad, ks, k, logits, ids, w); break;
+            default: router_topk_wide_kernel<4><<<wgrid, block, 0, s>>>(part, T, n, npad, ks, k, logits, ids, w); break;
+        }
+        return hipGetLastError();
+    }
     switch (ceil_div(n, 64)) {
         case 1: router_topk_kernel<1><<<grid, block, 0, s>>>(part, T, n, npad, ks, k, logits, ids, w); break;
         case 2: router_topk_kernel<2><<<grid, block, 0, s>>>(part, T, n, npad, ks, k, logits, ids, w); break;
