@@ -289,6 +289,23 @@ def test_layer_full_size(name):
     assert np.isfinite(y).all()
 
 
+def test_layer_split_k_projection_at_scale():
+    """Few output tiles per row block and a long F: the large-tile projection splits K in two
+    slices over hundreds of tiles. Sampled tokens against the oracle, bit-identical reruns."""
+    cfg = scaled(CONFIGS["mixtral"], T=8192, H=1024, F=4096, name="split_k")
+    say("split-K projection at scale: generating inputs")
+    inp = make_inputs(cfg, seed=12)
+    d = dev(inp)
+    y = run_layer(d, cfg.k)
+    y2 = run_layer(d, cfg.k)
+    assert np.array_equal(y, y2), "the K slices must give the same sums every run"
+    rng = np.random.default_rng(13)
+    tokens = np.unique(np.concatenate([[0, cfg.T - 1], rng.choice(cfg.T, 96, replace=False)]))
+    say(f"split-K projection at scale: oracle on {tokens.size} tokens")
+    ref = oracle.layer_inputs(inp, tokens=tokens)
+    assert_y_close(y[tokens], ref, cfg.dtype, "split-K at scale")
+
+
 # ------------------------------------------- per-path execution (ablation baselines)
 @pytest.mark.parametrize("reuse", [1, 0])
 @pytest.mark.parametrize("name", ["tiny", "mixtral_s", "olmoe_s", "fine_s", "decode_s"])
