@@ -172,18 +172,21 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
             for (int i = 0; i < 8; ++i) zz[it][b][i] = 0.f;
         const int c = (threadIdx.x + it * blockDim.x) * 8;
         if (c >= F) continue;
-        // sources in ascending order, each row's 8 values added to every target it feeds
+        // sources in ascending order, each row's 8 values added to every target it feeds;
+        // the loads of all sources are issued before the first multiply-add
+        float ua[KK][8];
+#pragma unroll
+        for (int a = 0; a < KK; ++a)
+            if (a < p.ns) load8(u + p.src[a] * F + c, ua[a]);
 #pragma unroll
         for (int a = 0; a < KK; ++a) {
             if (a >= p.ns) break;
-            float ua[8];
-            load8(u + p.src[a] * F + c, ua);
 #pragma unroll
             for (int b = 0; b < KK; ++b) {
                 if (b < p.nt && ((p.bits >> (a * p.K + b)) & 1)) {
                     const float w = p.beta ? p.beta[a * p.K + b] : 1.0f;
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) zz[it][b][i] = fmaf(w, ua[i], zz[it][b][i]);
+                    for (int i = 0; i < 8; ++i) zz[it][b][i] = fmaf(w, ua[a][i], zz[it][b][i]);
                 }
             }
         }
@@ -249,12 +252,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     const TokenPaths p = token_paths(m, t);
     for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
         float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (ksplit <= 2) {
+            // every row's loads issued before the first add; the adds keep the order below
+            float4 v[kMaxK][2];
 #pragma unroll
-        for (int b = 0; b < kMaxK; ++b) {
-            if (b >= p.nt) break;
-            for (int q = 0; q < ksplit; ++q) {  // K slices of the projection, in order
-                const float4 v = *(const float4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c);
-                s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+            for (int b = 0; b < kMaxK; ++b)
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    if (b < p.nt && q < ksplit)
+                        v[b][q] = *(const float4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c);
+#pragma unroll
+            for (int b = 0; b < kMaxK; ++b)
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    if (b < p.nt && q < ksplit) {
+                        s.x += v[b][q].x; s.y += v[b][q].y; s.z += v[b][q].z; s.w += v[b][q].w;
+                    }
+        } else {
+#pragma unroll
+            for (int b = 0; b < kMaxK; ++b) {
+                if (b >= p.nt) break;
+                for (int q = 0; q < ksplit; ++q) {  // K slices of the projection, in order
+                    const float4 v = *(const float4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c);
+                    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+                }
             }
         }
         float4* dst = (float4*)(y + t * H + c);
