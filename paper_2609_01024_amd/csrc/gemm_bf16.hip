@@ -108,15 +108,19 @@ __device__ bool find_tile(const int32_t* __restrict__ offsets, int n, int64_t a_
 // N-tiles: inside a group the M-tile varies slowest, so the workgroups resident on one XCD
 // at a time share a few weight tiles (same expert, neighbouring M-tiles) and a few
 // activation tiles (same M-tile, neighbouring N-tiles) through that XCD's L2.
-__device__ inline bool tile_of(int64_t bid, int64_t grid, int64_t mt_upper, int nt, int GN,
-                               int64_t* mt, int* ntile) {
-    const int64_t id = (bid % 8) * (grid / 8) + bid / 8;
-    if (id >= mt_upper * nt) return false;
-    const int64_t gsize = (int64_t)GN * mt_upper;
+__device__ inline void tile_from_id(int64_t id, int64_t mt_count, int nt, int GN, int64_t* mt,
+                                    int* ntile) {
+    const int64_t gsize = (int64_t)GN * mt_count;
     const int64_t grp = id / gsize, in = id % gsize;
     const int64_t gn = min<int64_t>(GN, nt - grp * GN);
     *mt = in / gn;
     *ntile = (int)(grp * GN + in % gn);
+}
+__device__ inline bool tile_of(int64_t bid, int64_t grid, int64_t mt_upper, int nt, int GN,
+                               int64_t* mt, int* ntile) {
+    const int64_t id = (bid % 8) * (grid / 8) + bid / 8;
+    if (id >= mt_upper * nt) return false;
+    tile_from_id(id, mt_upper, nt, GN, mt, ntile);
     return true;
 }
 
@@ -437,21 +441,111 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
     epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(gs, acc, row0, row1, ntile, wm, wn, lane);
 }
 
-template <class C, class CT, int MODE>
+// Work item of workgroup bid for the large-tile kernel, longest first. A group of c rows has
+// c / BM full tiles and, if rows remain, one remainder tile: a long item when more than TBM
+// rows remain, a short (tail-shape) item otherwise. Workgroups are dispatched round-robin over
+// the 8 XCDs (bid % 8) and in bid order within each; each XCD's run of ids holds its eighth of
+// the long items (every K slice) and then its eighth of the short items, so the short tiles
+// fill the last round instead of lengthening it. Within each list the order is the grouped
+// one of tile_from_id. Wave 0 counts and searches; the result is broadcast through LDS
+// (s_item: group, row0, row1, ntile, kslice, valid). Returns false past the last item.
+template <int BM, int TBM>
+__device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        int lo[4], full[4], nl[4], ns[4], suml = 0, sums = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int x = lane * 4 + j;
+            int c = 0, b = 0;
+            if (g.offsets == nullptr) {
+                if (x == 0) c = (int)g.a_rows;
+            } else if (x < g.n) {
+                b = g.offsets[x];
+                c = g.offsets[x + 1] - b;
+            }
+            const int rem = c % BM;
+            lo[j] = b;
+            full[j] = c / BM;
+            nl[j] = full[j] + (rem > TBM ? 1 : 0);
+            ns[j] = (rem > 0 && rem <= TBM) ? 1 : 0;
+            suml += nl[j];
+            sums += ns[j];
+        }
+        int incl = suml, incs = sums;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int vl = __shfl_up(incl, d), vs = __shfl_up(incs, d);
+            if (lane >= d) { incl += vl; incs += vs; }
+        }
+        const int64_t Lt = __shfl(incl, 63), St = __shfl(incs, 63);
+        const int64_t LT = Lt * nt * g.ksplit, ST = St * nt * g.ksplit;
+        const int64_t x8 = blockIdx.x % 8, j8 = blockIdx.x / 8;
+        const int64_t l0 = x8 * LT / 8, l1 = (x8 + 1) * LT / 8;
+        const int64_t s0 = x8 * ST / 8, s1 = (x8 + 1) * ST / 8;
+        bool valid = true, is_long = true;
+        int64_t item = 0, count = Lt;
+        if (j8 < l1 - l0) {
+            item = l0 + j8;
+        } else if (j8 - (l1 - l0) < s1 - s0) {
+            item = s0 + j8 - (l1 - l0);
+            is_long = false;
+            count = St;
+        } else {
+            valid = false;
+        }
+        if (lane == 0) s_item[5] = valid ? 1 : 0;
+        if (valid) {
+            const int64_t per_slice = count * nt;
+            const int kslice = (int)(item / per_slice);
+            int64_t m;
+            int ntile;
+            tile_from_id(item % per_slice, count, nt, GN, &m, &ntile);
+            // group holding list entry m: this lane's groups start at the exclusive prefix
+            int start = is_long ? incl - suml : incs - sums;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int cnt = is_long ? nl[j] : ns[j];
+                if (m >= start && m < start + cnt) {
+                    const int r0 = lo[j] + (is_long ? (int)(m - start) * BM : full[j] * BM);
+                    const int end = g.offsets == nullptr ? (int)g.a_rows : g.offsets[lane * 4 + j + 1];
+                    s_item[0] = lane * 4 + j;
+                    s_item[1] = r0;
+                    s_item[2] = min(end, r0 + BM);
+                    s_item[3] = ntile;
+                    s_item[4] = kslice;
+                }
+                start += cnt;
+            }
+        }
+    }
+    __syncthreads();
+    return s_item[5] != 0;
+}
+
+// LONGEST_FIRST: the work order of il_item (measured better for the projection); otherwise
+// the grouped tile order of tile_of (better for the expansion, whose weight tiles are shared
+// by the concurrently running row blocks of one expert).
+template <class C, class CT, int MODE, bool LONGEST_FIRST>
 __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_upper, int nt,
                                                          int group_n) {
     static_assert(CT::NT == C::NT && CT::BNB == C::BNB && CT::BM <= C::BM && CT::WTN == C::WTN,
                   "the tail tile runs on the same workgroup and N tiling");
     extern __shared__ __attribute__((aligned(1024))) char lds[];
-    __shared__ int s_tile[3];
-    int64_t mt;
-    int ntile;
-    const int64_t per_slice = gridDim.x / g.ksplit;
-    const int kslice = (int)(blockIdx.x / per_slice);
-    if (!tile_of(blockIdx.x % per_slice, per_slice, mt_upper, nt, group_n, &mt, &ntile)) return;
-    if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
-    const int e = s_tile[0], row0 = s_tile[1], row1 = s_tile[2];
-    if (row1 - row0 <= CT::BM)   // workgroup-uniform
+    __shared__ int s_item[6];
+    int e, row0, row1, ntile, kslice;
+    if constexpr (LONGEST_FIRST) {
+        if (!il_item<C::BM, CT::BM>(g, nt, group_n, s_item)) return;   // workgroup-uniform
+        e = s_item[0], row0 = s_item[1], row1 = s_item[2], ntile = s_item[3], kslice = s_item[4];
+    } else {
+        int64_t mt;
+        const int64_t per_slice = gridDim.x / g.ksplit;
+        kslice = (int)(blockIdx.x / per_slice);
+        if (!tile_of(blockIdx.x % per_slice, per_slice, mt_upper, nt, group_n, &mt, &ntile)) return;
+        if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_item)) return;
+        e = s_item[0], row0 = s_item[1], row1 = s_item[2];
+    }
+    if (row1 - row0 <= CT::BM)
         il_tile<CT, MODE>(g, lds, e, row0, row1, ntile, kslice);
     else
         il_tile<C, MODE>(g, lds, e, row0, row1, ntile, kslice);
@@ -682,7 +776,7 @@ template <class C, int MODE, bool IL>
 hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     const void* fn;
     if constexpr (IL)
-        fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE>;
+        fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE, MODE != kExpand>;
     else
         fn = (const void*)gemm_staged_kernel<C, MODE>;
     static bool attr_set = false;  // idempotent; a race only repeats the same call
@@ -694,17 +788,23 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     const int64_t mt_upper = g.offsets ? ceil_div(R, C::BM) + g.n : ceil_div(R, C::BM);
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
     const int nt = (int)ceil_div(g.N, kOutCols);
-    const int64_t grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
     if (mt_upper * nt <= 0) return hipSuccess;
     static const int group_n = [] {
         const char* env = getenv("PCM_GEMM_GROUP_N");
         const int v = env ? atoi(env) : 4;
         return v > 0 ? v : 4;
     }();
-    if constexpr (IL)
-        gemm_il_kernel<C, LargeIlTail, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
-    else
+    if constexpr (IL) {
+        // longest first: each XCD's run holds at most ceil(long / 8) + ceil(short / 8) items
+        constexpr bool kLf = MODE != kExpand;
+        const int64_t grid = kLf ? (ceil_div(mt_upper * nt * g.ksplit, 8) + 2) * 8
+                                 : ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
+        gemm_il_kernel<C, LargeIlTail, MODE, kLf><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(
+            g, mt_upper, nt, group_n);
+    } else {
+        const int64_t grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
         gemm_staged_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
+    }
     return hipGetLastError();
 }
 
