@@ -22,6 +22,8 @@
 //    next substep (and, once per stage, the loads of the stage after next). LDS rows are
 //    128 bytes; the 16-byte chunk c of row r sits at position c ^ ((r >> 1) & 7), which
 //    keeps the fragment reads (16 rows x 4 chunks per instruction) free of bank conflicts.
+//    A group's last tile with at most 128 rows runs as a 128 x 256 tile (64 x 128 per wave)
+//    in the same launch.
 //  * "staged" (medium tiles): loads through registers into two LDS stages of 64-wide K
 //    steps; rows of 128 bytes with chunk c of row r at position c ^ ((r >> 1) & 7).
 //  * "stream" (a few rows per group, decode): no LDS, fragments loaded straight into a
@@ -31,9 +33,11 @@
 // expansion, a wave's weight rows are half gate and half up for the same columns, so the
 // gate and up values of an output element sit in the same lane and register slot.
 //
-// Work decomposition: the grid is (upper bound of M tiles) x (N tiles). Each workgroup
-// finds its group (expert) and row range from the group offsets with one wave-wide scan
-// of per-group tile counts; workgroups past the last tile exit.
+// Work decomposition: the grid is (upper bound of M tiles) x (N tiles) (x K slices). Each
+// workgroup finds its group (expert) and row range from the group offsets with one wave-wide
+// scan of per-group tile counts; workgroups past the last tile exit. The expansion walks the
+// tiles in an XCD-aware grouped order (tile_of); the large-tile projection lists each XCD's
+// full-height tiles before its 128-row tail tiles (il_item), so the short ones come last.
 #include <stdlib.h>
 #include <string.h>
 
