@@ -15,9 +15,11 @@
 //
 // Three kernel shapes share the epilogue and the work decomposition:
 //  * "interleaved" (large tiles, 256 x 256): four waves, one per SIMD, each owning a 128 x 128
-//    block of C in 256 accumulation registers. Global -> LDS direct loads
-//    (global_load_lds_dwordx4, no register staging) of 64-wide K stages, double-buffered,
-//    each load covering 8 whole 128-byte rows; one workgroup barrier per 32-wide substep,
+//    block of C in 256 accumulation registers. Global -> LDS direct buffer loads
+//    (buffer_load_dwordx4 ... lds, no register staging: one 32-bit offset per lane for the
+//    whole tile, the stage's K offset in a scalar register) of 64-wide K stages,
+//    double-buffered, each load covering 8 whole 128-byte rows; one workgroup barrier per
+//    32-wide substep,
 //    within which each wave issues its 64 MFMAs interleaved with the fragment reads of the
 //    next substep (and, once per stage, the loads of the stage after next). LDS rows are
 //    128 bytes; the 16-byte chunk c of row r sits at position c ^ ((r >> 1) & 7), which
@@ -35,9 +37,13 @@
 //
 // Work decomposition: the grid is (upper bound of M tiles) x (N tiles) (x K slices). Each
 // workgroup finds its group (expert) and row range from the group offsets with one wave-wide
-// scan of per-group tile counts; workgroups past the last tile exit. The expansion walks the
-// tiles in an XCD-aware grouped order (tile_of); the large-tile projection lists each XCD's
-// full-height tiles before its 128-row tail tiles (il_item), so the short ones come last.
+// scan of per-group tile counts; workgroups past the last tile exit. Every order is
+// XCD-aware (workgroup ids are dispatched round-robin over the 8 XCDs). Grouped rows of the
+// large tiles walk an expert-major order (em_item: all row blocks of one expert for a few
+// N tiles at a time, so a weight tile is fetched while every row block that needs it runs);
+// a K-split projection lists each XCD's full-height tiles before its 128-row tail tiles
+// (il_item); one group of rows (the dense shared expert) and the medium tiles use the
+// grouped order of tile_of.
 #include <stdlib.h>
 #include <string.h>
 
@@ -153,6 +159,27 @@ __device__ inline const uint16_t* b_source_row(const GemmArgs& g, int e, int nti
     int h = ntile * OUT_COLS + j;
     h = h < g.N ? h : g.N - 1;
     return (const uint16_t*)g.b0 + ((int64_t)e * g.N + h) * g.K;
+}
+
+// Weight row (within its expert) of B row j of the tile, and whether it is an up row (the
+// expansion's second half); rows past N repeat row N - 1 (their outputs are never stored).
+// `up` is uniform over a load of 8 rows.
+template <int MODE, int WTN, int OUT_COLS>
+__device__ inline int b_source_col(const GemmArgs& g, int ntile, int j, bool* up) {
+    if (MODE == kExpand) {
+        const int grp = j / WTN, jj = j % WTN, half = jj / (WTN / 2);
+        const int f = ntile * OUT_COLS + grp * (WTN / 2) + jj % (WTN / 2);
+        *up = half != 0;
+        return f < g.N ? f : g.N - 1;
+    }
+    const int h = ntile * OUT_COLS + j;
+    *up = false;
+    return h < g.N ? h : g.N - 1;
+}
+
+// Raw buffer resource over `bytes` bytes at `base` (loads past the end read zero).
+__device__ inline __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
 // Row of `a` (and of row_scale) behind output row r.
@@ -319,28 +346,38 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
 
     // load q of a lane: LDS row blk * 8 + lane / 8 of the A or B region, 16-byte position
-    // lane % 8, holding chunk (lane % 8) ^ ((row >> 1) & 7) of that row
-    const char* src[C::LPW];
+    // lane % 8, holding chunk (lane % 8) ^ ((row >> 1) & 7) of that row. Loads are buffer
+    // loads: a 32-bit byte offset per lane (fixed for the tile) and the stage's K offset as
+    // the uniform scalar offset, against resources for `a` and for expert e's weights.
+    uint32_t voff[C::LPW];
     int dst[C::LPW];
     const int lrow = lane >> 3;
+    const int64_t wbytes = (int64_t)g.N * g.K * 2;   // one expert's weights
+    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(g.a, (uint32_t)((int64_t)g.a_rows * g.K * 2));
+    const __amdgpu_buffer_rsrc_t rb0 = buffer_rsrc((const char*)g.b0 + e * wbytes, (uint32_t)wbytes);
+    const __amdgpu_buffer_rsrc_t rb1 =
+        MODE == kExpand ? buffer_rsrc((const char*)g.b1 + e * wbytes, (uint32_t)wbytes) : rb0;
+    bool up[C::LPW];
 #pragma unroll
     for (int q = 0; q < C::LPW; ++q) {
+        up[q] = false;
         if (q < C::QA) {
             const int blk = q * C::NW + wave, lr = blk * 8 + lrow;
             const int chunk = (lane & 7) ^ ((lr >> 1) & 7);
             const int64_t srow = a_source_row(g, row0 + lr, row1);
-            src[q] = (const char*)g.a + srow * (int64_t)g.K * 2 + k_byte0 + chunk * 16;
+            voff[q] = (uint32_t)(srow * (int64_t)g.K * 2 + k_byte0 + chunk * 16);
             dst[q] = blk * 1024;
         } else {
             const int blk = (q - C::QA) * C::NW + wave, lb = blk * 8 + lrow;
             const int chunk = (lane & 7) ^ ((lb >> 1) & 7);
-            src[q] = (const char*)b_source_row<MODE, C::WTN, kOutCols>(g, e, ntile, lb) + k_byte0 + chunk * 16;
+            const int f = b_source_col<MODE, C::WTN, kOutCols>(g, ntile, lb, &up[q]);
+            voff[q] = (uint32_t)((int64_t)f * g.K * 2 + k_byte0 + chunk * 16);
             dst[q] = C::A_ROWS * 128 + blk * 1024;
         }
     }
     auto load = [&](int q, int ks, char* base) {
-        __builtin_amdgcn_global_load_lds((const void*)(src[q] + (int64_t)ks * 128),
-                                         (PCM_LDS void*)(base + dst[q]), 16, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(q < C::QA ? ra : (up[q] ? rb1 : rb0),
+                                                 (PCM_LDS void*)(base + dst[q]), 16, voff[q], ks * 128, 0, 0);
     };
 
     floatx4 acc[C::NBK][C::MB];
@@ -527,19 +564,93 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
     return s_item[5] != 0;
 }
 
-// LONGEST_FIRST: the work order of il_item (measured better for the projection); otherwise
-// the grouped tile order of tile_of (better for the expansion, whose weight tiles are shared
-// by the concurrently running row blocks of one expert).
-template <class C, class CT, int MODE, bool LONGEST_FIRST>
+// Work item of workgroup bid in the expert-major order. Group x has m_x = ceil(rows / BM)
+// M-tiles; its m_x * nt items are walked in blocks of gn_x N-tiles (gn_x = window / m_x,
+// at least 1), the M-tile varying slowest within a block, so that the `window` workgroups
+// an XCD runs at once cover all of a group's rows for a few N-tiles: each weight tile is
+// fetched while every row block that needs it runs, each activation tile once per block.
+// Each XCD (bid % 8) takes a contiguous eighth of the list (every K slice, slice-major).
+// Wave 0 counts and searches; the result is broadcast through LDS as for il_item.
+template <int BM>
+__device__ bool em_item(const GemmArgs& g, int nt, int window, int* s_item) {
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        int lo[4], cnt[4], m[4], local = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int x = lane * 4 + j;
+            int c = 0, b = 0;
+            if (g.offsets == nullptr) {
+                if (x == 0) c = (int)g.a_rows;
+            } else if (x < g.n) {
+                b = g.offsets[x];
+                c = g.offsets[x + 1] - b;
+            }
+            lo[j] = b;
+            cnt[j] = c;
+            m[j] = (int)ceil_div(c, BM);
+            local += m[j] * nt;
+        }
+        int incl = local;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int v = __shfl_up(incl, d);
+            if (lane >= d) incl += v;
+        }
+        const int64_t Tt = __shfl(incl, 63), TT = Tt * g.ksplit;
+        const int64_t x8 = blockIdx.x % 8, j8 = blockIdx.x / 8;
+        const int64_t l0 = x8 * TT / 8, l1 = (x8 + 1) * TT / 8;
+        const bool valid = j8 < l1 - l0;
+        if (lane == 0) s_item[5] = valid ? 1 : 0;
+        if (valid) {
+            const int64_t item = l0 + j8;
+            const int kslice = (int)(item / Tt);
+            const int64_t id = item % Tt;
+            int64_t start = incl - local;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t items = (int64_t)m[j] * nt;
+                if (id >= start && id < start + items) {
+                    const int64_t l = id - start;
+                    int gn = window / m[j];
+                    gn = gn < 1 ? 1 : (gn > nt ? nt : gn);
+                    const int64_t gsize = (int64_t)gn * m[j];
+                    const int64_t grp = l / gsize, in = l % gsize;
+                    const int gcols = (int)min<int64_t>(gn, nt - grp * gn);
+                    const int mm = (int)(in / gcols);
+                    const int r0 = lo[j] + mm * BM;
+                    s_item[0] = lane * 4 + j;
+                    s_item[1] = r0;
+                    s_item[2] = min(lo[j] + cnt[j], r0 + BM);
+                    s_item[3] = (int)(grp * gn + in % gcols);
+                    s_item[4] = kslice;
+                }
+                start += items;
+            }
+        }
+    }
+    __syncthreads();
+    return s_item[5] != 0;
+}
+
+// Work orders of the large-tile kernel.
+enum IlOrder { kGrouped = 0, kLongestFirst = 1, kExpertMajor = 2 };
+
+// order (an IlOrder): kLongestFirst is the order of il_item, kGrouped the grouped order of
+// tile_of, kExpertMajor the order of em_item (group_n is then the window).
+template <class C, class CT, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_upper, int nt,
-                                                         int group_n) {
+                                                         int group_n, int order) {
     static_assert(CT::NT == C::NT && CT::BNB == C::BNB && CT::BM <= C::BM && CT::WTN == C::WTN,
                   "the tail tile runs on the same workgroup and N tiling");
     extern __shared__ __attribute__((aligned(1024))) char lds[];
     __shared__ int s_item[6];
     int e, row0, row1, ntile, kslice;
-    if constexpr (LONGEST_FIRST) {
-        if (!il_item<C::BM, CT::BM>(g, nt, group_n, s_item)) return;   // workgroup-uniform
+    if (order == kLongestFirst) {          // workgroup-uniform branches and returns
+        if (!il_item<C::BM, CT::BM>(g, nt, group_n, s_item)) return;
+        e = s_item[0], row0 = s_item[1], row1 = s_item[2], ntile = s_item[3], kslice = s_item[4];
+    } else if (order == kExpertMajor) {
+        if (!em_item<C::BM>(g, nt, group_n, s_item)) return;
         e = s_item[0], row0 = s_item[1], row1 = s_item[2], ntile = s_item[3], kslice = s_item[4];
     } else {
         int64_t mt;
@@ -778,14 +889,19 @@ hipError_t launch_stream(const GemmArgs& g, int64_t R, hipStream_t s) {
 // ---------------------------------------------------------------------- launch
 template <class C, int MODE, bool IL>
 hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
-    const void* fn;
-    if constexpr (IL)
-        fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE, MODE != kExpand>;
-    else
-        fn = (const void*)gemm_staged_kernel<C, MODE>;
+    // work order of the large tiles, for tests and tuning (read on every call, like
+    // PCM_GEMM_TILE): PCM_GEMM_ORDER_EXPAND / PCM_GEMM_ORDER_DOWN = 0 grouped, 1 longest
+    // first, 2 expert-major; PCM_GEMM_EM_WINDOW sets the expert-major window
+    const char* order_s = getenv(MODE == kExpand ? "PCM_GEMM_ORDER_EXPAND" : "PCM_GEMM_ORDER_DOWN");
+    const int order_env = order_s ? atoi(order_s) : -1;
     static bool attr_set = false;  // idempotent; a race only repeats the same call
     if (!attr_set) {
-        hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+        const void* fn;
+        if constexpr (IL)
+            fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE>;
+        else
+            fn = (const void*)gemm_staged_kernel<C, MODE>;
+        const hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
         if (err != hipSuccess) return err;
         attr_set = true;
     }
@@ -799,12 +915,29 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
         return v > 0 ? v : 4;
     }();
     if constexpr (IL) {
-        // longest first: each XCD's run holds at most ceil(long / 8) + ceil(short / 8) items
-        constexpr bool kLf = MODE != kExpand;
-        const int64_t grid = kLf ? (ceil_div(mt_upper * nt * g.ksplit, 8) + 2) * 8
-                                 : ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
-        gemm_il_kernel<C, LargeIlTail, MODE, kLf><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(
-            g, mt_upper, nt, group_n);
+        // default: expert-major for grouped rows (the projection's K-split launches keep the
+        // longest-first order, one group of rows the orders tuned for it)
+        int order = order_env;
+        if (order < 0 || order > 2) {
+            if (g.offsets == nullptr) order = MODE == kExpand ? kGrouped : kLongestFirst;
+            else order = (MODE != kExpand && g.ksplit > 1) ? kLongestFirst : kExpertMajor;
+        }
+        int64_t grid;
+        int gparam = group_n;
+        if (order == kLongestFirst) {
+            // each XCD's run holds at most ceil(long / 8) + ceil(short / 8) items
+            grid = (ceil_div(mt_upper * nt * g.ksplit, 8) + 2) * 8;
+        } else if (order == kExpertMajor) {
+            // each XCD's run holds at most ceil(items / 8) <= ceil(mt_upper * nt * ksplit / 8)
+            const char* win_s = getenv("PCM_GEMM_EM_WINDOW");
+            const int window = win_s ? atoi(win_s) : 12;
+            grid = ceil_div(mt_upper * nt * g.ksplit, 8) * 8;
+            gparam = window > 0 ? window : 12;
+        } else {
+            grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
+        }
+        gemm_il_kernel<C, LargeIlTail, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(
+            g, mt_upper, nt, gparam, order);
     } else {
         const int64_t grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
         gemm_staged_kernel<C, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(g, mt_upper, nt, group_n);
@@ -814,12 +947,16 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
 
 // Tile shape: an environment override (PCM_GEMM_TILE = S | M | L) for tests and tuning,
 // otherwise by the mean rows per group.
-char pick_tile(int64_t R, int groups) {
+// The large tiles address `a` and one group's weights through 32-bit buffer offsets, so
+// both must stay below 4 GiB (a_bytes: all rows of `a`; w_bytes: one group's weights).
+char pick_tile(int64_t R, int groups, int64_t a_bytes, int64_t w_bytes) {
+    const bool large_ok = a_bytes < (int64_t(1) << 32) && w_bytes < (int64_t(1) << 32);
     const char* env = getenv("PCM_GEMM_TILE");
-    if (env && (env[0] == 'S' || env[0] == 'M' || env[0] == 'L')) return env[0];
+    if (env && (env[0] == 'S' || env[0] == 'M' || env[0] == 'L'))
+        return env[0] == 'L' && !large_ok ? 'M' : env[0];
     const int64_t mean = R / (groups > 0 ? groups : 1);
     if (mean <= 48) return 'S';
-    if (mean < 512) return 'M';
+    if (mean < 512 || !large_ok) return 'M';
     return 'L';
 }
 
@@ -827,7 +964,7 @@ char pick_tile(int64_t R, int groups) {
 
 int down_ksplit(int64_t R, int n, int H, int F) {
     // only the large-tile kernel slices K; its grid is (R/256 + n) x (H/256) tiles
-    if (pick_tile(R, n) != 'L') return 1;
+    if (pick_tile(R, n, R * F * 2, (int64_t)H * F * 2) != 'L') return 1;
     const int64_t tiles = (ceil_div(R, 256) + n) * ceil_div(H, 256);
     return (tiles < 4 * 256 && (F / 2) % 64 == 0 && F / 32 >= 128) ? 2 : 1;
 }
@@ -835,7 +972,7 @@ int down_ksplit(int64_t R, int n, int H, int F) {
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStream_t s) {
     GemmArgs g = g0;
     if (g.ksplit < 1) g.ksplit = 1;
-    const char t = pick_tile(R, g.offsets ? g.n : 1);
+    const char t = pick_tile(R, g.offsets ? g.n : 1, g.a_rows * g.K * 2, (int64_t)g.N * g.K * 2);
     if (g.ksplit > 1 && (mode != kDownStore || t != 'L')) return hipErrorInvalidValue;
     switch (mode) {
         case kExpand:

@@ -260,6 +260,27 @@ def test_dense_swiglu_large_tile_tails(T, monkeypatch):
     assert_y_close(y.cpu().numpy(), ref, cfg.dtype, f"dense T={T}")
 
 
+@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "splitk_s"])
+def test_large_tile_work_orders_bit_identical(name, monkeypatch):
+    """The work order of the large tiles (grouped, longest first, expert-major with several
+    windows) decides only which workgroup computes which tile: the layer output must be the
+    same bits under every order, and within tolerance of the oracle."""
+    monkeypatch.setenv("PCM_GEMM_TILE", "L")
+    cfg = SMALL[name]
+    inp = make_inputs(cfg, seed=21)
+    d = dev(inp)
+    base = run_layer(d, cfg.k)
+    assert_y_close(base, oracle.layer_inputs(inp), cfg.dtype, f"{name}/default order")
+    for order, window in [(0, None), (1, None), (2, "1"), (2, "5"), (2, "12"), (2, "64")]:
+        say(f"work order {order} window {window} on {name}")
+        monkeypatch.setenv("PCM_GEMM_ORDER_EXPAND", str(order))
+        monkeypatch.setenv("PCM_GEMM_ORDER_DOWN", str(order))
+        if window is not None:
+            monkeypatch.setenv("PCM_GEMM_EM_WINDOW", window)
+        y = run_layer(d, cfg.k)
+        assert np.array_equal(y, base), f"{name}: order {order} window {window} changed the output"
+
+
 def test_layer_is_deterministic():
     cfg = SMALL["olmoe_s"]
     d = dev(make_inputs(cfg, seed=7))
