@@ -264,12 +264,28 @@ def test_dense_swiglu_large_tile_tails(T, monkeypatch):
 def test_large_tile_work_orders_bit_identical(name, monkeypatch):
     """The work order of the large tiles (grouped, longest first, expert-major with several
     windows) decides only which workgroup computes which tile: the layer output must be the
-    same bits under every order, and within tolerance of the oracle."""
+    same bits under every order, and within tolerance of the oracle. Every intermediate
+    buffer is filled with NaN before each run, so a tile that no workgroup computes shows."""
     monkeypatch.setenv("PCM_GEMM_TILE", "L")
     cfg = SMALL[name]
     inp = make_inputs(cfg, seed=21)
     d = dev(inp)
-    base = run_layer(d, cfg.k)
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, DEV, cfg.shared_F)
+
+    def run():
+        plan.u.fill_(float("nan"))
+        plan.y.fill_(float("nan"))
+        for ws in (plan.ws_proj, plan.ws_shared):
+            if ws is not None:
+                ws.fill_(0xFF)   # NaN in float16 and float32 alike
+        y = plan.forward(d["x"], d["logits"], d["mask"], d["w_gate"], d["w_up"], d["w_down"],
+                         d.get("shared"))
+        torch.cuda.synchronize()
+        return y.cpu().numpy()
+
+    base = run()
+    assert np.isfinite(base).all()
     assert_y_close(base, oracle.layer_inputs(inp), cfg.dtype, f"{name}/default order")
     for order, window in [(0, None), (1, None), (2, "1"), (2, "5"), (2, "12"), (2, "64")]:
         say(f"work order {order} window {window} on {name}")
@@ -277,7 +293,7 @@ def test_large_tile_work_orders_bit_identical(name, monkeypatch):
         monkeypatch.setenv("PCM_GEMM_ORDER_DOWN", str(order))
         if window is not None:
             monkeypatch.setenv("PCM_GEMM_EM_WINDOW", window)
-        y = run_layer(d, cfg.k)
+        y = run()
         assert np.array_equal(y, base), f"{name}: order {order} window {window} changed the output"
 
 
