@@ -192,11 +192,12 @@ def ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args):
 
     def per_path(reuse):
         def fn():
+            if shared:
+                pcm.pcm_dense_swiglu(x, *shared, y=y, accumulate=False, ws=plan.ws_shared)
             pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
             pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
-            pcm.pcm_layer_per_path(x, wg, wu, wd, plan.paths, reuse=reuse, y=y, ws=ws)
-            if shared:
-                pcm.pcm_dense_swiglu(x, *shared, y=y, accumulate=True, ws=plan.ws_shared)
+            pcm.pcm_layer_per_path(x, wg, wu, wd, plan.paths, reuse=reuse, y=y,
+                                   accumulate=bool(shared), ws=ws)
         return fn
 
     eye = torch.eye(cfg.n, dtype=torch.uint8, device=x.device)
@@ -257,36 +258,43 @@ def main():
         g_tgt = torch.from_numpy(sinp.g_tgt).to(dev)
         plan = pcm.ScoredLayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
         plan.build_layout(mask, torch.from_numpy(sinp.bias).to(dev))   # once per layer
-        stages = ["route", "expand", "project_combine"] + (["shared"] if shared else [])
+        stages = (["shared"] if shared else []) + ["route", "expand", "project_combine"]
     else:
         plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
-        stages = ["route", "build_paths", "expand", "project_combine"] + (["shared"] if shared else [])
+        stages = (["shared"] if shared else []) + ["route", "build_paths", "expand", "project_combine"]
 
     def step(events=None):
-        def mark(i):
+        # the stages in the order LayerPlan.forward runs them: the shared expert (if any)
+        # stores y first, and the combine adds the routed sum to it
+        marks = iter(range(len(stages) + 1))
+
+        def mark():
+            i = next(marks)
             if events is not None:
                 events[i].record(stream)
-        mark(0)
+        mark()
+        if shared:
+            pcm.pcm_dense_swiglu(x, *shared, y=plan.y, accumulate=False, ws=plan.ws_shared)
+            mark()
         if scored:
             pcm.pcm_route_scored(logits, g_tgt, sinp.lam, plan.layout, cfg.k, out=plan.paths,
                                  ws=plan.ws_route)
-            mark(1)
+            mark()
             pcm.pcm_expand_scored(x, wg, wu, plan.paths, u=plan.u)
-            mark(2)
-            pcm.pcm_project_combine_scored(plan.u, wd, plan.paths, y=plan.y, ws=plan.ws_proj)
-            mark(3)
+            mark()
+            pcm.pcm_project_combine_scored(plan.u, wd, plan.paths, y=plan.y, accumulate=bool(shared),
+                                           ws=plan.ws_proj)
+            mark()
         else:
             pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
-            mark(1)
+            mark()
             pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
-            mark(2)
+            mark()
             pcm.pcm_expand(x, wg, wu, plan.paths, u=plan.u)
-            mark(3)
-            pcm.pcm_project_combine(plan.u, wd, plan.paths, y=plan.y, ws=plan.ws_proj)
-            mark(4)
-        if shared:
-            pcm.pcm_dense_swiglu(x, *shared, y=plan.y, accumulate=True, ws=plan.ws_shared)
-            mark(len(stages))
+            mark()
+            pcm.pcm_project_combine(plan.u, wd, plan.paths, y=plan.y, accumulate=bool(shared),
+                                    ws=plan.ws_proj)
+            mark()
 
     for _ in range(args.warmup):
         step()

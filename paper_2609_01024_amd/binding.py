@@ -399,12 +399,15 @@ class ScoredLayerPlan:
         pcm_path_layout_build(mask, bias, out=self.layout, stream=stream)
 
     def forward(self, x, g_base, g_tgt, lam, w_gate, w_up, w_down, shared=None, stream=None):
+        # the shared expert first, storing y; the combine then adds the routed sum to it
+        # (y_t = shared_t + routed_t either way, the same two float32 operands)
+        if shared is not None:
+            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=False, ws=self.ws_shared, stream=stream)
         pcm_route_scored(g_base, g_tgt, lam, self.layout, self.K, out=self.paths, ws=self.ws_route,
                          stream=stream)
         pcm_expand_scored(x, w_gate, w_up, self.paths, u=self.u, stream=stream)
-        pcm_project_combine_scored(self.u, w_down, self.paths, y=self.y, ws=self.ws_proj, stream=stream)
-        if shared is not None:
-            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=True, ws=self.ws_shared, stream=stream)
+        pcm_project_combine_scored(self.u, w_down, self.paths, y=self.y, accumulate=shared is not None,
+                                   ws=self.ws_proj, stream=stream)
         return self.y
 
 
@@ -428,13 +431,17 @@ class LayerPlan:
         self.y = torch.empty((T, H), dtype=torch.float32, device=device)
 
     def forward(self, x, logits, mask, w_gate, w_up, w_down, shared=None, stream=None):
+        # the shared expert first, storing y (its projection's epilogue then has no y to read);
+        # the combine adds the routed sum: y_t = shared_t + routed_t, the same two float32
+        # operands as accumulating the shared expert last
+        if shared is not None:
+            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=False, ws=self.ws_shared, stream=stream)
         pcm_route(logits, self.k, self.ids, self.w, stream=stream)
         pcm_build_paths(self.ids, self.w, mask, self.beta_mode, out=self.paths, ws=self.ws_paths,
                         stream=stream)
         pcm_expand(x, w_gate, w_up, self.paths, u=self.u, stream=stream)
-        pcm_project_combine(self.u, w_down, self.paths, y=self.y, ws=self.ws_proj, stream=stream)
-        if shared is not None:
-            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=True, ws=self.ws_shared, stream=stream)
+        pcm_project_combine(self.u, w_down, self.paths, y=self.y, accumulate=shared is not None,
+                            ws=self.ws_proj, stream=stream)
         return self.y
 
 
