@@ -250,40 +250,41 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
                                                       int accumulate) {
     const int64_t t = blockIdx.x;
     const TokenPaths p = token_paths(m, t);
-    for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
-        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (ksplit <= 2) {
-            // every row's loads issued before the first add; the adds keep the order below
-            float4 v[kMaxK][2];
+    constexpr int CU = 2;   // column chunks per thread, loads of all issued first
+    for (int c0 = threadIdx.x * 4; c0 < H; c0 += blockDim.x * 4 * CU) {
+        float4 v[CU][kMaxK][2];
+#pragma unroll
+        for (int u = 0; u < CU; ++u) {
+            const int c = c0 + u * blockDim.x * 4;
 #pragma unroll
             for (int b = 0; b < kMaxK; ++b)
 #pragma unroll
                 for (int q = 0; q < 2; ++q)
-                    if (b < p.nt && q < ksplit)
-                        v[b][q] = *(const float4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c);
+                    if (c < H && b < p.nt && q < ksplit)
+                        {
+                        const floatx4 w = __builtin_nontemporal_load((const floatx4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c));
+                        v[u][b][q] = make_float4(w[0], w[1], w[2], w[3]);
+                    }
+        }
+#pragma unroll
+        for (int u = 0; u < CU; ++u) {
+            const int c = c0 + u * blockDim.x * 4;
+            if (c >= H) continue;
+            float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
             for (int b = 0; b < kMaxK; ++b)
 #pragma unroll
                 for (int q = 0; q < 2; ++q)
                     if (b < p.nt && q < ksplit) {
-                        s.x += v[b][q].x; s.y += v[b][q].y; s.z += v[b][q].z; s.w += v[b][q].w;
+                        s.x += v[u][b][q].x; s.y += v[u][b][q].y; s.z += v[u][b][q].z; s.w += v[u][b][q].w;
                     }
-        } else {
-#pragma unroll
-            for (int b = 0; b < kMaxK; ++b) {
-                if (b >= p.nt) break;
-                for (int q = 0; q < ksplit; ++q) {  // K slices of the projection, in order
-                    const float4 v = *(const float4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c);
-                    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-                }
+            float4* dst = (float4*)(y + t * H + c);
+            if (accumulate) {
+                const float4 old = *dst;
+                s.x = old.x + s.x; s.y = old.y + s.y; s.z = old.z + s.z; s.w = old.w + s.w;
             }
+            *dst = s;
         }
-        float4* dst = (float4*)(y + t * H + c);
-        if (accumulate) {
-            const float4 old = *dst;
-            s.x = old.x + s.x; s.y = old.y + s.y; s.z = old.z + s.z; s.w = old.w + s.w;
-        }
-        *dst = s;
     }
 }
 
