@@ -245,45 +245,69 @@ void launch_mix_regs(unsigned blocks, int threads, const float* u, void* z, floa
     mix_regs_kernel<KK, ITER><<<blocks, threads, 0, s>>>(u, (uint16_t*)z, zscale, m, F);
 }
 
+// y_t = [y_t] + sum over targets b (ascending) and K slices q (ascending) of o_(t,b) slice q.
+// One token per workgroup; each thread takes two 4-column chunks and issues the loads of
+// every row of both before the first add (up to two K slices: the projection splits K in at
+// most two). o is read once, so its loads are non-temporal.
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o, int ksplit,
                                                       MixMap m, int H, float* __restrict__ y,
                                                       int accumulate) {
     const int64_t t = blockIdx.x;
     const TokenPaths p = token_paths(m, t);
-    constexpr int CU = 2;   // column chunks per thread, loads of all issued first
+    constexpr int CU = 2;
     for (int c0 = threadIdx.x * 4; c0 < H; c0 += blockDim.x * 4 * CU) {
-        float4 v[CU][kMaxK][2];
+        float4 s[CU];
+        if (ksplit <= 2) {
+            float4 v[CU][kMaxK][2];
 #pragma unroll
-        for (int u = 0; u < CU; ++u) {
-            const int c = c0 + u * blockDim.x * 4;
+            for (int u = 0; u < CU; ++u) {
+                const int c = c0 + u * blockDim.x * 4;
 #pragma unroll
-            for (int b = 0; b < kMaxK; ++b)
+                for (int b = 0; b < kMaxK; ++b)
 #pragma unroll
-                for (int q = 0; q < 2; ++q)
-                    if (c < H && b < p.nt && q < ksplit)
-                        {
-                        const floatx4 w = __builtin_nontemporal_load((const floatx4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c));
-                        v[u][b][q] = make_float4(w[0], w[1], w[2], w[3]);
+                    for (int q = 0; q < 2; ++q)
+                        if (c < H && b < p.nt && q < ksplit) {
+                            const floatx4 w = __builtin_nontemporal_load(
+                                (const floatx4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c));
+                            v[u][b][q] = make_float4(w[0], w[1], w[2], w[3]);
+                        }
+            }
+#pragma unroll
+            for (int u = 0; u < CU; ++u) {
+                s[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                for (int b = 0; b < kMaxK; ++b)
+#pragma unroll
+                    for (int q = 0; q < 2; ++q)
+                        if (b < p.nt && q < ksplit) {
+                            s[u].x += v[u][b][q].x; s[u].y += v[u][b][q].y;
+                            s[u].z += v[u][b][q].z; s[u].w += v[u][b][q].w;
+                        }
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < CU; ++u) {
+                const int c = c0 + u * blockDim.x * 4;
+                s[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (c >= H) continue;
+                for (int b = 0; b < p.nt; ++b)
+                    for (int q = 0; q < ksplit; ++q) {
+                        const float4 w = *(const float4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c);
+                        s[u].x += w.x; s[u].y += w.y; s[u].z += w.z; s[u].w += w.w;
                     }
+            }
         }
 #pragma unroll
         for (int u = 0; u < CU; ++u) {
             const int c = c0 + u * blockDim.x * 4;
             if (c >= H) continue;
-            float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-            for (int b = 0; b < kMaxK; ++b)
-#pragma unroll
-                for (int q = 0; q < 2; ++q)
-                    if (b < p.nt && q < ksplit) {
-                        s.x += v[u][b][q].x; s.y += v[u][b][q].y; s.z += v[u][b][q].z; s.w += v[u][b][q].w;
-                    }
+            float4 r = s[u];
             float4* dst = (float4*)(y + t * H + c);
             if (accumulate) {
                 const float4 old = *dst;
-                s.x = old.x + s.x; s.y = old.y + s.y; s.z = old.z + s.z; s.w = old.w + s.w;
+                r.x = old.x + r.x; r.y = old.y + r.y; r.z = old.z + r.z; r.w = old.w + r.w;
             }
-            *dst = s;
+            *dst = r;
         }
     }
 }
