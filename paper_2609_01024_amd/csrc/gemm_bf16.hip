@@ -494,7 +494,7 @@ template <int BM, int TBM>
 __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
     if (threadIdx.x < 64) {
         const int lane = threadIdx.x;
-        int lo[4], full[4], nl[4], ns[4], suml = 0, sums = 0;
+        int lo[4], hi[4], full[4], nl[4], ns[4], suml = 0, sums = 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int x = lane * 4 + j;
@@ -507,6 +507,7 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
             }
             const int rem = c % BM;
             lo[j] = b;
+            hi[j] = b + c;
             full[j] = c / BM;
             nl[j] = full[j] + (rem > TBM ? 1 : 0);
             ns[j] = (rem > 0 && rem <= TBM) ? 1 : 0;
@@ -519,13 +520,14 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
             const int vl = __shfl_up(incl, d), vs = __shfl_up(incs, d);
             if (lane >= d) { incl += vl; incs += vs; }
         }
-        const int64_t Lt = __shfl(incl, 63), St = __shfl(incs, 63);
-        const int64_t LT = Lt * nt * g.ksplit, ST = St * nt * g.ksplit;
-        const int64_t x8 = blockIdx.x % 8, j8 = blockIdx.x / 8;
-        const int64_t l0 = x8 * LT / 8, l1 = (x8 + 1) * LT / 8;
-        const int64_t s0 = x8 * ST / 8, s1 = (x8 + 1) * ST / 8;
+        // 32-bit arithmetic throughout: the host keeps item counts (times 8) within range
+        const int Lt = __shfl(incl, 63), St = __shfl(incs, 63);
+        const int LT = Lt * nt * g.ksplit, ST = St * nt * g.ksplit;
+        const int x8 = (int)(blockIdx.x % 8), j8 = (int)(blockIdx.x / 8);
+        const int l0 = x8 * LT / 8, l1 = (x8 + 1) * LT / 8;
+        const int s0 = x8 * ST / 8, s1 = (x8 + 1) * ST / 8;
         bool valid = true, is_long = true;
-        int64_t item = 0, count = Lt;
+        int item = 0, count = Lt;
         if (j8 < l1 - l0) {
             item = l0 + j8;
         } else if (j8 - (l1 - l0) < s1 - s0) {
@@ -537,22 +539,25 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
         }
         if (lane == 0) s_item[5] = valid ? 1 : 0;
         if (valid) {
-            const int64_t per_slice = count * nt;
-            const int kslice = (int)(item / per_slice);
-            int64_t m;
-            int ntile;
-            tile_from_id(item % per_slice, count, nt, GN, &m, &ntile);
+            const int per_slice = count * nt;
+            const int kslice = item / per_slice;
+            // grouped order within the list (as tile_from_id)
+            const int id = item - kslice * per_slice;
+            const int gsize = GN * count;
+            const int grp = id / gsize, in = id - grp * gsize;
+            const int gn = min(GN, nt - grp * GN);
+            const int m = in / gn;
+            const int ntile = grp * GN + (in - m * gn);
             // group holding list entry m: this lane's groups start at the exclusive prefix
             int start = is_long ? incl - suml : incs - sums;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int cnt = is_long ? nl[j] : ns[j];
                 if (m >= start && m < start + cnt) {
-                    const int r0 = lo[j] + (is_long ? (int)(m - start) * BM : full[j] * BM);
-                    const int end = g.offsets == nullptr ? (int)g.a_rows : g.offsets[lane * 4 + j + 1];
+                    const int r0 = lo[j] + (is_long ? (m - start) * BM : full[j] * BM);
                     s_item[0] = lane * 4 + j;
                     s_item[1] = r0;
-                    s_item[2] = min(end, r0 + BM);
+                    s_item[2] = min(hi[j], r0 + BM);
                     s_item[3] = ntile;
                     s_item[4] = kslice;
                 }
@@ -588,7 +593,7 @@ __device__ bool em_item(const GemmArgs& g, int nt, int window, int* s_item) {
             }
             lo[j] = b;
             cnt[j] = c;
-            m[j] = (int)ceil_div(c, BM);
+            m[j] = (c + BM - 1) / BM;
             local += m[j] * nt;
         }
         int incl = local;
@@ -597,32 +602,33 @@ __device__ bool em_item(const GemmArgs& g, int nt, int window, int* s_item) {
             const int v = __shfl_up(incl, d);
             if (lane >= d) incl += v;
         }
-        const int64_t Tt = __shfl(incl, 63), TT = Tt * g.ksplit;
-        const int64_t x8 = blockIdx.x % 8, j8 = blockIdx.x / 8;
-        const int64_t l0 = x8 * TT / 8, l1 = (x8 + 1) * TT / 8;
+        // 32-bit arithmetic throughout: the host keeps item counts (times 8) within range
+        const int Tt = __shfl(incl, 63), TT = Tt * g.ksplit;
+        const int x8 = (int)(blockIdx.x % 8), j8 = (int)(blockIdx.x / 8);
+        const int l0 = x8 * TT / 8, l1 = (x8 + 1) * TT / 8;
         const bool valid = j8 < l1 - l0;
         if (lane == 0) s_item[5] = valid ? 1 : 0;
         if (valid) {
-            const int64_t item = l0 + j8;
-            const int kslice = (int)(item / Tt);
-            const int64_t id = item % Tt;
-            int64_t start = incl - local;
+            const int item = l0 + j8;
+            const int kslice = item / Tt;
+            const int id = item - kslice * Tt;
+            int start = incl - local;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int64_t items = (int64_t)m[j] * nt;
+                const int items = m[j] * nt;
                 if (id >= start && id < start + items) {
-                    const int64_t l = id - start;
+                    const int l = id - start;
                     int gn = window / m[j];
                     gn = gn < 1 ? 1 : (gn > nt ? nt : gn);
-                    const int64_t gsize = (int64_t)gn * m[j];
-                    const int64_t grp = l / gsize, in = l % gsize;
-                    const int gcols = (int)min<int64_t>(gn, nt - grp * gn);
-                    const int mm = (int)(in / gcols);
+                    const int gsize = gn * m[j];
+                    const int grp = l / gsize, in = l - grp * gsize;
+                    const int gcols = min(gn, nt - grp * gn);
+                    const int mm = in / gcols;
                     const int r0 = lo[j] + mm * BM;
                     s_item[0] = lane * 4 + j;
                     s_item[1] = r0;
                     s_item[2] = min(lo[j] + cnt[j], r0 + BM);
-                    s_item[3] = (int)(grp * gn + in % gcols);
+                    s_item[3] = grp * gn + (in - mm * gcols);
                     s_item[4] = kslice;
                 }
                 start += items;
@@ -941,6 +947,8 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
             if (g.offsets == nullptr) order = MODE == kExpand ? kGrouped : kLongestFirst;
             else order = (MODE != kExpand && g.ksplit > 1) ? kLongestFirst : kExpertMajor;
         }
+        // the searches of il_item and em_item run in 32-bit integers (item counts times 8)
+        if (mt_upper * nt * g.ksplit >= (int64_t(1) << 27)) order = kGrouped;
         int64_t grid;
         int gparam = group_n;
         if (order == kLongestFirst) {
