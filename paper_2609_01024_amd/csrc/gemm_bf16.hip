@@ -521,8 +521,9 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
             if (lane >= d) { incl += vl; incs += vs; }
         }
         // 32-bit arithmetic throughout: the host keeps item counts (times 8) within range
+        // the short list in halves: 2 * nt N-tiles of half width
         const int Lt = __shfl(incl, 63), St = __shfl(incs, 63);
-        const int LT = Lt * nt * g.ksplit, ST = St * nt * g.ksplit;
+        const int LT = Lt * nt * g.ksplit, ST = St * 2 * nt * g.ksplit;
         const int x8 = (int)(blockIdx.x % 8), j8 = (int)(blockIdx.x / 8);
         const int l0 = x8 * LT / 8, l1 = (x8 + 1) * LT / 8;
         const int s0 = x8 * ST / 8, s1 = (x8 + 1) * ST / 8;
@@ -537,17 +538,21 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
         } else {
             valid = false;
         }
-        if (lane == 0) s_item[5] = valid ? 1 : 0;
+        if (lane == 0) {
+            s_item[5] = valid ? 1 : 0;
+            s_item[6] = is_long ? 0 : 1;
+        }
         if (valid) {
-            const int per_slice = count * nt;
+            const int ntl = is_long ? nt : 2 * nt, gnl = is_long ? GN : 2 * GN;
+            const int per_slice = count * ntl;
             const int kslice = item / per_slice;
             // grouped order within the list (as tile_from_id)
             const int id = item - kslice * per_slice;
-            const int gsize = GN * count;
+            const int gsize = gnl * count;
             const int grp = id / gsize, in = id - grp * gsize;
-            const int gn = min(GN, nt - grp * GN);
+            const int gn = min(gnl, ntl - grp * gnl);
             const int m = in / gn;
-            const int ntile = grp * GN + (in - m * gn);
+            const int ntile = grp * gnl + (in - m * gn);
             // group holding list entry m: this lane's groups start at the exclusive prefix
             int start = is_long ? incl - suml : incs - sums;
 #pragma unroll
@@ -647,14 +652,22 @@ enum IlOrder { kGrouped = 0, kLongestFirst = 1, kExpertMajor = 2 };
 template <class C, class CT, int MODE>
 __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_upper, int nt,
                                                          int group_n, int order) {
+    // half of a tail tile (128 x 128 for the large tiles, each wave 64 x 64): the longest-first
+    // order runs each tail item as two of these, so that shorter items fill the last round
+    using CH = ICfg<CT::BM, C::BNB / 2, CT::WM, CT::WN>;
     static_assert(CT::NT == C::NT && CT::BNB == C::BNB && CT::BM <= C::BM && CT::WTN == C::WTN,
                   "the tail tile runs on the same workgroup and N tiling");
+    static_assert(CH::NT == C::NT && CH::LDS_BYTES <= C::LDS_BYTES, "the half tail tile fits");
     extern __shared__ __attribute__((aligned(1024))) char lds[];
-    __shared__ int s_item[6];
+    __shared__ int s_item[7];
     int e, row0, row1, ntile, kslice;
     if (order == kLongestFirst) {          // workgroup-uniform branches and returns
         if (!il_item<C::BM, CT::BM>(g, nt, group_n, s_item)) return;
         e = s_item[0], row0 = s_item[1], row1 = s_item[2], ntile = s_item[3], kslice = s_item[4];
+        if (s_item[6]) {                   // half of a tail item: N-tile of half width
+            il_tile<CH, MODE>(g, lds, e, row0, row1, ntile, kslice);
+            return;
+        }
     } else if (order == kExpertMajor) {
         if (!em_item<C::BM>(g, nt, group_n, s_item)) return;
         e = s_item[0], row0 = s_item[1], row1 = s_item[2], ntile = s_item[3], kslice = s_item[4];
@@ -948,12 +961,14 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
             else order = (MODE != kExpand && g.ksplit > 1) ? kLongestFirst : kExpertMajor;
         }
         // the searches of il_item and em_item run in 32-bit integers (item counts times 8)
-        if (mt_upper * nt * g.ksplit >= (int64_t(1) << 27)) order = kGrouped;
+        if ((mt_upper + g.n + 1) * nt * g.ksplit >= (int64_t(1) << 27)) order = kGrouped;
         int64_t grid;
         int gparam = group_n;
         if (order == kLongestFirst) {
-            // each XCD's run holds at most ceil(long / 8) + ceil(short / 8) items
-            grid = (ceil_div(mt_upper * nt * g.ksplit, 8) + 2) * 8;
+            // each XCD's run holds at most ceil(long / 8) + ceil(2 * short / 8) items, where
+            // long + short <= mt_upper * nt * ksplit and short <= groups * nt * ksplit
+            const int64_t groups = g.offsets ? g.n : 1;
+            grid = (ceil_div((mt_upper + groups) * nt * g.ksplit, 8) + 2) * 8;
         } else if (order == kExpertMajor) {
             // each XCD's run holds at most ceil(items / 8) <= ceil(mt_upper * nt * ksplit / 8)
             const char* win_s = getenv("PCM_GEMM_EM_WINDOW");
