@@ -198,11 +198,26 @@ template <int MODE, int MB, int NBK, int WTM, int WTN, int OUT_COLS>
 __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB], int row0,
                                 int row1, int ntile, int wm, int wn, int lane) {
     const int N = g.N;
+    // The row scales of all of this lane's rows are loaded first, without branches, and
+    // waited for once, in code that every store follows. A scale load that is still in
+    // flight where the stores' branches (row and column bounds) merge makes the compiler
+    // wait for all outstanding memory operations before each store, the earlier stores
+    // included: the 64 stores of a wave then ran one after another (13 us of a 256 x 256
+    // projection tile).
+    float scs[MB];
+    if constexpr (MODE != kExpand) {
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-        const int r = row0 + wm * WTM + mb * 16 + (lane & 15);
-        if (r >= row1) continue;
-        if (MODE == kExpand) {
+        for (int mb = 0; mb < MB; ++mb) {
+            const int r = min(row0 + wm * WTM + mb * 16 + (lane & 15), row1 - 1);
+            scs[mb] = g.row_scale ? g.row_scale[scale_row(g, r)] : 1.0f;
+        }
+        __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, kNoLgkm));
+    }
+    if constexpr (MODE == kExpand) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const int r = row0 + wm * WTM + mb * 16 + (lane & 15);
+            if (r >= row1) continue;
 #pragma unroll
             for (int nb = 0; nb < NBK / 2; ++nb) {
                 const int f = ntile * OUT_COLS + wn * (WTN / 2) + nb * 16 + (lane >> 4) * 4;
@@ -213,21 +228,45 @@ __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB]
                 for (int i = 0; i < 4; ++i) v[i] = silu(gt[i]) * up[i];
                 *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
             }
-        } else {
-            float* O = (float*)g.out;
-            const float sc = g.row_scale ? g.row_scale[scale_row(g, r)] : 1.0f;
+        }
+    } else if (MODE == kDownAccum && g.accumulate) {
+        // read-modify-write: each row block's values are loaded before its stores
+        float* O = (float*)g.out;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const int r = row0 + wm * WTM + mb * 16 + (lane & 15);
+            if (r >= row1) continue;
+            float4 prev[NBK];
+#pragma unroll
+            for (int nb = 0; nb < NBK; ++nb) {
+                const int h = min(ntile * OUT_COLS + wn * WTN + nb * 16 + (lane >> 4) * 4, N - 4);
+                prev[nb] = *(const float4*)(O + (int64_t)r * N + h);
+            }
+            const float sc = scs[mb];
 #pragma unroll
             for (int nb = 0; nb < NBK; ++nb) {
                 const int h = ntile * OUT_COLS + wn * WTN + nb * 16 + (lane >> 4) * 4;
                 if (h >= N) continue;
-                float4 v = make_float4(acc[nb][mb][0] * sc, acc[nb][mb][1] * sc, acc[nb][mb][2] * sc,
-                                       acc[nb][mb][3] * sc);
-                float4* dst = (float4*)(O + (int64_t)r * N + h);
-                if (MODE == kDownAccum && g.accumulate) {
-                    const float4 o = *dst;
-                    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
-                }
-                *dst = v;
+                // the stored value plus the scaled product, each rounded (no fused multiply-add),
+                // so that accumulating adds exactly what the store path writes
+                *(float4*)(O + (int64_t)r * N + h) = make_float4(
+                    __fadd_rn(prev[nb].x, __fmul_rn(acc[nb][mb][0], sc)), __fadd_rn(prev[nb].y, __fmul_rn(acc[nb][mb][1], sc)),
+                    __fadd_rn(prev[nb].z, __fmul_rn(acc[nb][mb][2], sc)), __fadd_rn(prev[nb].w, __fmul_rn(acc[nb][mb][3], sc)));
+            }
+        }
+    } else {
+        float* O = (float*)g.out;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const int r = row0 + wm * WTM + mb * 16 + (lane & 15);
+            if (r >= row1) continue;
+            const float sc = scs[mb];
+#pragma unroll
+            for (int nb = 0; nb < NBK; ++nb) {
+                const int h = ntile * OUT_COLS + wn * WTN + nb * 16 + (lane >> 4) * 4;
+                if (h >= N) continue;
+                *(float4*)(O + (int64_t)r * N + h) = make_float4(acc[nb][mb][0] * sc, acc[nb][mb][1] * sc,
+                                                                 acc[nb][mb][2] * sc, acc[nb][mb][3] * sc);
             }
         }
     }
@@ -358,13 +397,25 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
     const __amdgpu_buffer_rsrc_t rb1 =
         MODE == kExpand ? buffer_rsrc((const char*)g.b1 + e * wbytes, (uint32_t)wbytes) : rb0;
     bool up[C::LPW];
+    // source rows of this lane's A loads: with a gather, every index is loaded before any is
+    // used (one wait instead of one per load)
+    int srows[C::QA];
+#pragma unroll
+    for (int q = 0; q < C::QA; ++q) srows[q] = min(row0 + (q * C::NW + wave) * 8 + lrow, row1 - 1);
+    if (g.gather) {
+#pragma unroll
+        for (int q = 0; q < C::QA; ++q) srows[q] = g.gather[srows[q]];
+#pragma unroll
+        for (int q = 0; q < C::QA; ++q)
+            srows[q] = srows[q] < 0 ? 0 : (srows[q] >= g.a_rows ? (int)(g.a_rows - 1) : srows[q]);
+    }
 #pragma unroll
     for (int q = 0; q < C::LPW; ++q) {
         up[q] = false;
         if (q < C::QA) {
             const int blk = q * C::NW + wave, lr = blk * 8 + lrow;
             const int chunk = (lane & 7) ^ ((lr >> 1) & 7);
-            const int64_t srow = a_source_row(g, row0 + lr, row1);
+            const int64_t srow = srows[q];
             voff[q] = (uint32_t)(srow * (int64_t)g.K * 2 + k_byte0 + chunk * 16);
             dst[q] = blk * 1024;
         } else {
