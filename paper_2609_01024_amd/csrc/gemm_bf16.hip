@@ -953,6 +953,183 @@ __global__ __launch_bounds__(SWAVES * 64) void gemm_stream_kernel(GemmArgs g, in
     }
 }
 
+// LDS-ring streaming kernel: the streaming kernel with its operands staged through a per-wave
+// LDS ring. A weight load of the register-ring kernel covers 16 rows x 64 bytes (the MFMA operand
+// layout puts four lanes on a row), half a cache line per row, and the weight stream then ran
+// at 5.4 TB/s; here each direct buffer -> LDS load covers 8 rows x 128 bytes (the 64 K values
+// of two MFMA steps, whole lines) and the MFMA fragments are read back from LDS. Ring slot j of
+// a wave holds NB blocks of 16 weight rows and one block of the 16 activation rows, each row
+// 128 bytes with chunk c of row r at position c ^ ((r >> 1) & 7) (conflict-free fragment
+// reads); D slots, D - 1 pairs in flight. No barrier: each wave owns its ring, and a slot is
+// reloaded only after the MFMAs that used its fragments. With the activations in the ring as
+// well, the loop holds no load into registers, whose waits the compiler would place itself
+// (it drained every load in flight at the loop head). K is a multiple of 64 (as the layer
+// entry points require of H and F), and `a` and one group's weights are below 4 GiB (32-bit
+// buffer offsets); otherwise the register-ring kernel runs.
+// (The body is a device function: the buffer resources and LDS-destination loads it uses have
+// no host form, and the host pass does not emit a kernel whose own body uses them.)
+template <int MODE, int NB, int D>
+__device__ __forceinline__ void lstream_tile(const GemmArgs& g, char* lds, int e, int row0, int row1,
+                                             int ntile) {
+    static_assert(NB % 2 == 0 && D >= 2 && (D - 1) * (2 * NB + 2) <= 63, "gate/up halves; vmcnt range");
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int K = g.K, N = g.N;
+    constexpr int kWaveCols = (MODE == kExpand) ? NB * 8 : NB * 16;
+    const int col0 = (ntile * SWAVES + wave) * kWaveCols;
+    if (col0 >= N) return;  // wave-uniform; no barrier follows
+    constexpr int kSlot = (NB + 1) * 2048;   // NB weight blocks, then the activation block
+    char* ring = lds + wave * (D * kSlot);
+    // weight row (within expert e) behind row R of block b; rows past N repeat row N - 1
+    auto wrow = [&](int b, int R) {
+        const int wr = (MODE == kExpand) ? col0 + (b % (NB / 2)) * 16 + R : col0 + b * 16 + R;
+        return wr < N ? wr : N - 1;
+    };
+    const int64_t wbytes = (int64_t)N * K * 2;
+    const __amdgpu_buffer_rsrc_t rb0 = buffer_rsrc((const char*)g.b0 + e * wbytes, (uint32_t)wbytes);
+    const __amdgpu_buffer_rsrc_t rb1 =
+        MODE == kExpand ? buffer_rsrc((const char*)g.b1 + e * wbytes, (uint32_t)wbytes) : rb0;
+    // load (b, h) of a pair: rows h * 8 + lane / 8 of block b, position lane % 8
+    uint32_t voff[NB][2];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int R = h * 8 + (lane >> 3);
+            const int chunk = (lane & 7) ^ ((R >> 1) & 7);
+            voff[b][h] = (uint32_t)(wrow(b, R) * (int64_t)K * 2 + chunk * 16);
+        }
+    // activation loads (h = 0, 1): rows h * 8 + lane / 8, position lane % 8
+    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(g.a, (uint32_t)((int64_t)g.a_rows * K * 2));
+    uint32_t aoff[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int R = h * 8 + (lane >> 3);
+        const int chunk = (lane & 7) ^ ((R >> 1) & 7);
+        aoff[h] = (uint32_t)(a_source_row(g, row0 + R, row1) * (int64_t)K * 2 + chunk * 16);
+    }
+    const int r16 = lane & 15, kg = lane >> 4;
+    // the projection's row scale, loaded and waited for before the loop (a load into a
+    // register still in flight across the loop makes the compiler wait for every load in it)
+    float sc = 1.0f;
+    if constexpr (MODE != kExpand) {
+        if (g.row_scale) sc = g.row_scale[scale_row(g, min(row0 + r16, row1 - 1))];
+        __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, kNoLgkm));
+    }
+    // fragment of row r16, chunk 4 * step + kg
+    const int fo0 = r16 * 128 + ((kg ^ ((r16 >> 1) & 7)) * 16);
+    const int fo1 = r16 * 128 + (((4 + kg) ^ ((r16 >> 1) & 7)) * 16);
+
+    floatx4 acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int KP = K / 64;
+    auto issue = [&](int j, int p) {
+        char* slot = ring + j * kSlot;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds((MODE == kExpand && b >= NB / 2) ? rb1 : rb0,
+                                                         (PCM_LDS void*)(slot + b * 2048 + h * 1024), 16,
+                                                         voff[b][h], p * 128, 0, 0);
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (PCM_LDS void*)(slot + NB * 2048 + h * 1024), 16,
+                                                     aoff[h], p * 128, 0, 0);
+    };
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j)
+        if (j < KP) issue(j, j);
+    for (int base = 0; base < KP; base += D) {
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const int p = base + j;
+            if (p >= KP) break;
+            // slot (j + D - 1) % D held pair p - 1, whose fragments the previous MFMAs used
+            if (p + D - 1 < KP) issue((j + D - 1) % D, p + D - 1);
+            // pair p has landed: only the pairs issued after it may still be in flight
+            if (p + D - 1 < KP) __builtin_amdgcn_s_waitcnt(waitcnt_imm((D - 1) * (2 * NB + 2), kNoLgkm));
+            else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, kNoLgkm));
+            const char* slot = ring + j * kSlot;
+#pragma unroll
+            for (int st = 0; st < 2; ++st) {
+                const int fo = st ? fo1 : fo0;
+                const bf16x8 av = *(const bf16x8*)(slot + NB * 2048 + fo);
+                if constexpr (MODE == kExpand) {
+#pragma unroll
+                    for (int b = 0; b < NB; ++b)
+                        acc[b] = mfma_step(*(const bf16x8*)(slot + b * 2048 + fo), av, acc[b]);
+                } else {
+                    const halfx8 a16 = __builtin_bit_cast(halfx8, av);
+#pragma unroll
+                    for (int b = 0; b < NB; ++b)
+                        acc[b] = mfma_step(widen_to_f16(*(const bf16x8*)(slot + b * 2048 + fo)), a16, acc[b]);
+                }
+            }
+        }
+    }
+    // epilogue: lane holds output columns c..c+3 (c = 4 * (lane >> 4)) of activation row r16
+    // in each block
+    const int r = row0 + r16;
+    if (r >= row1) return;
+    if (MODE == kExpand) {
+#pragma unroll
+        for (int b = 0; b < NB / 2; ++b) {
+            const int f = col0 + b * 16 + 4 * kg;
+            if (f >= N) continue;
+            float v[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = silu(acc[b][i]) * acc[b + NB / 2][i];
+            *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
+        }
+    } else {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int h = col0 + b * 16 + 4 * kg;
+            if (h >= N) continue;
+            float4 v = make_float4(acc[b][0] * sc, acc[b][1] * sc, acc[b][2] * sc, acc[b][3] * sc);
+            float4* dst = (float4*)((float*)g.out + (int64_t)r * N + h);
+            if (MODE == kDownAccum && g.accumulate) {
+                const float4 o = *dst;
+                v.x = __fadd_rn(o.x, v.x); v.y = __fadd_rn(o.y, v.y);
+                v.z = __fadd_rn(o.z, v.z); v.w = __fadd_rn(o.w, v.w);
+            }
+            *dst = v;
+        }
+    }
+}
+
+template <int MODE, int NB, int D>
+__global__ __launch_bounds__(SWAVES * 64) void gemm_lstream_kernel(GemmArgs g, int64_t mt_upper,
+                                                                  int nt, int n_fastest) {
+    extern __shared__ __attribute__((aligned(1024))) char lds[];
+    __shared__ int s_tile[3];
+    const int64_t mt = n_fastest ? blockIdx.x / nt : blockIdx.x % mt_upper;
+    const int ntile = n_fastest ? (int)(blockIdx.x % nt) : (int)(blockIdx.x / mt_upper);
+    if (!find_tile<SROWS>(g.offsets, g.n, g.a_rows, mt, s_tile)) return;
+    lstream_tile<MODE, NB, D>(g, lds, s_tile[0], s_tile[1], s_tile[2], ntile);
+}
+
+template <int MODE, int NB, int D>
+hipError_t launch_lstream_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
+    const int64_t mt_upper = g.offsets ? ceil_div(R, SROWS) + g.n : ceil_div(R, SROWS);
+    constexpr int kWgCols = SWAVES * ((MODE == kExpand) ? NB * 8 : NB * 16);
+    constexpr int kLds = SWAVES * D * (NB + 1) * 2048;
+    const int nt = (int)ceil_div(g.N, kWgCols);
+    const int64_t grid = mt_upper * nt;
+    if (grid <= 0) return hipSuccess;
+    static bool attr_set = false;  // idempotent; a race only repeats the same call
+    if (!attr_set) {
+        const hipError_t err = hipFuncSetAttribute((const void*)gemm_lstream_kernel<MODE, NB, D>,
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+        if (err != hipSuccess) return err;
+        attr_set = true;
+    }
+    const int n_fastest = MODE == kExpand ? 1 : 0;
+    gemm_lstream_kernel<MODE, NB, D><<<dim3((unsigned)grid), dim3(SWAVES * 64), kLds, s>>>(g, mt_upper, nt, n_fastest);
+    return hipGetLastError();
+}
+
 template <int MODE, int NB, int SDP>
 hipError_t launch_stream_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     const int64_t mt_upper = g.offsets ? ceil_div(R, SROWS) + g.n : ceil_div(R, SROWS);
@@ -968,10 +1145,23 @@ hipError_t launch_stream_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     return hipGetLastError();
 }
 
-// two 16-row blocks per wave, eight k-steps in flight (four or six blocks, or six steps,
-// measured 1-3% slower on the decode-shaped layer)
+// Register-ring kernel: two 16-row blocks per wave, eight k-steps in flight (four or six
+// blocks, or six steps, measured 1-3% slower on the decode-shaped layer).
 template <int MODE>
 hipError_t launch_stream(const GemmArgs& g, int64_t R, hipStream_t s) {
+    // the LDS-ring kernel (whole-line weight loads) where its constraints hold; ring depth 3
+    // for the expansion and 2 for the projection (decode-shaped layer: 2-6 within 0.5% for the
+    // expansion; the projection 3% slower at 3 and 45% at 4, where the compiler waits for every
+    // load in flight before the fragment reads and only one workgroup fits a compute unit);
+    // PCM_LSTREAM_D overrides the depth (0: the register-ring kernel), for tests and tuning
+    if (g.K % 64 == 0 && g.a_rows * g.K * 2 < (int64_t(1) << 32) && (int64_t)g.N * g.K * 2 < (int64_t(1) << 32)) {
+        const char* d = getenv("PCM_LSTREAM_D");
+        const int dv = d ? atoi(d) : (MODE == kExpand ? 3 : 2);
+        if (dv == 2) return launch_lstream_cfg<MODE, 2, 2>(g, R, s);
+        if (dv == 4) return launch_lstream_cfg<MODE, 2, 4>(g, R, s);
+        if (dv == 6) return launch_lstream_cfg<MODE, 2, 6>(g, R, s);
+        if (dv != 0) return launch_lstream_cfg<MODE, 2, 3>(g, R, s);
+    }
     return launch_stream_cfg<MODE, 2, 8>(g, R, s);
 }
 

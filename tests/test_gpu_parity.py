@@ -297,6 +297,40 @@ def test_large_tile_work_orders_bit_identical(name, monkeypatch):
         assert np.array_equal(y, base), f"{name}: order {order} window {window} changed the output"
 
 
+@pytest.mark.parametrize("name", ["decode_s", "olmoe_s", "fine_s"])
+def test_stream_kernels_bit_identical(name, monkeypatch):
+    """The streaming GEMMs of few-row groups: the LDS-ring kernel (whole-line weight loads) at
+    every ring depth and the register-ring kernel (depth 0; otherwise run only where buffer
+    offsets would pass 4 GiB) feed the same operands to the same MFMAs, so the layer output must
+    be the same bits under each, and within tolerance of the oracle."""
+    monkeypatch.setenv("PCM_GEMM_TILE", "S")
+    cfg = SMALL[name]
+    inp = make_inputs(cfg, seed=23)
+    d = dev(inp)
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, DEV, cfg.shared_F)
+
+    def run():
+        plan.u.fill_(float("nan"))
+        plan.y.fill_(float("nan"))
+        for ws in (plan.ws_proj, plan.ws_shared):
+            if ws is not None:
+                ws.fill_(0xFF)
+        y = plan.forward(d["x"], d["logits"], d["mask"], d["w_gate"], d["w_up"], d["w_down"],
+                         d.get("shared"))
+        torch.cuda.synchronize()
+        return y.cpu().numpy()
+
+    base = run()
+    assert np.isfinite(base).all()
+    assert_y_close(base, oracle.layer_inputs(inp), cfg.dtype, f"{name}/default stream kernel")
+    for depth in ["0", "2", "3", "4", "6"]:
+        say(f"stream kernel depth {depth} on {name}")
+        monkeypatch.setenv("PCM_LSTREAM_D", depth)
+        y = run()
+        assert np.array_equal(y, base), f"{name}: ring depth {depth} changed the output"
+
+
 def test_layer_is_deterministic():
     cfg = SMALL["olmoe_s"]
     d = dev(make_inputs(cfg, seed=7))
