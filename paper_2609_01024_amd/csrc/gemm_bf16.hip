@@ -17,11 +17,13 @@
 //  * "interleaved" (large tiles, 256 x 256): four waves, one per SIMD, each owning a 128 x 128
 //    block of C in 256 accumulation registers. Global -> LDS direct buffer loads
 //    (buffer_load_dwordx4 ... lds, no register staging: one 32-bit offset per lane for the
-//    whole tile, the stage's K offset in a scalar register) of 64-wide K stages,
-//    double-buffered, each load covering 8 whole 128-byte rows; one workgroup barrier per
-//    32-wide substep,
+//    whole tile, the stage's K offset in a scalar register) of 64-wide K stages, two stages
+//    of A and three of B (the weights, mostly fetched from HBM, get two stages of latency
+//    budget, the activations one), each load covering 8 whole 128-byte rows; one workgroup
+//    barrier per 32-wide substep,
 //    within which each wave issues its 64 MFMAs interleaved with the fragment reads of the
-//    next substep (and, once per stage, the loads of the stage after next). LDS rows are
+//    next substep (and, once per stage, the loads of A two stages and of B three stages
+//    ahead). LDS rows are
 //    128 bytes; the 16-byte chunk c of row r sits at position c ^ ((r >> 1) & 7), which
 //    keeps the fragment reads (16 rows x 4 chunks per instruction) free of bank conflicts.
 //    A group's last tile with at most 128 rows runs as a 128 x 256 tile (64 x 128 per wave)
@@ -306,22 +308,26 @@ __device__ inline floatx4 mfma_step(const halfx8& w, const halfx8& a, floatx4 c)
 
 // ---------------------------------------------------------- interleaved kernel
 // One wave per SIMD, each owning a 128 x 128 block of C (256 accumulator registers). K runs
-// in 64-wide stages, two of them in LDS (double buffering); a stage is two 32-wide MFMA
-// substeps, and every substep starts at a workgroup barrier. Between two barriers a wave
-// issues the 64 MFMAs of one substep from registers, interleaved with the LDS fragment
-// reads of the next substep (into the other register set); the first substep of a stage
-// also issues every global->LDS load of the stage after next (into the stage just freed).
+// in 64-wide stages; LDS holds two stages of A and three of B (160 KB for 256 x 256 tiles,
+// the whole of it: the kernel has no static LDS, and the work item is broadcast through the
+// first bytes of the first A stage before its loads are issued). A stage is two 32-wide
+// MFMA substeps, and every substep starts at a workgroup barrier. Between two barriers a
+// wave issues the 64 MFMAs of one substep from registers, interleaved with the LDS fragment
+// reads of the next substep (into the other register set); the first substep of stage kt
+// also issues the global->LDS loads of A for stage kt + 2 and of B for stage kt + 3 (into
+// the stage slots just freed). A third B stage (weights, mostly fetched from HBM) took the
+// Mixtral-shaped expansion from 1583 to 1527 us and its projection from 1162 to 1089 us.
 // A load covers 8 whole 128-byte rows, so each fetched cache line is used in full.
 template <int BM_, int BNB_, int WM_, int WN_>
 struct ICfg {
-    static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_, NS = 2;
+    static constexpr int BM = BM_, BNB = BNB_, WM = WM_, WN = WN_;
     static constexpr int NW = WM * WN, NT = NW * 64;
     static constexpr int WTM = BM / WM, WTN = BNB / WN, MB = WTM / 16, NBK = WTN / 16;
     static constexpr int A_ROWS = BM;
     static constexpr int A_INSTR = A_ROWS / 8, B_INSTR = BNB / 8;
     static constexpr int QA = A_INSTR / NW, QB = B_INSTR / NW, LPW = QA + QB;
-    static constexpr int STAGE = (A_ROWS + BNB) * 128;
-    static constexpr int LDS_BYTES = NS * STAGE;
+    static constexpr int SA = A_ROWS * 128, SB = BNB * 128;   // one stage of A, of B
+    static constexpr int LDS_BYTES = 2 * SA + 3 * SB;          // A: 2 stages, B: 3 stages
     // schedule of a substep: MFMA i is followed by fragment read i / R_EVERY (weights
     // first), load i / L_EVERY and, from slot W_FROM on, WPS dwords of weight widening
     static constexpr int NM = NBK * MB, NR = NBK + MB;
@@ -331,7 +337,7 @@ struct ICfg {
     static constexpr int WPS = (4 * NBK + (NM - W_FROM) - 1) / (NM - W_FROM);
     static_assert(A_INSTR % NW == 0 && B_INSTR % NW == 0, "every wave issues the same loads");
     static_assert(WTM % 16 == 0 && WTN % 32 == 0, "whole MFMA blocks, gate/up halves");
-    static_assert(LDS_BYTES <= 160 * 1024 - 1024, "LDS budget");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget (the kernel has no static LDS)");
     static_assert(LPW <= 63, "vmcnt range");
     static_assert(R_EVERY * (NR - 1) < NM && L_EVERY >= 1 && L_EVERY * (LPW - 1) + 1 < NM, "slots");
     static_assert(W_FROM < NM && (NM - W_FROM) * WPS >= 4 * NBK, "widen slots");
@@ -423,13 +429,17 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
             const int chunk = (lane & 7) ^ ((lb >> 1) & 7);
             const int f = b_source_col<MODE, C::WTN, kOutCols>(g, ntile, lb, &up[q]);
             voff[q] = (uint32_t)((int64_t)f * g.K * 2 + k_byte0 + chunk * 16);
-            dst[q] = C::A_ROWS * 128 + blk * 1024;
+            dst[q] = blk * 1024;
         }
     }
-    auto load = [&](int q, int ks, char* base) {
+    // A stage i at lds + i * SA (i < 2), B stage i at lds + 2 * SA + i * SB (i < 3)
+    auto load = [&](int q, int ksa, int ksb, char* abase, char* bbase) {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(q < C::QA ? ra : (up[q] ? rb1 : rb0),
-                                                 (PCM_LDS void*)(base + dst[q]), 16, voff[q], ks * 128, 0, 0);
+                                                 (PCM_LDS void*)((q < C::QA ? abase : bbase) + dst[q]), 16, voff[q],
+                                                 (q < C::QA ? ksa : ksb) * 128, 0, 0);
     };
+    char* const A0 = lds;
+    char* const B0 = lds + 2 * C::SA;
 
     floatx4 acc[C::NBK][C::MB];
     const int KT2 = K / 64;
@@ -441,7 +451,7 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
     FT af[2][C::MB], bf[2][C::NBK];
     bf16x8 braw[C::NBK];
     uint32_t bw[C::NBK][4];
-    auto b_at = [&](const char* S, int nb, int fo) { return S + (C::A_ROWS + wn * C::WTN + nb * 16) * 128 + fo; };
+    auto b_at = [&](const char* S, int nb, int fo) { return S + (wn * C::WTN + nb * 16) * 128 + fo; };
     auto a_at = [&](const char* S, int mb, int fo) { return S + (wm * C::WTM + mb * 16) * 128 + fo; };
     auto barrier = [&]() {
         __builtin_amdgcn_sched_barrier(0);
@@ -453,16 +463,21 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
     constexpr int NM = C::NM, NR = C::NR, R_EVERY = C::R_EVERY, L_EVERY = C::L_EVERY;
     constexpr int W_FROM = C::W_FROM, WPS = C::WPS;
     // One 32-wide substep: the MFMAs of (ca, cb), the fragment reads of the next substep
-    // from stage S at chunk offset fo, and (LOADS, the first substep of a stage) every load
-    // of stage ks into slot lbase. It starts with this wave's fragment reads complete and a
-    // barrier; a LOADS substep first also waits until no load is in flight, so the stage
-    // its reads need has landed and the slot it loads has been read by every wave.
+    // from the A and B stages SAr, SBr at chunk offset fo, and (LOADS, the first substep of a
+    // stage) every load of A stage ksa into slot la and of B stage ksb into slot lb. It
+    // starts with this wave's fragment reads complete and a barrier; a LOADS substep first
+    // waits until only the newest B loads (the next B stage, issued after the A loads of the
+    // stage its reads need) may be in flight, so that stage has landed, and the barrier
+    // makes the slots it loads free (read by every wave).
     // The barrier also keeps VALU writes of fragment registers (the prologue's widening)
     // at least two wait states ahead of the MFMAs that read them: the MFMAs are inline
     // assembly, which the compiler's hazard checks do not see.
     auto sub = [&](auto first, auto loads, FT (&ca)[C::MB], FT (&cb)[C::NBK],
-                   FT (&na)[C::MB], FT (&nb_)[C::NBK], const char* S, int fo, int ks, char* lbase) {
-        __builtin_amdgcn_s_waitcnt(waitcnt_imm(decltype(loads)::value ? 0 : kNoVm, 0));
+                   FT (&na)[C::MB], FT (&nb_)[C::NBK], const char* SAr, const char* SBr, int fo, int ksa, int ksb,
+                   char* la, char* lb) {
+        // a LOADS substep waits for the stage its reads need; only the B loads issued after
+        // that stage's A loads (the next B stage) may stay in flight
+        __builtin_amdgcn_s_waitcnt(waitcnt_imm(decltype(loads)::value ? C::QB : kNoVm, 0));
         barrier();
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
@@ -470,14 +485,14 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
             if (i % R_EVERY == 0 && i / R_EVERY < NR) {
                 const int j = i / R_EVERY;
                 if (j < C::NBK) {
-                    if constexpr (MODE == kExpand) nb_[j] = *(const bf16x8*)b_at(S, j, fo);
-                    else braw[j] = *(const bf16x8*)b_at(S, j, fo);
+                    if constexpr (MODE == kExpand) nb_[j] = *(const bf16x8*)b_at(SBr, j, fo);
+                    else braw[j] = *(const bf16x8*)b_at(SBr, j, fo);
                 } else {
-                    na[j - C::NBK] = Frag<MODE>::acts(a_at(S, j - C::NBK, fo));
+                    na[j - C::NBK] = Frag<MODE>::acts(a_at(SAr, j - C::NBK, fo));
                 }
             }
             if constexpr (decltype(loads)::value)
-                if (i % L_EVERY == 1 && i / L_EVERY < C::LPW) load(i / L_EVERY, ks, lbase);
+                if (i % L_EVERY == 1 && i / L_EVERY < C::LPW) load(i / L_EVERY, ksa, ksb, la, lb);
             if constexpr (MODE != kExpand) {
 #pragma unroll
                 for (int w = 0; w < WPS; ++w) {
@@ -497,26 +512,37 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
     using F_ = std::false_type;
 
     // prologue: stages 0 and 1 in flight, stage 0 landed, the fragments of substep 0 read
+    // stages 0 and 1 of A and stages 0-2 of B in flight (in that order: A0 B0 A1 B1 B2),
+    // stage 0 landed, the fragments of substep 0 read
+    const int s1 = KT2 > 1 ? 1 : 0, s2 = KT2 > 2 ? 2 : KT2 - 1;
 #pragma unroll
-    for (int q = 0; q < C::LPW; ++q) load(q, 0, lds);
+    for (int q = 0; q < C::LPW; ++q) load(q, 0, 0, A0, B0);
 #pragma unroll
-    for (int q = 0; q < C::LPW; ++q) load(q, KT2 > 1 ? 1 : 0, lds + C::STAGE);
-    __builtin_amdgcn_s_waitcnt(waitcnt_imm(C::LPW, kNoLgkm));
+    for (int q = 0; q < C::LPW; ++q) load(q, s1, s1, A0 + C::SA, B0 + C::SB);
+#pragma unroll
+    for (int q = C::QA; q < C::LPW; ++q) load(q, s2, s2, A0, B0 + 2 * C::SB);
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(C::QA + 2 * C::QB, kNoLgkm));
     barrier();
 #pragma unroll
-    for (int nb = 0; nb < C::NBK; ++nb) bf[0][nb] = Frag<MODE>::weights(b_at(lds, nb, foff0));
+    for (int nb = 0; nb < C::NBK; ++nb) bf[0][nb] = Frag<MODE>::weights(b_at(B0, nb, foff0));
 #pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb) af[0][mb] = Frag<MODE>::acts(a_at(lds, mb, foff0));
+    for (int mb = 0; mb < C::MB; ++mb) af[0][mb] = Frag<MODE>::acts(a_at(A0, mb, foff0));
     // substep 0: stage 0, first half; reads its second half
-    sub(T_{}, F_{}, af[0], bf[0], af[1], bf[1], lds, foff1, 0, lds);
+    sub(T_{}, F_{}, af[0], bf[0], af[1], bf[1], A0, B0, foff1, 0, 0, A0, B0);
+    int bi = 0;                                          // kt % 3
     for (int kt = 0; kt + 1 < KT2; ++kt) {
-        char* cur = lds + (kt & 1) * C::STAGE;          // stage kt: free after the barrier
-        const char* nxt = lds + ((kt + 1) & 1) * C::STAGE;
-        const int ks = kt + 2 < KT2 ? kt + 2 : KT2 - 1;  // past the end: re-read, never used
-        // second half of stage kt; reads the first half of stage kt+1; loads stage kt+2
-        sub(F_{}, T_{}, af[1], bf[1], af[0], bf[0], nxt, foff0, ks, cur);
+        const int bn = bi == 2 ? 0 : bi + 1;
+        char* ca = A0 + (kt & 1) * C::SA;               // stage kt: free after the barrier
+        char* cb = B0 + bi * C::SB;
+        const char* na = A0 + ((kt + 1) & 1) * C::SA;
+        const char* nbp = B0 + bn * C::SB;
+        // past the end: re-read, never used
+        const int ksa = kt + 2 < KT2 ? kt + 2 : KT2 - 1, ksb = kt + 3 < KT2 ? kt + 3 : KT2 - 1;
+        // second half of stage kt; reads the first half of stage kt+1; loads A kt+2, B kt+3
+        sub(F_{}, T_{}, af[1], bf[1], af[0], bf[0], na, nbp, foff0, ksa, ksb, ca, cb);
         // first half of stage kt+1; reads its second half
-        sub(F_{}, F_{}, af[0], bf[0], af[1], bf[1], nxt, foff1, ks, cur);
+        sub(F_{}, F_{}, af[0], bf[0], af[1], bf[1], na, nbp, foff1, ksa, ksb, ca, cb);
+        bi = bn;
     }
     // second half of the last stage: MFMAs only (after the two wait states its fragments'
     // last VALU writes need)
@@ -710,18 +736,21 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
                   "the tail tile runs on the same workgroup and N tiling");
     static_assert(CH::NT == C::NT && CH::LDS_BYTES <= C::LDS_BYTES, "the half tail tile fits");
     extern __shared__ __attribute__((aligned(1024))) char lds[];
-    __shared__ int s_item[7];
+    int* const s_item = (int*)lds;   // read into registers before the stage loads overwrite it
     int e, row0, row1, ntile, kslice;
     if (order == kLongestFirst) {          // workgroup-uniform branches and returns
         if (!il_item<C::BM, CT::BM>(g, nt, group_n, s_item)) return;
         e = s_item[0], row0 = s_item[1], row1 = s_item[2], ntile = s_item[3], kslice = s_item[4];
-        if (s_item[6]) {                   // half of a tail item: N-tile of half width
+        const int half = s_item[6];
+        __syncthreads();
+        if (half) {                        // half of a tail item: N-tile of half width
             il_tile<CH, MODE>(g, lds, e, row0, row1, ntile, kslice);
             return;
         }
     } else if (order == kExpertMajor) {
         if (!em_item<C::BM>(g, nt, group_n, s_item)) return;
         e = s_item[0], row0 = s_item[1], row1 = s_item[2], ntile = s_item[3], kslice = s_item[4];
+        __syncthreads();
     } else {
         int64_t mt;
         const int64_t per_slice = gridDim.x / g.ksplit;
@@ -729,6 +758,7 @@ __global__ __launch_bounds__(C::NT) void gemm_il_kernel(GemmArgs g, int64_t mt_u
         if (!tile_of(blockIdx.x % per_slice, per_slice, mt_upper, nt, group_n, &mt, &ntile)) return;
         if (!find_tile<C::BM>(g.offsets, g.n, g.a_rows, mt, s_item)) return;
         e = s_item[0], row0 = s_item[1], row1 = s_item[2];
+        __syncthreads();
     }
     if (row1 - row0 <= CT::BM)
         il_tile<CT, MODE>(g, lds, e, row0, row1, ntile, kslice);
