@@ -149,10 +149,11 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
     }
 }
 
-// Single-pass form of the float16 mix: each thread keeps its ITER column chunks of every
-// target row in registers (KK >= the token's target count), so U is read once; then the row maxima are
-// reduced over the workgroup and the scaled rows stored.
-template <int KK, int ITER>
+// Single-pass form of the float16 mix: each thread keeps its ITER column chunks (CPT columns
+// each) of every target row in registers (KK >= the token's target count), so U is read once;
+// then the row maxima are reduced over the workgroup and the scaled rows stored. Eight target
+// rows take 4-column chunks: with 8-column chunks a thread held 128 values and spilled.
+template <int KK, int ITER, int CPT>
 __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict__ u,
                                                         uint16_t* __restrict__ z,
                                                         float* __restrict__ zscale, MixMap m,
@@ -160,7 +161,7 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
     const int64_t t = blockIdx.x;
     if (m.live && t >= *m.live) return;  // whole workgroup
     const TokenPaths p = token_paths(m, t);
-    float zz[ITER][KK][8];
+    float zz[ITER][KK][CPT];
     float mx[KK];
 #pragma unroll
     for (int b = 0; b < KK; ++b) mx[b] = 0.f;
@@ -169,15 +170,22 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
 #pragma unroll
         for (int b = 0; b < KK; ++b)
 #pragma unroll
-            for (int i = 0; i < 8; ++i) zz[it][b][i] = 0.f;
-        const int c = (threadIdx.x + it * blockDim.x) * 8;
+            for (int i = 0; i < CPT; ++i) zz[it][b][i] = 0.f;
+        const int c = (threadIdx.x + it * blockDim.x) * CPT;
         if (c >= F) continue;
         // sources in ascending order, each row's 8 values added to every target it feeds;
         // the loads of all sources are issued before the first multiply-add
-        float ua[KK][8];
+        float ua[KK][CPT];
 #pragma unroll
         for (int a = 0; a < KK; ++a)
-            if (a < p.ns) load8(u + p.src[a] * F + c, ua[a]);
+            if (a < p.ns) {
+                if constexpr (CPT == 8) {
+                    load8(u + p.src[a] * F + c, ua[a]);
+                } else {
+                    const float4 v = *(const float4*)(u + p.src[a] * F + c);
+                    ua[a][0] = v.x; ua[a][1] = v.y; ua[a][2] = v.z; ua[a][3] = v.w;
+                }
+            }
 #pragma unroll
         for (int a = 0; a < KK; ++a) {
             if (a >= p.ns) break;
@@ -186,14 +194,14 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
                 if (b < p.nt && ((p.bits >> (a * p.K + b)) & 1)) {
                     const float w = p.beta ? p.beta[a * p.K + b] : 1.0f;
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) zz[it][b][i] = fmaf(w, ua[a][i], zz[it][b][i]);
+                    for (int i = 0; i < CPT; ++i) zz[it][b][i] = fmaf(w, ua[a][i], zz[it][b][i]);
                 }
             }
         }
 #pragma unroll
         for (int b = 0; b < KK; ++b)
 #pragma unroll
-            for (int i = 0; i < 8; ++i) mx[b] = fmaxf(mx[b], fabsf(zz[it][b][i]));
+            for (int i = 0; i < CPT; ++i) mx[b] = fmaxf(mx[b], fabsf(zz[it][b][i]));
     }
     __shared__ float red[KK][16];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -221,34 +229,38 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
     }
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {
-        const int c = (threadIdx.x + it * blockDim.x) * 8;
+        const int c = (threadIdx.x + it * blockDim.x) * CPT;
         if (c >= F) continue;
 #pragma unroll
         for (int b = 0; b < KK; ++b) {
             if (b >= p.nt) break;
-            uint32_t w[4];
+            uint32_t w[CPT / 2];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < CPT / 2; ++i) {
                 const _Float16 lo = (_Float16)(zz[it][b][2 * i] * scale[b]);
                 const _Float16 hi = (_Float16)(zz[it][b][2 * i + 1] * scale[b]);
                 w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) |
                        ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
             }
-            *(uint4*)(z + p.tgt[b] * F + c) = make_uint4(w[0], w[1], w[2], w[3]);
+            if constexpr (CPT == 8) *(uint4*)(z + p.tgt[b] * F + c) = make_uint4(w[0], w[1], w[2], w[3]);
+            else *(uint2*)(z + p.tgt[b] * F + c) = make_uint2(w[0], w[1]);
         }
     }
 }
 
-template <int KK, int ITER>
+template <int KK, int ITER, int CPT>
 void launch_mix_regs(unsigned blocks, int threads, const float* u, void* z, float* zscale,
                      const MixMap& m, int F, hipStream_t s) {
-    mix_regs_kernel<KK, ITER><<<blocks, threads, 0, s>>>(u, (uint16_t*)z, zscale, m, F);
+    mix_regs_kernel<KK, ITER, CPT><<<blocks, threads, 0, s>>>(u, (uint16_t*)z, zscale, m, F);
 }
 
 // y_t = [y_t] + sum over targets b (ascending) and K slices q (ascending) of o_(t,b) slice q.
 // One token per workgroup; each thread takes two 4-column chunks and issues the loads of
-// every row of both before the first add (up to two K slices: the projection splits K in at
-// most two). o is read once, so its loads are non-temporal.
+// every row of both before the first add. The register copy is sized by the layer (KMAX >= the
+// target count, KS = the K slices, 1 or 2; KS = 0: a loop for more slices): sized for the
+// largest case, it held 128 values and let three waves run per SIMD. o is read once, so its
+// loads are non-temporal.
+template <int KMAX, int KS>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o, int ksplit,
                                                       MixMap m, int H, float* __restrict__ y,
                                                       int accumulate) {
@@ -257,16 +269,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     constexpr int CU = 2;
     for (int c0 = threadIdx.x * 4; c0 < H; c0 += blockDim.x * 4 * CU) {
         float4 s[CU];
-        if (ksplit <= 2) {
-            float4 v[CU][kMaxK][2];
+        if constexpr (KS > 0) {   // ksplit == KS, at most KMAX targets: loads held in registers
+            float4 v[CU][KMAX][KS];
 #pragma unroll
             for (int u = 0; u < CU; ++u) {
                 const int c = c0 + u * blockDim.x * 4;
 #pragma unroll
-                for (int b = 0; b < kMaxK; ++b)
+                for (int b = 0; b < KMAX; ++b)
 #pragma unroll
-                    for (int q = 0; q < 2; ++q)
-                        if (c < H && b < p.nt && q < ksplit) {
+                    for (int q = 0; q < KS; ++q)
+                        if (c < H && b < p.nt) {
                             const floatx4 w = __builtin_nontemporal_load(
                                 (const floatx4*)(o + (q * m.R_tgt + p.tgt[b]) * H + c));
                             v[u][b][q] = make_float4(w[0], w[1], w[2], w[3]);
@@ -276,10 +288,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
             for (int u = 0; u < CU; ++u) {
                 s[u] = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-                for (int b = 0; b < kMaxK; ++b)
+                for (int b = 0; b < KMAX; ++b)
 #pragma unroll
-                    for (int q = 0; q < 2; ++q)
-                        if (b < p.nt && q < ksplit) {
+                    for (int q = 0; q < KS; ++q)
+                        if (b < p.nt) {
                             s[u].x += v[u][b][q].x; s[u].y += v[u][b][q].y;
                             s[u].z += v[u][b][q].z; s[u].w += v[u][b][q].w;
                         }
@@ -350,10 +362,11 @@ hipError_t launch_mix(const float* u, void* z, float* zscale, const MixMap& m, i
     const int kslots = m.bits ? m.K : 1;
     if (zscale) {
         // single pass when a thread's share of every target row fits in 64 registers
-        const int chunks = F / 8;
+        const int kk = kslots <= 1 ? 1 : (kslots <= 2 ? 2 : (kslots <= 4 ? 4 : 8));
+        const int cpt = (kk == 8 && F / 4 <= 1024) ? 4 : 8;   // columns per thread
+        const int chunks = F / cpt;
         const int threads_r = chunks >= 1024 ? 1024 : ((chunks + 63) / 64) * 64;
         const int iter = (chunks + threads_r - 1) / threads_r;
-        const int kk = kslots <= 1 ? 1 : (kslots <= 2 ? 2 : (kslots <= 4 ? 4 : 8));
         const int it = iter <= 1 ? 1 : (iter <= 2 ? 2 : (iter <= 4 ? 4 : (iter <= 8 ? 8 : 16)));  // 16: two-pass
         const unsigned blocks = (unsigned)T;
         if (kk * it <= 8) {
@@ -362,16 +375,16 @@ hipError_t launch_mix(const float* u, void* z, float* zscale, const MixMap& m, i
                 return hipGetLastError();
             };
             switch (kk * 100 + it) {
-                case 101: return go(launch_mix_regs<1, 1>);
-                case 102: return go(launch_mix_regs<1, 2>);
-                case 104: return go(launch_mix_regs<1, 4>);
-                case 108: return go(launch_mix_regs<1, 8>);
-                case 201: return go(launch_mix_regs<2, 1>);
-                case 202: return go(launch_mix_regs<2, 2>);
-                case 204: return go(launch_mix_regs<2, 4>);
-                case 401: return go(launch_mix_regs<4, 1>);
-                case 402: return go(launch_mix_regs<4, 2>);
-                case 801: return go(launch_mix_regs<8, 1>);
+                case 101: return go(launch_mix_regs<1, 1, 8>);
+                case 102: return go(launch_mix_regs<1, 2, 8>);
+                case 104: return go(launch_mix_regs<1, 4, 8>);
+                case 108: return go(launch_mix_regs<1, 8, 8>);
+                case 201: return go(launch_mix_regs<2, 1, 8>);
+                case 202: return go(launch_mix_regs<2, 2, 8>);
+                case 204: return go(launch_mix_regs<2, 4, 8>);
+                case 401: return go(launch_mix_regs<4, 1, 8>);
+                case 402: return go(launch_mix_regs<4, 2, 8>);
+                case 801: return cpt == 4 ? go(launch_mix_regs<8, 1, 4>) : go(launch_mix_regs<8, 1, 8>);
                 default: break;
             }
         }
@@ -385,8 +398,24 @@ hipError_t launch_combine(const float* o, int ksplit, const MixMap& m, int64_t T
                           int accumulate, hipStream_t s) {
     if (T == 0) return hipSuccess;
     const int threads = H / 4 >= 256 ? 256 : ((H / 4 + 63) / 64) * 64;
-    combine_kernel<<<(unsigned)T, threads, 0, s>>>(o, ksplit, m, H, y, accumulate);
-    return hipGetLastError();
+    const int K = m.bits ? m.K : 1;
+    const int kmax = K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8));
+    const int ks = ksplit == 1 || ksplit == 2 ? ksplit : 0;
+    auto go = [&](auto kern) {
+        kern<<<(unsigned)T, threads, 0, s>>>(o, ksplit, m, H, y, accumulate);
+        return hipGetLastError();
+    };
+    switch (kmax * 10 + ks) {
+        case 11: return go(combine_kernel<1, 1>);
+        case 12: return go(combine_kernel<1, 2>);
+        case 21: return go(combine_kernel<2, 1>);
+        case 22: return go(combine_kernel<2, 2>);
+        case 41: return go(combine_kernel<4, 1>);
+        case 42: return go(combine_kernel<4, 2>);
+        case 81: return go(combine_kernel<8, 1>);
+        case 82: return go(combine_kernel<8, 2>);
+        default: return go(combine_kernel<8, 0>);
+    }
 }
 
 }  // namespace pcm
