@@ -161,6 +161,9 @@ SMALL = {
     "decode_s": scaled(CONFIGS["decode"], H=512, F=256, name="decode_s"),
     # long F and few output tiles: the large-tile projection splits K in two slices
     "splitk_s": scaled(CONFIGS["mixtral"], T=300, H=256, F=4096, n=4, name="splitk_s"),
+    # one and two 64-wide K stages (H = 64, F = 128): the pipelines' start-up loads past the
+    # last stage are clamped re-reads
+    "shortk_s": scaled(CONFIGS["mixtral"], T=700, H=64, F=128, n=4, name="shortk_s"),
 }
 
 
