@@ -267,7 +267,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     const int64_t t = blockIdx.x;
     const TokenPaths p = token_paths(m, t);
     constexpr int CU = 2;
-    for (int c0 = threadIdx.x * 4; c0 < H; c0 += blockDim.x * 4 * CU) {
+    // column blocks of CB columns (CU chunks of 4 per thread): blockIdx.y takes every
+    // gridDim.y-th block
+    const int CB = blockDim.x * 4 * CU;
+    for (int c0 = blockIdx.y * CB + threadIdx.x * 4; c0 < H; c0 += gridDim.y * CB) {
         float4 s[CU];
         if constexpr (KS > 0) {   // ksplit == KS, at most KMAX targets: loads held in registers
             float4 v[CU][KMAX][KS];
@@ -401,8 +404,12 @@ hipError_t launch_combine(const float* o, int ksplit, const MixMap& m, int64_t T
     const int K = m.bits ? m.K : 1;
     const int kmax = K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8));
     const int ks = ksplit == 1 || ksplit == 2 ? ksplit : 0;
+    // a few tokens (decode): the columns of a token are split over several workgroups, so that
+    // the chip is not left to a handful of long-running ones
+    const int col_blocks = (H + threads * 8 - 1) / (threads * 8);
+    const int split = T >= 1024 ? 1 : col_blocks;
     auto go = [&](auto kern) {
-        kern<<<(unsigned)T, threads, 0, s>>>(o, ksplit, m, H, y, accumulate);
+        kern<<<dim3((unsigned)T, (unsigned)split), threads, 0, s>>>(o, ksplit, m, H, y, accumulate);
         return hipGetLastError();
     };
     switch (kmax * 10 + ks) {
