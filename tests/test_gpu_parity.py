@@ -181,6 +181,20 @@ def test_layer_small(name, tile, monkeypatch):
     assert_y_close(y, ref, cfg.dtype, f"{name}/{tile}")
 
 
+@pytest.mark.parametrize("T", [60, 64, 68])
+def test_layer_tile_policy_boundary(T):
+    """Mean expansion rows per expert of 15, 16 and 17 (n = 8, k = 2): the default choice moves
+    from the streaming kernel to the large tiles at 16 rows, and the projection (fewer rows after
+    the target mix) may take the other kernel in the same layer; every side matches the
+    oracle."""
+    cfg = scaled(SMALL["mixtral_s"], T=T, name=f"boundary{T}")
+    assert (cfg.n, cfg.k) == (8, 2)
+    say(f"tile policy boundary T={T} mean rows {T * cfg.k // cfg.n}")
+    inp = make_inputs(cfg, seed=29)
+    y = run_layer(dev(inp), cfg.k)
+    assert_y_close(y, oracle.layer_inputs(inp), cfg.dtype, cfg.name)
+
+
 @pytest.mark.parametrize("beta_mode", [1, 2])
 def test_layer_beta_modes(beta_mode):
     cfg = SMALL["olmoe_s"]
