@@ -29,9 +29,13 @@
 //    A group's last tile with at most 128 rows runs as a 128 x 256 tile (64 x 128 per wave)
 //    in the same launch.
 //  * "staged" (medium tiles): loads through registers into two LDS stages of 64-wide K
-//    steps; rows of 128 bytes with chunk c of row r at position c ^ ((r >> 1) & 7).
-//  * "stream" (a few rows per group, decode): no LDS, fragments loaded straight into a
-//    register ring several k-steps ahead; the weights are the traffic.
+//    steps; rows of 128 bytes with chunk c of row r at position c ^ ((r >> 1) & 7). Runs
+//    only where the large tiles' 32-bit buffer offsets would not reach.
+//  * "stream" (fewer than 16 rows per group, decode): each wave streams its 32 weight rows
+//    and its activation block through a ring of its own in LDS (no barrier), every direct
+//    load covering whole 128-byte lines; the weights are the traffic. A register-ring
+//    variant (fragments loaded straight into registers several k-steps ahead) runs where
+//    the ring's 32-bit offsets would not reach.
 // The MFMA takes the weight fragment as its first operand, so each lane's four
 // accumulators are four consecutive output columns of one row (16-byte stores). For the
 // expansion, a wave's weight rows are half gate and half up for the same columns, so the
@@ -1315,7 +1319,7 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
 }
 
 // Tile shape: an environment override (PCM_GEMM_TILE = S | M | L) for tests and tuning,
-// otherwise by the mean rows per group.
+// otherwise by the mean rows per group (below 16 the streaming kernel, else the large tiles).
 // The large tiles address `a` and one group's weights through 32-bit buffer offsets, so
 // both must stay below 4 GiB (a_bytes: all rows of `a`; w_bytes: one group's weights).
 char pick_tile(int64_t R, int groups, int64_t a_bytes, int64_t w_bytes) {
