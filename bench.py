@@ -2,18 +2,28 @@
 
 A step is one forward pass of the whole layer (route, build paths, expand, project
 and combine, plus the shared expert when the workload has one) over one batch of
-synthetic, seeded inputs already resident in HBM. Prints ONE JSON line.
+synthetic, seeded inputs already resident in HBM. Prints ONE JSON line: the headline
+workload (Mixtral-shaped) at the top level, and every workload under "workloads".
 
-  python bench.py [--steps K] [--warmup W] [--config NAME] [--router topk|scored]
+  python bench.py [--steps K] [--warmup W] [--config NAME] [--only] [--router topk|scored]
                   [--no-cpu-baseline]
+  python bench.py --trace-summary DIR     per-kernel durations of the timed launches in a
+                                          rocprofv3 kernel trace written under DIR
 
-The dominant kernel's roofline figure uses its average launch duration, measured
-with HIP events recorded on the stream the kernel runs on, over the timed steps.
-The CPU baseline times the float64 oracle on a bounded sample of the same tokens.
+Per-kernel times come from HIP events recorded on the stream the kernels run on: around
+each call, and inside pcm_project_combine between the mix, the projection GEMM and the
+combine (pcm_tuning's stage events). A second pass over the same steps writes a 512 MB
+buffer before each step, so that the memory-bound stages (route, path build, mix,
+combine) read from HBM rather than from the 256 MB MALL; their GB/s come from that pass.
+The timed region is fenced by two short spin kernels, which --trace-summary uses to keep
+only the timed launches of a rocprofv3 trace. The CPU baseline times the float64 oracle on
+a bounded sample of the headline workload's tokens.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
 import json
 import os
 import sys
@@ -25,6 +35,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "path-MoE layer tokens/sec and grouped-GEMM TFLOP/s (% bf16 MFMA peak), 1 GPU"
+FLUSH_BYTES = 512 << 20
+FENCE = "spin_kernel"
 
 
 def parse():
@@ -32,7 +44,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default=None)
+    ap.add_argument("--config", default=None, help="headline workload (default: mixtral)")
+    ap.add_argument("--only", action="store_true",
+                    help="measure the headline workload only (for profiler runs)")
     ap.add_argument("--router", choices=("topk", "scored"), default="topk",
                     help="topk: top-k experts, paths among them allowed by the mask; "
                          "scored: scored compositional routing over the active paths")
@@ -49,7 +63,40 @@ def parse():
                     help="target CPU time of the oracle sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer 5 times (calibrates HBM byte counters)")
+    ap.add_argument("--trace-summary", default=None, metavar="DIR",
+                    help="summarise the timed launches of a rocprofv3 kernel trace under DIR")
     return ap.parse_args()
+
+
+# ------------------------------------------------------------------ trace summary
+def trace_summary(path: str):
+    """Per-kernel launch durations inside each fenced timed region of a rocprofv3 kernel
+    trace (markdown table on stdout)."""
+    files = sorted(glob.glob(os.path.join(path, "**", "*kernel_trace.csv"), recursive=True))
+    if not files:
+        sys.exit(f"no kernel_trace.csv under {path}")
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    fences = [i for i, r in enumerate(rows) if FENCE in r["Kernel_Name"]]
+    if len(fences) < 2:
+        sys.exit("the trace has no fenced timed region")
+    for reg, (a, b) in enumerate(zip(fences[0::2], fences[1::2])):
+        stats = {}
+        for r in rows[a + 1:b]:
+            d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            stats.setdefault(r["Kernel_Name"], []).append(d)
+        span = (int(rows[b]["Start_Timestamp"]) - int(rows[a]["End_Timestamp"])) / 1e3
+        print(f"### timed region {reg}: {span:.1f} us between the fences\n")
+        print("| kernel | launches | avg us | min us | max us | total us |")
+        print("|---|---|---|---|---|---|")
+        for name, ds in sorted(stats.items(), key=lambda kv: -sum(kv[1])):
+            short = name.split("(")[0].replace("void ", "")
+            print(f"| `{short}` | {len(ds)} | {np.mean(ds):.1f} | {min(ds):.1f} | {max(ds):.1f} | "
+                  f"{sum(ds):.1f} |")
+        print()
 
 
 def copy_probe(mib: int):
@@ -79,6 +126,16 @@ def measured_traffic(workload: str):
     return None if w is None else w["bytes_per_launch"]
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(inp, target_s: float) -> dict:
     import oracle
     cfg = inp.cfg
@@ -95,10 +152,198 @@ def cpu_baseline(inp, target_s: float) -> dict:
             break
         ntok = min(cfg.T, int(ntok * max(2.0, target_s / max(spent, 1e-3) * 0.9)))
     return {"value": round(toks.size / spent, 3), "unit": "tokens/s", "cores": nt, "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{toks.size} of {cfg.T} tokens of the same workload (route, paths, per-path "
                       f"float64 evaluation), {spent:.1f} s wall on {nt} threads"}
 
 
+# ------------------------------------------------------------------ inputs on the device
+def device_inputs(cfg, seed: int, host_weights: bool):
+    """The layer's inputs on cuda:0. x, logits and the mask always come from the seeded host
+    generator (they decide the routing); the expert weights too when host_weights (the
+    oracle needs them), otherwise they are drawn on the device with the same distribution
+    (N(0, w_std), rounded to the layer's dtype), which keeps the decode-shaped layer's 22 GB
+    of weights off the host."""
+    import torch
+    from workloads import make_inputs
+    dev = "cuda:0"
+    inp = make_inputs(cfg, seed=seed, with_weights=host_weights)
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    d = {"x": inp.x.to(dev), "logits": torch.from_numpy(inp.logits).to(dev),
+         "mask": torch.from_numpy(inp.mask).to(dev), "dtype": dtype, "inp": inp}
+    if host_weights:
+        d["wg"], d["wu"], d["wd"] = inp.w_gate.to(dev), inp.w_up.to(dev), inp.w_down.to(dev)
+        d["shared"] = ((inp.s_gate.to(dev), inp.s_up.to(dev), inp.s_down.to(dev))
+                       if cfg.shared_F else None)
+    else:
+        g = torch.Generator(device=dev).manual_seed(seed * 1000 + 17)
+
+        def rnd(*shape):
+            w = torch.empty(shape, dtype=torch.float32, device=dev)
+            w.normal_(0.0, cfg.w_std, generator=g)
+            return w.to(dtype)
+        d["wg"], d["wu"], d["wd"] = rnd(cfg.n, cfg.F, cfg.H), rnd(cfg.n, cfg.F, cfg.H), rnd(cfg.n, cfg.H, cfg.F)
+        d["shared"] = ((rnd(cfg.shared_F, cfg.H), rnd(cfg.shared_F, cfg.H), rnd(cfg.H, cfg.shared_F))
+                       if cfg.shared_F else None)
+    return d
+
+
+# ------------------------------------------------------------------ one workload
+def measure(pcm, name, cfg, d, args, flush, scored):
+    """Timed steps of one workload: wall time per step, per-stage times from HIP events, and
+    the same stages again with the MALL flushed before each step."""
+    import torch
+    from paper_2609_01024_amd import binding
+    dev = "cuda:0"
+    stream = torch.cuda.current_stream()
+    x, logits, mask, wg, wu, wd, shared = (d["x"], d["logits"], d["mask"], d["wg"], d["wu"],
+                                           d["wd"], d["shared"])
+    if scored:
+        from workloads import make_scored_inputs
+        sinp = make_scored_inputs(cfg, seed=args.seed)
+        g_tgt = torch.from_numpy(sinp.g_tgt).to(dev)
+        plan = pcm.ScoredLayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, d["dtype"], dev, cfg.shared_F)
+        plan.build_layout(mask, torch.from_numpy(sinp.bias).to(dev))   # once per layer
+        marks = (["shared"] if shared else []) + ["route", "expand"]
+    else:
+        sinp = None
+        plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, d["dtype"], dev, cfg.shared_F)
+        marks = (["shared"] if shared else []) + ["route", "build_paths", "expand"]
+
+    def new_events():
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(marks) + 1)]
+        inner = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        for e in inner:           # created by a first record; the library records them again
+            e.record(stream)
+        t = binding.Tuning(stage_events=inner).struct()
+        return ev, inner, t
+
+    def step(slot=None):
+        ev, _, tun = slot if slot is not None else (None, None, None)
+        it = iter(range(len(marks) + 1))
+
+        def mark():
+            i = next(it)
+            if ev is not None:
+                ev[i].record(stream)
+        mark()
+        if shared:
+            pcm.pcm_dense_swiglu(x, *shared, y=plan.y, accumulate=False, ws=plan.ws_shared)
+            mark()
+        if scored:
+            pcm.pcm_route_scored(logits, g_tgt, sinp.lam, plan.layout, cfg.k, out=plan.paths,
+                                 ws=plan.ws_route)
+            mark()
+            pcm.pcm_expand_scored(x, wg, wu, plan.paths, u=plan.u)
+            mark()
+            pcm.pcm_project_combine_scored(plan.u, wd, plan.paths, y=plan.y,
+                                           accumulate=bool(shared), ws=plan.ws_proj, tuning=tun)
+        else:
+            pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
+            mark()
+            pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
+            mark()
+            pcm.pcm_expand(x, wg, wu, plan.paths, u=plan.u)
+            mark()
+            pcm.pcm_project_combine(plan.u, wd, plan.paths, y=plan.y, accumulate=bool(shared),
+                                    ws=plan.ws_proj, tuning=tun)
+
+    def stage_ms(slots):
+        out = {}
+        for i, st in enumerate(marks):
+            out[st] = float(np.median([s[0][i].elapsed_time(s[0][i + 1]) for s in slots]))
+        for i, st in enumerate(("mix", "project", "combine")):
+            out[st] = float(np.median([s[1][i].elapsed_time(s[1][i + 1]) for s in slots]))
+        out["project_combine"] = float(np.median([s[0][-1].elapsed_time(s[1][3]) for s in slots]))
+        return out
+
+    def fence():
+        if hasattr(torch.cuda, "_sleep"):
+            torch.cuda._sleep(1000)
+
+    for _ in range(args.warmup):
+        step()
+    slots = [new_events() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    fence()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(slots[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fence()
+    torch.cuda.synchronize()
+    timed = stage_ms(slots)
+    # the same steps with the MALL flushed before each (outside the recorded stages)
+    fslots = [new_events() for _ in range(args.steps)]
+    for s in range(args.steps):
+        flush.fill_(s & 0xFF)
+        step(fslots[s])
+    torch.cuda.synchronize()
+    flushed = stage_ms(fslots)
+    return plan, sinp, wall * 1e3 / args.steps, timed, flushed
+
+
+def workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored):
+    """Throughput, GEMM rates against the bf16 peak and GB/s of the memory-bound stages."""
+    bf16 = cfg.dtype == "bf16"
+    K = cfg.k
+    if scored:
+        src_off = plan.paths.src_offsets.cpu().numpy()
+        tgt_off = plan.paths.tgt_offsets.cpu().numpy()
+        R, R_tgt = int(src_off[-1]), int(tgt_off[-1])
+        touched_src = int(np.count_nonzero(np.diff(src_off)))
+        touched_tgt = int(np.count_nonzero(np.diff(tgt_off)))
+        touched = int(np.count_nonzero(np.diff(src_off) + np.diff(tgt_off)))
+        R_bound = cfg.T * K
+    else:
+        off = plan.paths.expert_offsets.cpu().numpy()
+        touched = touched_src = touched_tgt = int(np.count_nonzero(np.diff(off)))
+        R = R_tgt = R_bound = cfg.R
+    f = acc.gemm_flops(R, cfg.H, cfg.F, cfg.T, cfg.shared_F, R_tgt)
+    peak = acc.BF16_PEAK_TFLOPS if bf16 else acc.FP32_PEAK_TFLOPS
+    gemm_ms = st["expand"] + st["project_combine"] + st.get("shared", 0.0)
+    ksplit = pcm.project_workspace_layout(cfg.T, cfg.H, cfg.F, cfg.n, K,
+                                          pcm.PCM_BF16 if bf16 else pcm.PCM_F32)["ksplit"]
+    u_elem, z_elem = 4, (2 if bf16 else 4)
+    hbm = {"mix": acc.mix_bytes(R, R_tgt, cfg.F, cfg.T, K, u_elem, z_elem) / (fl["mix"] * 1e-3) / 1e9,
+           "combine": acc.combine_bytes(R_bound, cfg.H, cfg.T, K, ksplit, bool(cfg.shared_F))
+           / (fl["combine"] * 1e-3) / 1e9}
+    if not scored:
+        hbm["route"] = acc.route_bytes(cfg.T, cfg.n, K) / (fl["route"] * 1e-3) / 1e9
+        hbm["build_paths"] = acc.paths_bytes(cfg.T, cfg.n, K) / (fl["build_paths"] * 1e-3) / 1e9
+    rec = {"ms": round(ms, 4), "tokens_per_s": round(cfg.T / (ms * 1e-3), 1),
+           "rows": R, "touched_experts": touched,
+           "gemm_tflops": round(f["total"] / (gemm_ms * 1e-3) / 1e12, 1),
+           "gemm_frac_peak": round(f["total"] / (gemm_ms * 1e-3) / 1e12 / peak, 4),
+           "stages_ms": {k: round(v, 4) for k, v in st.items()},
+           "stages_flushed_ms": {k: round(v, 4) for k, v in fl.items()},
+           "hbm_GBps": {k: round(v, 1) for k, v in hbm.items()},
+           "hbm_frac": {k: round(v / acc.HBM_PEAK_GBS, 4) for k, v in hbm.items()}}
+    if scored:
+        rec["projection_rows"] = R_tgt
+    if name == "decode":
+        # weight streaming: every touched expert's matrices are read once per step
+        eb = touched_src * 2 * cfg.H * cfg.F * 2
+        pb = touched_tgt * cfg.H * cfg.F * 2
+        rec.update({"expand_GBps": round(eb / (st["expand"] * 1e-3) / 1e9, 1),
+                    "expand_frac": round(eb / (st["expand"] * 1e-3) / 1e9 / acc.HBM_PEAK_GBS, 4),
+                    "project_GBps": round(pb / (st["project"] * 1e-3) / 1e9, 1),
+                    "project_frac": round(pb / (st["project"] * 1e-3) / 1e9 / acc.HBM_PEAK_GBS, 4),
+                    "layer_weight_GBps": round((eb + pb) / (ms * 1e-3) / 1e9, 1)})
+    else:
+        et = f["expand"] / (st["expand"] * 1e-3) / 1e12
+        pt = f["project"] / (st["project"] * 1e-3) / 1e12
+        rec.update({"expand_tflops": round(et, 1), "expand_frac": round(et / peak, 4),
+                    "project_tflops": round(pt, 1), "project_frac": round(pt / peak, 4)})
+        if cfg.shared_F:
+            rec["shared_tflops"] = round((f["shared_expand"] + f["shared_project"])
+                                         / (st["shared"] * 1e-3) / 1e12, 1)
+    return rec, f, R, touched_src
+
+
+# ------------------------------------------------------------------ other modes
 def stack_bench(args):
     """A decode step through a stack of L MoE layers of the workload's shape, weights drawn
     on the device (resident in HBM before timing)."""
@@ -168,11 +413,13 @@ def router_gemm(pcm, cfg, x, args):
             "TFLOPs": round(2 * cfg.T * cfg.H * cfg.n / (ms * 1e-3) / 1e12, 2)}
 
 
-def ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args):
+def ablation(pcm, plan, cfg, d, args):
     """Layer time of the same routing and paths executed three other ways (Table 3's
     question on this hardware): one projection per path reusing U per source; one expansion
     and one projection per path; and the vanilla top-k layer (diagonal-only mask)."""
     import torch
+    x, logits, mask, wg, wu, wd, shared = (d["x"], d["logits"], d["mask"], d["wg"], d["wu"],
+                                           d["wd"], d["shared"])
     n_paths = int(np.unpackbits(plan.paths.path_bits.cpu().numpy().view(np.uint8)).sum())
 
     def timed(fn):
@@ -218,158 +465,81 @@ def ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args):
 
 def main():
     args = parse()
+    if args.trace_summary:
+        trace_summary(args.trace_summary)
+        return
     if args.copy_probe:
         copy_probe(args.copy_probe)
-        return
-    if args.stack:
-        if args.gpus != 1:
-            print("bench.py measures one GPU only", file=sys.stderr)
-            sys.exit(2)
-        stack_bench(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the layer is sharded by design, not measured, across GPUs)", file=sys.stderr)
         sys.exit(2)
+    if args.stack:
+        stack_bench(args)
+        return
 
     import torch
 
     import paper_2609_01024_amd as pcm
     from paper_2609_01024_amd import accounting as acc
-    from workloads import CONFIGS, HEADLINE, make_inputs
+    from workloads import CONFIGS, HEADLINE
 
-    name = args.config or HEADLINE
-    cfg = CONFIGS[name]
-    t0 = time.time()
-    inp = make_inputs(cfg, seed=args.seed)
-    print(f"[bench] {name}: inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
-    dev = "cuda:0"
-    x = inp.x.to(dev)
-    logits = torch.from_numpy(inp.logits).to(dev)
-    mask = torch.from_numpy(inp.mask).to(dev)
-    wg, wu, wd = inp.w_gate.to(dev), inp.w_up.to(dev), inp.w_down.to(dev)
-    shared = (inp.s_gate.to(dev), inp.s_up.to(dev), inp.s_down.to(dev)) if cfg.shared_F else None
-    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-    stream = torch.cuda.current_stream()
+    head = args.config or HEADLINE
     scored = args.router == "scored"
-    if scored:
-        from workloads import make_scored_inputs
-        sinp = make_scored_inputs(cfg, seed=args.seed)
-        g_tgt = torch.from_numpy(sinp.g_tgt).to(dev)
-        plan = pcm.ScoredLayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
-        plan.build_layout(mask, torch.from_numpy(sinp.bias).to(dev))   # once per layer
-        stages = (["shared"] if shared else []) + ["route", "expand", "project_combine"]
-    else:
-        plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, dtype, dev, cfg.shared_F)
-        stages = (["shared"] if shared else []) + ["route", "build_paths", "expand", "project_combine"]
-
-    def step(events=None):
-        # the stages in the order LayerPlan.forward runs them: the shared expert (if any)
-        # stores y first, and the combine adds the routed sum to it
-        marks = iter(range(len(stages) + 1))
-
-        def mark():
-            i = next(marks)
-            if events is not None:
-                events[i].record(stream)
-        mark()
-        if shared:
-            pcm.pcm_dense_swiglu(x, *shared, y=plan.y, accumulate=False, ws=plan.ws_shared)
-            mark()
-        if scored:
-            pcm.pcm_route_scored(logits, g_tgt, sinp.lam, plan.layout, cfg.k, out=plan.paths,
-                                 ws=plan.ws_route)
-            mark()
-            pcm.pcm_expand_scored(x, wg, wu, plan.paths, u=plan.u)
-            mark()
-            pcm.pcm_project_combine_scored(plan.u, wd, plan.paths, y=plan.y, accumulate=bool(shared),
-                                           ws=plan.ws_proj)
-            mark()
-        else:
-            pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
-            mark()
-            pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
-            mark()
-            pcm.pcm_expand(x, wg, wu, plan.paths, u=plan.u)
-            mark()
-            pcm.pcm_project_combine(plan.u, wd, plan.paths, y=plan.y, accumulate=bool(shared),
-                                    ws=plan.ws_proj)
-            mark()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
-           for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(evs[s])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    stage_ms = {st: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
-                for i, st in enumerate(stages)}
-    ms = wall * 1e3 / args.steps
-
-    if scored:
-        src_off = plan.paths.src_offsets.cpu().numpy()
-        tgt_off = plan.paths.tgt_offsets.cpu().numpy()
-        R, R_tgt = int(src_off[-1]), int(tgt_off[-1])
-        touched = int(np.count_nonzero(np.diff(src_off) + np.diff(tgt_off)))
-        touched_src = int(np.count_nonzero(np.diff(src_off)))
-        touched_tgt = int(np.count_nonzero(np.diff(tgt_off)))
-    else:
-        offsets = plan.paths.expert_offsets.cpu().numpy()
-        touched = touched_src = touched_tgt = int(np.count_nonzero(np.diff(offsets)))
-        R = R_tgt = cfg.R
-    fl = acc.gemm_flops(R, cfg.H, cfg.F, cfg.T, cfg.shared_F, R_tgt)
-    gemm_ms = stage_ms["expand"] + stage_ms["project_combine"] + stage_ms.get("shared", 0.0)
-    gemm_tflops = fl["total"] / (gemm_ms * 1e-3) / 1e12
-    bf16 = cfg.dtype == "bf16"
-    peak = acc.BF16_PEAK_TFLOPS if bf16 else acc.FP32_PEAK_TFLOPS
-
-    traffic = measured_traffic(name)
-
-    if name == "decode":
-        # weight streaming: every touched expert's three matrices are read once per step
-        wbytes = (touched_src * 2 + touched_tgt) * cfg.H * cfg.F * 2 + \
-            (3 * cfg.H * cfg.shared_F * 2 if cfg.shared_F else 0)
-        exp_bytes = touched_src * 2 * cfg.H * cfg.F * 2
-        achieved = exp_bytes / (stage_ms["expand"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": acc.HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / acc.HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "expand (grouped gate/up GEMM + SwiGLU)",
-                "per_launch": f"{touched_src} source experts x 2*H*F*2 B of gate/up weights"}
-        extra = {"layer_weight_GBps": round(wbytes / (ms * 1e-3) / 1e9, 1)}
-    else:
-        achieved = fl["expand"] / (stage_ms["expand"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": traffic,
-                "kernel": "expand (grouped gate/up GEMM + SwiGLU)",
-                "per_launch": f"4*H*F flop x R={R} rows"}
-        extra = {}
-
-    line = {
-        "metric": METRIC, "value": round(cfg.T / (ms * 1e-3), 1), "unit": "tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
-        "config": {"workload": f"{name}: T={cfg.T} H={cfg.H} n={cfg.n} F={cfg.F} k={cfg.k} "
-                               f"mask density {cfg.density}"
-                               + (f" shared F={cfg.shared_F}" if cfg.shared_F else ""),
-                   "tokens": cfg.T, "rows": R, "touched_experts": touched,
-                   "router": args.router,
-                   **({"projection_rows": R_tgt, "lambda": sinp.lam} if scored else {})},
-        "gemm_tflops": round(gemm_tflops, 1), "gemm_frac_peak": round(gemm_tflops / peak, 4),
-        "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
-        "roofline": roof, **extra,
-    }
-    line["router_gemm"] = router_gemm(pcm, cfg, x, args)
-    if args.ablation and not scored:
-        line["ablation"] = ablation(pcm, plan, cfg, x, wg, wu, wd, logits, mask, shared, args)
-    if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    order = [head] + ([] if args.only else [w for w in CONFIGS if w != head])
+    flush = torch.empty((FLUSH_BYTES,), dtype=torch.uint8, device="cuda:0")
+    records, line = {}, None
+    for name in order:
+        cfg = CONFIGS[name]
+        t0 = time.time()
+        d = device_inputs(cfg, args.seed, host_weights=(name == head))
+        print(f"[bench] {name}: inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+        plan, sinp, ms, st, fl = measure(pcm, name, cfg, d, args, flush, scored)
+        rec, f, R, touched_src = workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored)
+        records[name] = rec
+        print(f"[bench] {name}: {ms:.3f} ms per layer", file=sys.stderr, flush=True)
+        if name == head:
+            bf16 = cfg.dtype == "bf16"
+            peak = acc.BF16_PEAK_TFLOPS if bf16 else acc.FP32_PEAK_TFLOPS
+            traffic = measured_traffic(name)
+            if name == "decode":
+                exp_bytes = touched_src * 2 * cfg.H * cfg.F * 2
+                achieved = exp_bytes / (st["expand"] * 1e-3) / 1e9
+                roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": acc.HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(achieved / acc.HBM_PEAK_GBS, 4),
+                        "traffic": traffic, "kernel": "expand (grouped gate/up GEMM + SwiGLU)",
+                        "per_launch": f"{touched_src} source experts x 2*H*F*2 B of gate/up weights"}
+            else:
+                achieved = f["expand"] / (st["expand"] * 1e-3) / 1e12
+                roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak,
+                        "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
+                        "kernel": "expand (grouped gate/up GEMM + SwiGLU)",
+                        "per_launch": f"4*H*F flop x R={R} rows"}
+            line = {
+                "metric": METRIC, "value": round(cfg.T / (ms * 1e-3), 1), "unit": "tokens/s",
+                "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+                "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+                "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
+                "config": {"workload": f"{name}: T={cfg.T} H={cfg.H} n={cfg.n} F={cfg.F} k={cfg.k} "
+                                       f"mask density {cfg.density}"
+                                       + (f" shared F={cfg.shared_F}" if cfg.shared_F else ""),
+                           "tokens": cfg.T, "rows": R, "touched_experts": rec["touched_experts"],
+                           "router": args.router,
+                           **({"projection_rows": rec["projection_rows"], "lambda": sinp.lam}
+                              if scored else {})},
+                "gemm_tflops": rec["gemm_tflops"], "gemm_frac_peak": rec["gemm_frac_peak"],
+                "stages_ms": rec["stages_ms"], "hbm_GBps": rec["hbm_GBps"], "roofline": roof,
+            }
+            line["router_gemm"] = router_gemm(pcm, cfg, d["x"], args)
+            if args.ablation and not scored:
+                line["ablation"] = ablation(pcm, plan, cfg, d, args)
+            if not args.no_cpu_baseline:
+                print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+                line["cpu_baseline"] = cpu_baseline(d["inp"], args.cpu_seconds)
+        del plan, d
+        torch.cuda.empty_cache()
+    line["workloads"] = records
     print(json.dumps(line), flush=True)
 
 

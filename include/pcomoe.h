@@ -52,8 +52,14 @@ typedef enum pcm_dtype {
     PCM_BF16 = 1   /* x and weights bfloat16; float32 accumulate throughout. The expansion
                       runs on bf16 MFMA and keeps u in float32; the projection input z is
                       carried as row-scaled float16 (11 significant bits) and the bf16
-                      projection weights are widened to float16 in registers (exact in
-                      float16's normal range), so the projection runs on f16 MFMA */
+                      projection weights are widened to float16 in registers, so the
+                      projection runs on f16 MFMA. Precondition on the projection weights
+                      (w_down, and the shared expert's): |w| <= 65504, float16's largest value
+                      (larger values become inf). Values with |w| >= 2^-17 widen exactly (a
+                      bfloat16 there has at most 8 significant bits, all of which float16's
+                      normal and upper subnormal range keep); smaller values round to the nearest
+                      multiple of 2^-24 (float16's subnormal spacing; absolute error <= 2^-25),
+                      so that magnitudes of 2^-25 or less become 0 */
 } pcm_dtype;
 
 /* Path weights beta_ab for (a, b) in Pi (p = the renormalised router weights).
@@ -246,6 +252,59 @@ pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void
                                       const pcm_scored_paths* paths, int64_t T, int H, int F,
                                       int n, int K, float* y, int accumulate, void* ws,
                                       size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------- tests and measurement
+ * A layer never needs these. The *_tuned calls are the calls above with a pcm_tuning that
+ * forces kernel choices the library otherwise makes by shape (every choice computes the same
+ * bits) and that records HIP events between the internal stages of a call; tuning = NULL is
+ * the plain call. They let tests check each kernel on the same inputs and let benchmarks time
+ * each stage on the stream it runs on. Values outside the documented sets give PCM_ERR_ARG. */
+typedef struct pcm_tuning {
+    int tile;              /* 0: chosen by the mean rows per expert; 'S' the few-row streaming
+                              kernel, 'M' the medium tiles, 'L' the large tiles (the medium tiles
+                              run instead where 32-bit buffer offsets would not reach) */
+    int order_expand;      /* work order of the large tiles in expansion GEMMs: -1 by shape,
+                              0 grouped, 1 longest first, 2 expert-major */
+    int order_down;        /* the same for projection GEMMs */
+    int em_window;         /* workgroups per expert-major window (0: 8) */
+    int group_n;           /* N tiles per group of the grouped order (0: 4) */
+    int stream_depth;      /* streaming kernel: -1 by GEMM side; 0 the register-ring kernel;
+                              2, 3, 4 or 6 LDS ring slots */
+    void* stage_events[4]; /* hipEvent_t each, or NULL: the project-and-combine calls record
+                              them on `stream` before the mix, before the projection GEMM,
+                              before the combine and after it (the caller creates them) */
+} pcm_tuning;
+
+pcm_status pcm_expand_tuned(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                            const pcm_paths* paths, int64_t T, int H, int F, int n, int k, void* u,
+                            void* ws, size_t ws_bytes, void* stream, const pcm_tuning* tuning);
+pcm_status pcm_project_combine_tuned(pcm_dtype dtype, const void* u, const void* w_down,
+                                     const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
+                                     float* y, int accumulate, void* ws, size_t ws_bytes,
+                                     void* stream, const pcm_tuning* tuning);
+pcm_status pcm_dense_swiglu_tuned(pcm_dtype dtype, const void* x, const void* w_gate,
+                                  const void* w_up, const void* w_down, int64_t T, int H, int Fs,
+                                  float* y, int accumulate, void* ws, size_t ws_bytes, void* stream,
+                                  const pcm_tuning* tuning);
+pcm_status pcm_expand_scored_tuned(pcm_dtype dtype, const void* x, const void* w_gate,
+                                   const void* w_up, const pcm_scored_paths* paths, int64_t T,
+                                   int H, int F, int n, int K, void* u, void* ws, size_t ws_bytes,
+                                   void* stream, const pcm_tuning* tuning);
+pcm_status pcm_project_combine_scored_tuned(pcm_dtype dtype, const void* u, const void* w_down,
+                                            const pcm_scored_paths* paths, int64_t T, int H, int F,
+                                            int n, int K, float* y, int accumulate, void* ws,
+                                            size_t ws_bytes, void* stream,
+                                            const pcm_tuning* tuning);
+
+/* Where pcm_project_combine(_tuned) keeps its intermediates inside its workspace, so that a
+ * test can read them back after the call: the projection input z [T*k, F] (bf16 layers:
+ * float16 rows, each multiplied by a power of two; f32 layers: float32) at byte *z_off; the
+ * inverse of each z row's power of two [T*k] f32 at *zscale_off (bf16 layers; 0 otherwise);
+ * the projected rows o [ksplit, T*k, H] f32 at *o_off, K slice s of row r at (s*T*k + r)*H
+ * (the combine adds the slices in order). All outputs are host pointers. */
+pcm_status pcm_project_workspace_layout(pcm_dtype dtype, int64_t T, int H, int F, int n, int k,
+                                        const pcm_tuning* tuning, size_t* z_off,
+                                        size_t* zscale_off, size_t* o_off, int* ksplit);
 
 /* Device workspace bytes an operation needs (0 if none). Returns 0 for invalid sizes. */
 size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm_dtype dtype);

@@ -53,3 +53,30 @@ def decode_weight_bytes(touched_experts: int, H: int, F: int, elem: int,
                         shared_F: int = 0) -> int:
     """Weight bytes a layer must stream when each touched expert is read once."""
     return touched_experts * 3 * H * F * elem + (3 * H * shared_F * elem if shared_F else 0)
+
+
+# ------------------------------------------------------------ bytes of the memory-bound stages
+def route_bytes(T: int, n: int, k: int) -> int:
+    """Top-k of T logit rows: the logits in, ids and weights out."""
+    return T * n * 4 + T * k * 8
+
+
+def paths_bytes(T: int, n: int, k: int) -> int:
+    """Path table and dispatch layout: ids and weights in (and the n x n mask once); path bits,
+    weights beta, row_token / row_slot / row_of and the offsets out."""
+    return T * k * 8 + n * n + T * 8 + T * k * k * 4 + T * k * 12 + (n + 1) * 4
+
+
+def mix_bytes(R_src: int, R_tgt: int, F: int, T: int, K: int, u_elem: int = 4,
+              z_elem: int = 2) -> int:
+    """z_(t,b) = sum_a beta_ab u_(t,a): every U row in, every z row (and its scale) out, plus
+    the per-token bits, weights and row indices."""
+    return (R_src * F * u_elem + R_tgt * F * z_elem + (R_tgt * 4 if z_elem == 2 else 0)
+            + T * 8 + T * K * K * 4 + 2 * T * K * 4)
+
+
+def combine_bytes(R_tgt: int, H: int, T: int, K: int, ksplit: int = 1,
+                  accumulate: bool = False) -> int:
+    """y_t = [y_t] + sum_b o_(t,b): every o row of every K slice in, y out (and in when
+    accumulating), plus the row indices."""
+    return ksplit * R_tgt * H * 4 + T * H * 4 * (2 if accumulate else 1) + T * K * 4

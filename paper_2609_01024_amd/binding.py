@@ -8,10 +8,11 @@ not built, the first call raises RuntimeError.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
-from dataclasses import dataclass
-from typing import Optional
+from dataclasses import dataclass, field
+from typing import Optional, Sequence
 
 import torch
 
@@ -26,7 +27,37 @@ EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version",
            "pcm_path_layout_build", "pcm_route_scored", "pcm_expand_scored",
            "pcm_project_combine_scored", "pcm_layer_per_path", "pcm_route_logits",
-           "pcm_residual_add")
+           "pcm_residual_add", "pcm_expand_tuned", "pcm_project_combine_tuned",
+           "pcm_dense_swiglu_tuned", "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
+           "pcm_project_workspace_layout")
+
+
+class PcmTuning(ctypes.Structure):
+    _fields_ = [("tile", ctypes.c_int), ("order_expand", ctypes.c_int), ("order_down", ctypes.c_int),
+                ("em_window", ctypes.c_int), ("group_n", ctypes.c_int), ("stream_depth", ctypes.c_int),
+                ("stage_events", ctypes.c_void_p * 4)]
+
+
+@dataclass
+class Tuning:
+    """Kernel choices forced for tests and measurement (pcm_tuning); the defaults are the
+    library's own choices. stage_events: four torch.cuda.Event (created by a first record)
+    that the project-and-combine calls record before the mix, the projection GEMM, the combine
+    and after it."""
+    tile: str = ""              # "", "S", "M" or "L"
+    order_expand: int = -1
+    order_down: int = -1
+    em_window: int = 0
+    group_n: int = 0
+    stream_depth: int = -1
+    stage_events: Sequence = field(default_factory=tuple)
+
+    def struct(self) -> PcmTuning:
+        ev = [0, 0, 0, 0]
+        for i, e in enumerate(self.stage_events):
+            ev[i] = e.cuda_event
+        return PcmTuning(ord(self.tile) if self.tile else 0, self.order_expand, self.order_down,
+                         self.em_window, self.group_n, self.stream_depth, (ctypes.c_void_p * 4)(*ev))
 
 
 class PcmPaths(ctypes.Structure):
@@ -82,10 +113,20 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
     L.pcm_residual_add.argtypes = [I, P, P, I64, I, P]
     L.pcm_layer_per_path.argtypes = [I, P, P, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, I, P,
                                      I, P, SZ, P]
+    TP = ctypes.POINTER(PcmTuning)
+    for name in ("pcm_expand", "pcm_project_combine", "pcm_dense_swiglu", "pcm_expand_scored",
+                 "pcm_project_combine_scored"):
+        getattr(L, name + "_tuned").argtypes = getattr(L, name).argtypes + [TP]
+    SZP = ctypes.POINTER(SZ)
+    L.pcm_project_workspace_layout.argtypes = [I, I64, I, I, I, I, TP, SZP, SZP, SZP,
+                                               ctypes.POINTER(I)]
     for name in ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
                  "pcm_dense_swiglu", "pcm_abi_version", "pcm_path_layout_build",
                  "pcm_route_scored", "pcm_expand_scored", "pcm_project_combine_scored",
-                 "pcm_layer_per_path", "pcm_route_logits", "pcm_residual_add"):
+                 "pcm_layer_per_path", "pcm_route_logits", "pcm_residual_add",
+                 "pcm_expand_tuned", "pcm_project_combine_tuned", "pcm_dense_swiglu_tuned",
+                 "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
+                 "pcm_project_workspace_layout"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -103,6 +144,35 @@ def _ptr(t: Optional[torch.Tensor]):
 def _stream(stream: Optional[torch.cuda.Stream]):
     s = stream if stream is not None else torch.cuda.current_stream()
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def _on(stream: Optional[torch.cuda.Stream]):
+    """Context for allocating outputs and workspaces: on `stream` when one is given, so that the
+    caching allocator orders their reuse after the kernels enqueued there."""
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+
+
+def _call(name: str, args: list, tuning):
+    """The plain entry point, or its *_tuned form with the tuning (a Tuning, or a PcmTuning
+    built beforehand) appended."""
+    if tuning is None:
+        return getattr(lib(), name)(*args)
+    t = tuning if isinstance(tuning, PcmTuning) else tuning.struct()
+    return getattr(lib(), name + "_tuned")(*args, ctypes.byref(t))
+
+
+def project_workspace_layout(T: int, H: int, F: int, n: int, k: int, dtype: int,
+                             tuning: Optional[Tuning] = None) -> dict:
+    """Byte offsets of z, its row scales and o inside pcm_project_combine's workspace, and the
+    number of K slices of o (pcm_project_workspace_layout)."""
+    z, zs, o = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    ks = ctypes.c_int()
+    t = tuning.struct() if tuning is not None else None
+    _check(lib().pcm_project_workspace_layout(dtype, T, H, F, n, k,
+                                              ctypes.byref(t) if t is not None else None,
+                                              ctypes.byref(z), ctypes.byref(zs), ctypes.byref(o),
+                                              ctypes.byref(ks)))
+    return {"z": z.value, "zscale": zs.value, "o": o.value, "ksplit": ks.value}
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -131,8 +201,9 @@ def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
 def pcm_route(logits: torch.Tensor, k: int, topk_ids=None, topk_w=None, stream=None):
     _dev(logits)
     T, n = logits.shape
-    ids = topk_ids if topk_ids is not None else torch.empty((T, k), dtype=torch.int32, device=logits.device)
-    w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=logits.device)
+    with _on(stream):
+        ids = topk_ids if topk_ids is not None else torch.empty((T, k), dtype=torch.int32, device=logits.device)
+        w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=logits.device)
     _dev(ids, w)
     _check(lib().pcm_route(_ptr(logits), T, n, k, _ptr(ids), _ptr(w), _stream(stream)))
     return ids, w
@@ -145,14 +216,15 @@ def pcm_route_logits(x, w_router, k: int, logits=None, topk_ids=None, topk_w=Non
     T, H = x.shape
     n = w_router.shape[0]
     dev = x.device
-    ids = topk_ids if topk_ids is not None else torch.empty((T, k), dtype=torch.int32, device=dev)
-    w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=dev)
-    if want_logits and logits is None:
-        logits = torch.empty((T, n), dtype=torch.float32, device=dev)
-    _dev(ids, w, logits)
     dt = _dtype_code(x)
-    if ws is None:
-        ws = _workspace(workspace_bytes(OP_ROUTE_LOGITS, T, H, 0, n, k, dt), dev)
+    with _on(stream):
+        ids = topk_ids if topk_ids is not None else torch.empty((T, k), dtype=torch.int32, device=dev)
+        w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=dev)
+        if want_logits and logits is None:
+            logits = torch.empty((T, n), dtype=torch.float32, device=dev)
+        if ws is None:
+            ws = _workspace(workspace_bytes(OP_ROUTE_LOGITS, T, H, 0, n, k, dt), dev)
+    _dev(ids, w, logits)
     _check(lib().pcm_route_logits(dt, _ptr(x), _ptr(w_router), T, H, n, k, _ptr(logits), _ptr(ids),
                                   _ptr(w), _ptr(ws), ws.numel() if ws is not None else 0,
                                   _stream(stream)))
@@ -198,10 +270,11 @@ def pcm_build_paths(topk_ids, topk_w, mask, beta_mode: int = BETA_SRC_COND, out:
     _dev(topk_ids, topk_w, mask)
     T, k = topk_ids.shape
     n = mask.shape[0]
-    out = out or PathTable.empty(T, n, k, topk_ids.device)
     need = workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0)
-    if ws is None:
-        ws = _workspace(need, topk_ids.device)
+    with _on(stream):
+        out = out or PathTable.empty(T, n, k, topk_ids.device)
+        if ws is None:
+            ws = _workspace(need, topk_ids.device)
     st = out.struct()
     _check(lib().pcm_build_paths(_ptr(topk_ids), _ptr(topk_w), _ptr(mask), T, n, k, beta_mode,
                                  ctypes.byref(st), _ptr(ws), ws.numel() if ws is not None else 0,
@@ -209,45 +282,52 @@ def pcm_build_paths(topk_ids, topk_w, mask, beta_mode: int = BETA_SRC_COND, out:
     return out
 
 
-def pcm_expand(x, w_gate, w_up, paths: PathTable, u=None, stream=None) -> torch.Tensor:
+def pcm_expand(x, w_gate, w_up, paths: PathTable, u=None, stream=None,
+               tuning: Optional[Tuning] = None) -> torch.Tensor:
     _dev(x, w_gate, w_up, u)
     T, H = x.shape
     n, F, _ = w_gate.shape
-    u = u if u is not None else torch.empty((T * paths.k, F), dtype=torch.float32, device=x.device)
+    with _on(stream):
+        u = u if u is not None else torch.empty((T * paths.k, F), dtype=torch.float32, device=x.device)
     st = paths.struct()
-    _check(lib().pcm_expand(_dtype_code(x), _ptr(x), _ptr(w_gate), _ptr(w_up), ctypes.byref(st), T, H,
-                            F, n, paths.k, _ptr(u), None, 0, _stream(stream)))
+    _check(_call("pcm_expand", [_dtype_code(x), _ptr(x), _ptr(w_gate), _ptr(w_up), ctypes.byref(st),
+                                T, H, F, n, paths.k, _ptr(u), None, 0, _stream(stream)], tuning))
     return u
 
 
 def pcm_project_combine(u, w_down, paths: PathTable, y=None, accumulate: bool = False,
-                        ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+                        ws: torch.Tensor = None, stream=None,
+                        tuning: Optional[Tuning] = None) -> torch.Tensor:
     _dev(u, w_down, y)
     n, H, F = w_down.shape
     T, k = paths.T, paths.k
-    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
     dt = _dtype_code(w_down)
-    if ws is None:
-        ws = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), u.device)
+    with _on(stream):
+        y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
+        if ws is None:
+            ws = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), u.device)
     st = paths.struct()
-    _check(lib().pcm_project_combine(dt, _ptr(u), _ptr(w_down), ctypes.byref(st), T, H, F, n, k,
-                                     _ptr(y), int(bool(accumulate)), _ptr(ws),
-                                     ws.numel() if ws is not None else 0, _stream(stream)))
+    _check(_call("pcm_project_combine", [dt, _ptr(u), _ptr(w_down), ctypes.byref(st), T, H, F, n, k,
+                                         _ptr(y), int(bool(accumulate)), _ptr(ws),
+                                         ws.numel() if ws is not None else 0, _stream(stream)],
+                 tuning))
     return y
 
 
 def pcm_dense_swiglu(x, w_gate, w_up, w_down, y=None, accumulate: bool = False,
-                     ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+                     ws: torch.Tensor = None, stream=None,
+                     tuning: Optional[Tuning] = None) -> torch.Tensor:
     _dev(x, w_gate, w_up, w_down, y)
     T, H = x.shape
     Fs = w_gate.shape[0]
-    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
     dt = _dtype_code(x)
-    if ws is None:
-        ws = _workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, Fs, 1, 1, dt), x.device)
-    _check(lib().pcm_dense_swiglu(dt, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down), T, H, Fs,
-                                  _ptr(y), int(bool(accumulate)), _ptr(ws),
-                                  ws.numel() if ws is not None else 0, _stream(stream)))
+    with _on(stream):
+        y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
+        if ws is None:
+            ws = _workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, Fs, 1, 1, dt), x.device)
+    _check(_call("pcm_dense_swiglu", [dt, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down), T, H, Fs,
+                                      _ptr(y), int(bool(accumulate)), _ptr(ws),
+                                      ws.numel() if ws is not None else 0, _stream(stream)], tuning))
     return y
 
 
@@ -259,10 +339,11 @@ def pcm_layer_per_path(x, w_gate, w_up, w_down, paths: PathTable, reuse: bool = 
     T, H = x.shape
     n, F, _ = w_gate.shape
     k = paths.k
-    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
     dt = _dtype_code(x)
-    if ws is None:
-        ws = _workspace(workspace_bytes(OP_LAYER_PER_PATH, T, H, F, n, k, dt), x.device)
+    with _on(stream):
+        y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
+        if ws is None:
+            ws = _workspace(workspace_bytes(OP_LAYER_PER_PATH, T, H, F, n, k, dt), x.device)
     st = paths.struct()
     _check(lib().pcm_layer_per_path(dt, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down),
                                     ctypes.byref(st), T, H, F, n, k, int(bool(reuse)), _ptr(y),
@@ -295,7 +376,8 @@ def pcm_path_layout_build(mask, bias, out: PathLayout = None, stream=None) -> Pa
     n = mask.shape[0]
     if bias.dtype != torch.float32 or bias.shape != (n, n) or mask.dtype != torch.uint8:
         raise TypeError("mask [n,n] uint8 and bias [n,n] float32")
-    out = out or PathLayout.empty(n, mask.device)
+    with _on(stream):
+        out = out or PathLayout.empty(n, mask.device)
     st = out.struct()
     _check(lib().pcm_path_layout_build(_ptr(mask), _ptr(bias), n, ctypes.byref(st), _stream(stream)))
     return out
@@ -342,9 +424,10 @@ def pcm_route_scored(g_base, g_tgt, lam: float, layout: PathLayout, K: int,
                      stream=None) -> ScoredPathTable:
     _dev(g_base, g_tgt)
     T, n = g_base.shape
-    out = out or ScoredPathTable.empty(T, n, K, g_base.device)
-    if ws is None:
-        ws = _workspace(workspace_bytes(OP_ROUTE_SCORED, T, 0, 0, n, K, 0), g_base.device)
+    with _on(stream):
+        out = out or ScoredPathTable.empty(T, n, K, g_base.device)
+        if ws is None:
+            ws = _workspace(workspace_bytes(OP_ROUTE_SCORED, T, 0, 0, n, K, 0), g_base.device)
     lst, st = layout.struct(), out.struct()
     _check(lib().pcm_route_scored(_ptr(g_base), _ptr(g_tgt), float(lam), ctypes.byref(lst), T, n, K,
                                   ctypes.byref(st), _ptr(ws), ws.numel() if ws is not None else 0,
@@ -352,30 +435,36 @@ def pcm_route_scored(g_base, g_tgt, lam: float, layout: PathLayout, K: int,
     return out
 
 
-def pcm_expand_scored(x, w_gate, w_up, paths: ScoredPathTable, u=None, stream=None) -> torch.Tensor:
+def pcm_expand_scored(x, w_gate, w_up, paths: ScoredPathTable, u=None, stream=None,
+                      tuning: Optional[Tuning] = None) -> torch.Tensor:
     _dev(x, w_gate, w_up, u)
     T, H = x.shape
     n, F, _ = w_gate.shape
-    u = u if u is not None else torch.empty((T * paths.K, F), dtype=torch.float32, device=x.device)
+    with _on(stream):
+        u = u if u is not None else torch.empty((T * paths.K, F), dtype=torch.float32, device=x.device)
     st = paths.struct()
-    _check(lib().pcm_expand_scored(_dtype_code(x), _ptr(x), _ptr(w_gate), _ptr(w_up), ctypes.byref(st),
-                                   T, H, F, n, paths.K, _ptr(u), None, 0, _stream(stream)))
+    _check(_call("pcm_expand_scored", [_dtype_code(x), _ptr(x), _ptr(w_gate), _ptr(w_up),
+                                       ctypes.byref(st), T, H, F, n, paths.K, _ptr(u), None, 0,
+                                       _stream(stream)], tuning))
     return u
 
 
 def pcm_project_combine_scored(u, w_down, paths: ScoredPathTable, y=None, accumulate: bool = False,
-                               ws: torch.Tensor = None, stream=None) -> torch.Tensor:
+                               ws: torch.Tensor = None, stream=None,
+                               tuning: Optional[Tuning] = None) -> torch.Tensor:
     _dev(u, w_down, y)
     n, H, F = w_down.shape
     T, K = paths.T, paths.K
-    y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
     dt = _dtype_code(w_down)
-    if ws is None:
-        ws = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, K, dt), u.device)
+    with _on(stream):
+        y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
+        if ws is None:
+            ws = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, K, dt), u.device)
     st = paths.struct()
-    _check(lib().pcm_project_combine_scored(dt, _ptr(u), _ptr(w_down), ctypes.byref(st), T, H, F, n,
-                                            K, _ptr(y), int(bool(accumulate)), _ptr(ws),
-                                            ws.numel() if ws is not None else 0, _stream(stream)))
+    _check(_call("pcm_project_combine_scored", [dt, _ptr(u), _ptr(w_down), ctypes.byref(st), T, H, F,
+                                                n, K, _ptr(y), int(bool(accumulate)), _ptr(ws),
+                                                ws.numel() if ws is not None else 0,
+                                                _stream(stream)], tuning))
     return y
 
 
@@ -398,16 +487,18 @@ class ScoredLayerPlan:
     def build_layout(self, mask, bias, stream=None):
         pcm_path_layout_build(mask, bias, out=self.layout, stream=stream)
 
-    def forward(self, x, g_base, g_tgt, lam, w_gate, w_up, w_down, shared=None, stream=None):
+    def forward(self, x, g_base, g_tgt, lam, w_gate, w_up, w_down, shared=None, stream=None,
+                tuning: Optional[Tuning] = None):
         # the shared expert first, storing y; the combine then adds the routed sum to it
         # (y_t = shared_t + routed_t either way, the same two float32 operands)
         if shared is not None:
-            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=False, ws=self.ws_shared, stream=stream)
+            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=False, ws=self.ws_shared, stream=stream,
+                             tuning=tuning)
         pcm_route_scored(g_base, g_tgt, lam, self.layout, self.K, out=self.paths, ws=self.ws_route,
                          stream=stream)
-        pcm_expand_scored(x, w_gate, w_up, self.paths, u=self.u, stream=stream)
+        pcm_expand_scored(x, w_gate, w_up, self.paths, u=self.u, stream=stream, tuning=tuning)
         pcm_project_combine_scored(self.u, w_down, self.paths, y=self.y, accumulate=shared is not None,
-                                   ws=self.ws_proj, stream=stream)
+                                   ws=self.ws_proj, stream=stream, tuning=tuning)
         return self.y
 
 
@@ -430,25 +521,29 @@ class LayerPlan:
                           if shared_F else None)
         self.y = torch.empty((T, H), dtype=torch.float32, device=device)
 
-    def forward(self, x, logits, mask, w_gate, w_up, w_down, shared=None, stream=None):
+    def forward(self, x, logits, mask, w_gate, w_up, w_down, shared=None, stream=None,
+                tuning: Optional[Tuning] = None):
         # the shared expert first, storing y (its projection's epilogue then has no y to read);
         # the combine adds the routed sum: y_t = shared_t + routed_t, the same two float32
         # operands as accumulating the shared expert last
         if shared is not None:
-            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=False, ws=self.ws_shared, stream=stream)
+            pcm_dense_swiglu(x, *shared, y=self.y, accumulate=False, ws=self.ws_shared, stream=stream,
+                             tuning=tuning)
         pcm_route(logits, self.k, self.ids, self.w, stream=stream)
         pcm_build_paths(self.ids, self.w, mask, self.beta_mode, out=self.paths, ws=self.ws_paths,
                         stream=stream)
-        pcm_expand(x, w_gate, w_up, self.paths, u=self.u, stream=stream)
+        pcm_expand(x, w_gate, w_up, self.paths, u=self.u, stream=stream, tuning=tuning)
         pcm_project_combine(self.u, w_down, self.paths, y=self.y, accumulate=shared is not None,
-                            ws=self.ws_proj, stream=stream)
+                            ws=self.ws_proj, stream=stream, tuning=tuning)
         return self.y
 
 
 def layer_forward(x, logits, mask, w_gate, w_up, w_down, k: int, beta_mode: int = BETA_SRC_COND,
-                  shared=None, stream=None) -> torch.Tensor:
+                  shared=None, stream=None, tuning: Optional[Tuning] = None) -> torch.Tensor:
     """One layer: route, build paths, expand, project and combine (+ shared expert)."""
     T, H = x.shape
     n, F, _ = w_gate.shape
-    plan = LayerPlan(T, H, F, n, k, x.dtype, x.device, shared[0].shape[0] if shared else 0, beta_mode)
-    return plan.forward(x, logits, mask, w_gate, w_up, w_down, shared, stream)
+    with _on(stream):
+        plan = LayerPlan(T, H, F, n, k, x.dtype, x.device, shared[0].shape[0] if shared else 0,
+                         beta_mode)
+    return plan.forward(x, logits, mask, w_gate, w_up, w_down, shared, stream, tuning)

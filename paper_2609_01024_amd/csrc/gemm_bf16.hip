@@ -50,9 +50,6 @@
 // a K-split projection lists each XCD's full-height tiles before its 128-row tail tiles
 // (il_item); one group of rows (the dense shared expert) and the medium tiles use the
 // grouped order of tile_of.
-#include <stdlib.h>
-#include <string.h>
-
 #include <type_traits>
 
 #include "internal.h"
@@ -1206,13 +1203,10 @@ hipError_t launch_lstream_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     const int nt = (int)ceil_div(g.N, kWgCols);
     const int64_t grid = mt_upper * nt;
     if (grid <= 0) return hipSuccess;
-    static bool attr_set = false;  // idempotent; a race only repeats the same call
-    if (!attr_set) {
-        const hipError_t err = hipFuncSetAttribute((const void*)gemm_lstream_kernel<MODE, NB, D>,
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
-        if (err != hipSuccess) return err;
-        attr_set = true;
-    }
+    // set on every launch (idempotent, and the library keeps no state between calls)
+    const hipError_t err = hipFuncSetAttribute((const void*)gemm_lstream_kernel<MODE, NB, D>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+    if (err != hipSuccess) return err;
     const int n_fastest = MODE == kExpand ? 1 : 0;
     gemm_lstream_kernel<MODE, NB, D><<<dim3((unsigned)grid), dim3(SWAVES * 64), kLds, s>>>(g, mt_upper, nt, n_fastest);
     return hipGetLastError();
@@ -1236,15 +1230,14 @@ hipError_t launch_stream_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
 // Register-ring kernel: two 16-row blocks per wave, eight k-steps in flight (four or six
 // blocks, or six steps, measured 1-3% slower on the decode-shaped layer).
 template <int MODE>
-hipError_t launch_stream(const GemmArgs& g, int64_t R, hipStream_t s) {
+hipError_t launch_stream(const GemmArgs& g, int64_t R, hipStream_t s, int depth) {
     // the LDS-ring kernel (whole-line weight loads) where its constraints hold; ring depth 3
     // for the expansion and 2 for the projection (decode-shaped layer: 2-6 within 0.5% for the
     // expansion; the projection 3% slower at 3 and 45% at 4, where the compiler waits for every
     // load in flight before the fragment reads and only one workgroup fits a compute unit);
-    // PCM_LSTREAM_D overrides the depth (0: the register-ring kernel), for tests and tuning
+    // a forced depth of 0 runs the register-ring kernel
     if (g.K % 64 == 0 && g.a_rows * g.K * 2 < (int64_t(1) << 32) && (int64_t)g.N * g.K * 2 < (int64_t(1) << 32)) {
-        const char* d = getenv("PCM_LSTREAM_D");
-        const int dv = d ? atoi(d) : (MODE == kExpand ? 3 : 2);
+        const int dv = depth >= 0 ? depth : (MODE == kExpand ? 3 : 2);
         if (dv == 2) return launch_lstream_cfg<MODE, 2, 2>(g, R, s);
         if (dv == 4) return launch_lstream_cfg<MODE, 2, 4>(g, R, s);
         if (dv == 6) return launch_lstream_cfg<MODE, 2, 6>(g, R, s);
@@ -1255,36 +1248,24 @@ hipError_t launch_stream(const GemmArgs& g, int64_t R, hipStream_t s) {
 
 // ---------------------------------------------------------------------- launch
 template <class C, int MODE, bool IL>
-hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
-    // work order of the large tiles, for tests and tuning (read on every call, like
-    // PCM_GEMM_TILE): PCM_GEMM_ORDER_EXPAND / PCM_GEMM_ORDER_DOWN = 0 grouped, 1 longest
-    // first, 2 expert-major; PCM_GEMM_EM_WINDOW sets the expert-major window
-    const char* order_s = getenv(MODE == kExpand ? "PCM_GEMM_ORDER_EXPAND" : "PCM_GEMM_ORDER_DOWN");
-    const int order_env = order_s ? atoi(order_s) : -1;
-    static bool attr_set = false;  // idempotent; a race only repeats the same call
-    if (!attr_set) {
-        const void* fn;
-        if constexpr (IL)
-            fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE>;
-        else
-            fn = (const void*)gemm_staged_kernel<C, MODE>;
-        const hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-        if (err != hipSuccess) return err;
-        attr_set = true;
-    }
+hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s, const GemmTune& t) {
+    // set on every launch (idempotent, and the library keeps no state between calls)
+    const void* fn;
+    if constexpr (IL)
+        fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE>;
+    else
+        fn = (const void*)gemm_staged_kernel<C, MODE>;
+    const hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+    if (err != hipSuccess) return err;
     const int64_t mt_upper = g.offsets ? ceil_div(R, C::BM) + g.n : ceil_div(R, C::BM);
     constexpr int kOutCols = (MODE == kExpand) ? C::BNB / 2 : C::BNB;
     const int nt = (int)ceil_div(g.N, kOutCols);
     if (mt_upper * nt <= 0) return hipSuccess;
-    static const int group_n = [] {
-        const char* env = getenv("PCM_GEMM_GROUP_N");
-        const int v = env ? atoi(env) : 4;
-        return v > 0 ? v : 4;
-    }();
+    const int group_n = t.group_n > 0 ? t.group_n : 4;
     if constexpr (IL) {
         // default: expert-major for grouped rows (the projection's K-split launches keep the
         // longest-first order, one group of rows the orders tuned for it)
-        int order = order_env;
+        int order = t.order;
         if (order < 0 || order > 2) {
             if (g.offsets == nullptr) order = MODE == kExpand ? kGrouped : kLongestFirst;
             else order = (MODE != kExpand && g.ksplit > 1) ? kLongestFirst : kExpertMajor;
@@ -1302,10 +1283,8 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
             // each XCD's run holds at most ceil(items / 8) <= ceil(mt_upper * nt * ksplit / 8)
             // window 8: with three weight stages 0.2-1.1% ahead of 12, 16 and 24 on the three
             // grouped workloads (12 was best with two)
-            const char* win_s = getenv("PCM_GEMM_EM_WINDOW");
-            const int window = win_s ? atoi(win_s) : 8;
             grid = ceil_div(mt_upper * nt * g.ksplit, 8) * 8;
-            gparam = window > 0 ? window : 8;
+            gparam = t.window > 0 ? t.window : 8;
         } else {
             grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
         }
@@ -1318,15 +1297,13 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Tile shape: an environment override (PCM_GEMM_TILE = S | M | L) for tests and tuning,
-// otherwise by the mean rows per group (below 16 the streaming kernel, else the large tiles).
-// The large tiles address `a` and one group's weights through 32-bit buffer offsets, so
-// both must stay below 4 GiB (a_bytes: all rows of `a`; w_bytes: one group's weights).
-char pick_tile(int64_t R, int groups, int64_t a_bytes, int64_t w_bytes) {
+// Tile shape: a forced choice (tile = 'S', 'M' or 'L', for tests and tuning), otherwise by the
+// mean rows per group (below 16 the streaming kernel, else the large tiles). The large tiles
+// address `a` and one group's weights through 32-bit buffer offsets, so both must stay below
+// 4 GiB (a_bytes: all rows of `a`; w_bytes: one group's weights).
+char pick_tile(int64_t R, int groups, int64_t a_bytes, int64_t w_bytes, char tile) {
     const bool large_ok = a_bytes < (int64_t(1) << 32) && w_bytes < (int64_t(1) << 32);
-    const char* env = getenv("PCM_GEMM_TILE");
-    if (env && (env[0] == 'S' || env[0] == 'M' || env[0] == 'L'))
-        return env[0] == 'L' && !large_ok ? 'M' : env[0];
+    if (tile == 'S' || tile == 'M' || tile == 'L') return tile == 'L' && !large_ok ? 'M' : tile;
     // below 16 rows per group the streaming kernel (weights streamed once, little MFMA work
     // wasted on padding); from 16 on the large tiles, which were faster than the medium ones
     // at every size measured (Mixtral-shaped, 1024 tokens: 2.6 -> 0.87 ms for the two GEMMs
@@ -1339,31 +1316,32 @@ char pick_tile(int64_t R, int groups, int64_t a_bytes, int64_t w_bytes) {
 
 }  // namespace
 
-int down_ksplit(int64_t R, int n, int H, int F) {
+int down_ksplit(int64_t R, int n, int H, int F, char tile) {
     // only the large-tile kernel slices K; its grid is (R/256 + n) x (H/256) tiles
-    if (pick_tile(R, n, R * F * 2, (int64_t)H * F * 2) != 'L') return 1;
+    if (pick_tile(R, n, R * F * 2, (int64_t)H * F * 2, tile) != 'L') return 1;
     const int64_t tiles = (ceil_div(R, 256) + n) * ceil_div(H, 256);
     return (tiles < 4 * 256 && (F / 2) % 64 == 0 && F / 32 >= 128) ? 2 : 1;
 }
 
-hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStream_t s) {
+hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStream_t s,
+                            const GemmTune& tune) {
     GemmArgs g = g0;
     if (g.ksplit < 1) g.ksplit = 1;
-    const char t = pick_tile(R, g.offsets ? g.n : 1, g.a_rows * g.K * 2, (int64_t)g.N * g.K * 2);
+    const char t = pick_tile(R, g.offsets ? g.n : 1, g.a_rows * g.K * 2, (int64_t)g.N * g.K * 2, tune.tile);
     if (g.ksplit > 1 && (mode != kDownStore || t != 'L')) return hipErrorInvalidValue;
     switch (mode) {
         case kExpand:
-            if (t == 'S') return launch_stream<kExpand>(g, R, s);
-            if (t == 'M') return launch_cfg<MediumStaged, kExpand, false>(g, R, s);
-            return launch_cfg<LargeIl, kExpand, true>(g, R, s);
+            if (t == 'S') return launch_stream<kExpand>(g, R, s, tune.stream_depth);
+            if (t == 'M') return launch_cfg<MediumStaged, kExpand, false>(g, R, s, tune);
+            return launch_cfg<LargeIl, kExpand, true>(g, R, s, tune);
         case kDownStore:
-            if (t == 'S') return launch_stream<kDownStore>(g, R, s);
-            if (t == 'M') return launch_cfg<MediumStaged, kDownStore, false>(g, R, s);
-            return launch_cfg<LargeIl, kDownStore, true>(g, R, s);
+            if (t == 'S') return launch_stream<kDownStore>(g, R, s, tune.stream_depth);
+            if (t == 'M') return launch_cfg<MediumStaged, kDownStore, false>(g, R, s, tune);
+            return launch_cfg<LargeIl, kDownStore, true>(g, R, s, tune);
         default:
-            if (t == 'S') return launch_stream<kDownAccum>(g, R, s);
-            if (t == 'M') return launch_cfg<MediumStaged, kDownAccum, false>(g, R, s);
-            return launch_cfg<LargeIl, kDownAccum, true>(g, R, s);
+            if (t == 'S') return launch_stream<kDownAccum>(g, R, s, tune.stream_depth);
+            if (t == 'M') return launch_cfg<MediumStaged, kDownAccum, false>(g, R, s, tune);
+            return launch_cfg<LargeIl, kDownAccum, true>(g, R, s, tune);
     }
 }
 

@@ -69,11 +69,23 @@ struct GemmArgs {
     int64_t rows_total;         // rows of `out` per slice (down-store with ksplit > 1)
 };
 
-// Number of K slices the projection of R rows uses (1 or 2): split when the output tiles
-// alone would leave the chip's 256 compute units idle for much of the last round.
-int down_ksplit(int64_t R, int n, int H, int F);
+// Kernel choices of a bf16 GEMM launch that a caller may force (tests and measurement, through
+// the *_tuned entry points). The defaults choose by shape; every choice gives the same bits.
+struct GemmTune {
+    char tile = 0;          // 0: by mean rows per group; 'S' streaming, 'M' medium, 'L' large tiles
+    int order = -1;         // large tiles: -1 by shape; 0 grouped, 1 longest first, 2 expert-major
+    int window = 0;         // expert-major window (0: 8)
+    int group_n = 0;        // N tiles per group of the grouped order (0: 4)
+    int stream_depth = -1;  // streaming kernel: -1 by mode; 0 register ring; 2, 3, 4, 6 LDS slots
+};
 
-hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
+// Number of K slices the projection of R rows uses (1 or 2): split when the output tiles
+// alone would leave the chip's 256 compute units idle for much of the last round. `tile` is
+// a forced tile kernel (GemmTune::tile) or 0.
+int down_ksplit(int64_t R, int n, int H, int F, char tile);
+
+hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s,
+                            const GemmTune& tune);
 hipError_t launch_gemm_f32(GemmMode mode, const GemmArgs& g, int64_t R, hipStream_t s);
 
 // Per-token path structure read by the mix and the combine. Token t has n_src[t] source

@@ -47,6 +47,31 @@ pcm_status check_layout(const pcm_path_layout* l) {
     return PCM_OK;
 }
 
+// The kernel choices of a pcm_tuning (NULL: every default) for the expansion or the
+// projection side; PCM_ERR_ARG for a value outside the documented set.
+pcm_status to_tune(const pcm_tuning* t, bool expansion, GemmTune* out) {
+    *out = GemmTune();
+    if (!t) return PCM_OK;
+    if (t->tile != 0 && t->tile != 'S' && t->tile != 'M' && t->tile != 'L') return PCM_ERR_ARG;
+    if (t->order_expand < -1 || t->order_expand > 2 || t->order_down < -1 || t->order_down > 2)
+        return PCM_ERR_ARG;
+    if (t->em_window < 0 || t->group_n < 0) return PCM_ERR_ARG;
+    const int d = t->stream_depth;
+    if (d != -1 && d != 0 && d != 2 && d != 3 && d != 4 && d != 6) return PCM_ERR_ARG;
+    out->tile = (char)t->tile;
+    out->order = expansion ? t->order_expand : t->order_down;
+    out->window = t->em_window;
+    out->group_n = t->group_n;
+    out->stream_depth = d;
+    return PCM_OK;
+}
+
+// Records stage event i of a tuning (if any) on the stream.
+hipError_t stage_event(const pcm_tuning* t, int i, hipStream_t s) {
+    if (!t || !t->stage_events[i]) return hipSuccess;
+    return hipEventRecord((hipEvent_t)t->stage_events[i], s);
+}
+
 // Workspace of the projection of R rows of n groups: z [R,F] (f16 for bf16 layers, f32
 // otherwise), the per-row inverse scales [R] f32 (bf16 layers), then, when `with_o`, the
 // projected rows o [ksplit, R, H] f32 (K slices of the projection); parts 256-byte aligned.
@@ -54,9 +79,9 @@ struct ProjWs {
     size_t zscale_off, o_off, total;
     int ksplit;
 };
-ProjWs proj_ws(size_t R, int n, int H, int F, pcm_dtype dt, bool with_o) {
+ProjWs proj_ws(size_t R, int n, int H, int F, pcm_dtype dt, bool with_o, char tile = 0) {
     ProjWs w;
-    w.ksplit = (with_o && dt == PCM_BF16) ? down_ksplit((int64_t)R, n, H, F) : 1;
+    w.ksplit = (with_o && dt == PCM_BF16) ? down_ksplit((int64_t)R, n, H, F, tile) : 1;
     const size_t z = align_up(R * F * (dt == PCM_BF16 ? 2 : 4), 256);
     w.zscale_off = z;
     w.o_off = z + (dt == PCM_BF16 ? align_up(R * sizeof(float), 256) : 0);
@@ -96,7 +121,7 @@ PathWs path_ws(int64_t T, int H, int F, int n, int k, pcm_dtype dt) {
 
 extern "C" {
 
-int pcm_abi_version(void) { return 110; }
+int pcm_abi_version(void) { return 120; }
 
 const char* pcm_status_string(pcm_status s) {
     switch (s) {
@@ -181,23 +206,30 @@ pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const u
     if (beta_mode < PCM_BETA_SRC_COND || beta_mode > PCM_BETA_GLOBAL) return PCM_ERR_ARG;
     if (T == 0) return PCM_OK;
     if (!topk_ids || !topk_w || !mask || check_paths(out) != PCM_OK) return PCM_ERR_ARG;
+    if (!aligned16(topk_ids) || !aligned16(topk_w) || !aligned16(mask) ||
+        !aligned16(out->path_bits) || !aligned16(out->beta) || !aligned16(out->expert_offsets) ||
+        !aligned16(out->row_token) || !aligned16(out->row_slot) || !aligned16(out->row_of))
+        return PCM_ERR_ARG;
     const size_t need = build_paths_ws_bytes(T, n);
     if (ws_bytes < need || (need && !ws)) return PCM_ERR_WORKSPACE;
+    if (need && !aligned16(ws)) return PCM_ERR_ARG;
     return from_hip(launch_build_paths(topk_ids, topk_w, mask, T, n, k, (int)beta_mode,
                                        out->path_bits, out->beta, out->expert_offsets,
                                        out->row_token, out->row_slot, out->row_of, (int32_t*)ws,
                                        (hipStream_t)stream));
 }
 
-pcm_status pcm_expand(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
-                      const pcm_paths* paths, int64_t T, int H, int F, int n, int k, void* u,
-                      void* ws, size_t ws_bytes, void* stream) {
+pcm_status pcm_expand_tuned(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                            const pcm_paths* paths, int64_t T, int H, int F, int n, int k, void* u,
+                            void* ws, size_t ws_bytes, void* stream, const pcm_tuning* tuning) {
     (void)ws;
     (void)ws_bytes;
     pcm_status st = check_shape(T, n, k);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
     if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    GemmTune tune;
+    if ((st = to_tune(tuning, true, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
     if (!x || !w_gate || !w_up || !u || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
     if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(u)) return PCM_ERR_ARG;
@@ -214,22 +246,32 @@ pcm_status pcm_expand(pcm_dtype dtype, const void* x, const void* w_gate, const 
     g.N = F;
     const int64_t R = T * k;
     hipStream_t s = (hipStream_t)stream;
-    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s)
+    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s, tune)
                                       : launch_gemm_f32(kExpand, g, R, s));
 }
 
-pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_down,
-                               const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
-                               float* y, int accumulate, void* ws, size_t ws_bytes, void* stream) {
+pcm_status pcm_expand(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                      const pcm_paths* paths, int64_t T, int H, int F, int n, int k, void* u,
+                      void* ws, size_t ws_bytes, void* stream) {
+    return pcm_expand_tuned(dtype, x, w_gate, w_up, paths, T, H, F, n, k, u, ws, ws_bytes, stream,
+                            nullptr);
+}
+
+pcm_status pcm_project_combine_tuned(pcm_dtype dtype, const void* u, const void* w_down,
+                                     const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
+                                     float* y, int accumulate, void* ws, size_t ws_bytes,
+                                     void* stream, const pcm_tuning* tuning) {
     pcm_status st = check_shape(T, n, k);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
     if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    GemmTune tune;
+    if ((st = to_tune(tuning, false, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
     if (!u || !w_down || !y || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
     if (!aligned16(u) || !aligned16(w_down) || !aligned16(y)) return PCM_ERR_ARG;
     const int64_t R = T * k;
-    const ProjWs w = proj_ws((size_t)R, n, H, F, dtype, true);
+    const ProjWs w = proj_ws((size_t)R, n, H, F, dtype, true, tune.tile);
     if (!ws || ws_bytes < w.total) return PCM_ERR_WORKSPACE;
     if (!aligned16(ws)) return PCM_ERR_ARG;
     void* z = ws;
@@ -243,7 +285,9 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
     m.src_row = m.tgt_row = paths->row_of;
     m.K = k;
     m.R_src = m.R_tgt = R;
-    hipError_t e = launch_mix((const float*)u, z, zscale, m, T, F, s);
+    hipError_t e = stage_event(tuning, 0, s);
+    if (e == hipSuccess) e = launch_mix((const float*)u, z, zscale, m, T, F, s);
+    if (e == hipSuccess) e = stage_event(tuning, 1, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     GemmArgs g{};
     g.a = z;
@@ -257,18 +301,50 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
     g.N = H;
     g.ksplit = w.ksplit;
     g.rows_total = R;
-    e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s) : launch_gemm_f32(kDownStore, g, R, s);
+    e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s, tune) : launch_gemm_f32(kDownStore, g, R, s);
+    if (e == hipSuccess) e = stage_event(tuning, 2, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
-    return from_hip(launch_combine(o, w.ksplit, m, T, H, y, accumulate, s));
+    e = launch_combine(o, w.ksplit, m, T, H, y, accumulate, s);
+    if (e == hipSuccess) e = stage_event(tuning, 3, s);
+    return from_hip(e);
 }
 
-pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
-                            const void* w_down, int64_t T, int H, int Fs, float* y, int accumulate,
-                            void* ws, size_t ws_bytes, void* stream) {
+pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_down,
+                               const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
+                               float* y, int accumulate, void* ws, size_t ws_bytes, void* stream) {
+    return pcm_project_combine_tuned(dtype, u, w_down, paths, T, H, F, n, k, y, accumulate, ws,
+                                     ws_bytes, stream, nullptr);
+}
+
+pcm_status pcm_project_workspace_layout(pcm_dtype dtype, int64_t T, int H, int F, int n, int k,
+                                        const pcm_tuning* tuning, size_t* z_off,
+                                        size_t* zscale_off, size_t* o_off, int* ksplit) {
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if ((st = check_dims(H, F)) != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    GemmTune tune;
+    if ((st = to_tune(tuning, false, &tune)) != PCM_OK) return st;
+    if (!z_off || !zscale_off || !o_off || !ksplit) return PCM_ERR_ARG;
+    const ProjWs w = proj_ws((size_t)(T * k), n, H, F, dtype, true, tune.tile);
+    *z_off = 0;
+    *zscale_off = dtype == PCM_BF16 ? w.zscale_off : 0;
+    *o_off = w.o_off;
+    *ksplit = w.ksplit;
+    return PCM_OK;
+}
+
+pcm_status pcm_dense_swiglu_tuned(pcm_dtype dtype, const void* x, const void* w_gate,
+                                  const void* w_up, const void* w_down, int64_t T, int H, int Fs,
+                                  float* y, int accumulate, void* ws, size_t ws_bytes, void* stream,
+                                  const pcm_tuning* tuning) {
     if (T < 0) return PCM_ERR_ARG;
     pcm_status st = check_dims(H, Fs);
     if (st != PCM_OK) return st;
     if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    GemmTune tune_up, tune_down;
+    if ((st = to_tune(tuning, true, &tune_up)) != PCM_OK) return st;
+    if ((st = to_tune(tuning, false, &tune_down)) != PCM_OK) return st;
     if (T >= ((int64_t)1 << 31)) return PCM_ERR_UNSUPPORTED;
     if (T == 0) return PCM_OK;
     if (!x || !w_gate || !w_up || !w_down || !y) return PCM_ERR_ARG;
@@ -293,7 +369,7 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     g.n = 1;
     g.K = H;
     g.N = Fs;
-    hipError_t e = bf16 ? launch_gemm_bf16(kExpand, g, T, s) : launch_gemm_f32(kExpand, g, T, s);
+    hipError_t e = bf16 ? launch_gemm_bf16(kExpand, g, T, s, tune_up) : launch_gemm_f32(kExpand, g, T, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     void* z = u;
     float* zscale = nullptr;
@@ -317,8 +393,15 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, 
     d.K = Fs;
     d.N = H;
     d.accumulate = accumulate;
-    e = bf16 ? launch_gemm_bf16(kDownAccum, d, T, s) : launch_gemm_f32(kDownAccum, d, T, s);
+    e = bf16 ? launch_gemm_bf16(kDownAccum, d, T, s, tune_down) : launch_gemm_f32(kDownAccum, d, T, s);
     return from_hip(e);
+}
+
+pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                            const void* w_down, int64_t T, int H, int Fs, float* y, int accumulate,
+                            void* ws, size_t ws_bytes, void* stream) {
+    return pcm_dense_swiglu_tuned(dtype, x, w_gate, w_up, w_down, T, H, Fs, y, accumulate, ws,
+                                  ws_bytes, stream, nullptr);
 }
 
 pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate,
@@ -372,7 +455,7 @@ pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate
         u_rows = P;
         gather_src = i32(w.rof_s);
     }
-    e = bf16 ? launch_gemm_bf16(kExpand, g, u_rows, s) : launch_gemm_f32(kExpand, g, u_rows, s);
+    e = bf16 ? launch_gemm_bf16(kExpand, g, u_rows, s, GemmTune()) : launch_gemm_f32(kExpand, g, u_rows, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     if (bf16) {  // U rows as row-scaled float16, no mixing
         MixMap id{};
@@ -402,7 +485,7 @@ pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate
     d.N = H;
     d.ksplit = 1;
     d.rows_total = P;
-    e = bf16 ? launch_gemm_bf16(kDownStore, d, P, s) : launch_gemm_f32(kDownStore, d, P, s);
+    e = bf16 ? launch_gemm_bf16(kDownStore, d, P, s, GemmTune()) : launch_gemm_f32(kDownStore, d, P, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     return from_hip(launch_combine_paths(o, paths->path_bits, paths->beta, i32(w.rof_t), T, k, H, P,
                                          y, accumulate, s));
@@ -443,15 +526,18 @@ pcm_status pcm_route_scored(const float* g_base, const float* g_tgt, float lambd
                                     one ? (int32_t*)((char*)ws + one) : nullptr, s));
 }
 
-pcm_status pcm_expand_scored(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
-                             const pcm_scored_paths* paths, int64_t T, int H, int F, int n, int K,
-                             void* u, void* ws, size_t ws_bytes, void* stream) {
+pcm_status pcm_expand_scored_tuned(pcm_dtype dtype, const void* x, const void* w_gate,
+                                   const void* w_up, const pcm_scored_paths* paths, int64_t T,
+                                   int H, int F, int n, int K, void* u, void* ws, size_t ws_bytes,
+                                   void* stream, const pcm_tuning* tuning) {
     (void)ws;
     (void)ws_bytes;
     pcm_status st = check_shape(T, n, K);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
     if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    GemmTune tune;
+    if ((st = to_tune(tuning, true, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
     if (!x || !w_gate || !w_up || !u || check_scored(paths) != PCM_OK) return PCM_ERR_ARG;
     if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(u)) return PCM_ERR_ARG;
@@ -468,23 +554,33 @@ pcm_status pcm_expand_scored(pcm_dtype dtype, const void* x, const void* w_gate,
     g.N = F;
     const int64_t R = T * K;  // upper bound: the rows in use are src_offsets[n]
     hipStream_t s = (hipStream_t)stream;
-    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s)
+    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s, tune)
                                       : launch_gemm_f32(kExpand, g, R, s));
 }
 
-pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void* w_down,
-                                      const pcm_scored_paths* paths, int64_t T, int H, int F, int n,
-                                      int K, float* y, int accumulate, void* ws, size_t ws_bytes,
-                                      void* stream) {
+pcm_status pcm_expand_scored(pcm_dtype dtype, const void* x, const void* w_gate, const void* w_up,
+                             const pcm_scored_paths* paths, int64_t T, int H, int F, int n, int K,
+                             void* u, void* ws, size_t ws_bytes, void* stream) {
+    return pcm_expand_scored_tuned(dtype, x, w_gate, w_up, paths, T, H, F, n, K, u, ws, ws_bytes,
+                                   stream, nullptr);
+}
+
+pcm_status pcm_project_combine_scored_tuned(pcm_dtype dtype, const void* u, const void* w_down,
+                                            const pcm_scored_paths* paths, int64_t T, int H, int F,
+                                            int n, int K, float* y, int accumulate, void* ws,
+                                            size_t ws_bytes, void* stream,
+                                            const pcm_tuning* tuning) {
     pcm_status st = check_shape(T, n, K);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
     if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    GemmTune tune;
+    if ((st = to_tune(tuning, false, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
     if (!u || !w_down || !y || check_scored(paths) != PCM_OK) return PCM_ERR_ARG;
     if (!aligned16(u) || !aligned16(w_down) || !aligned16(y)) return PCM_ERR_ARG;
     const int64_t R = T * K;  // row bound of U, z and o
-    const ProjWs w = proj_ws((size_t)R, n, H, F, dtype, true);
+    const ProjWs w = proj_ws((size_t)R, n, H, F, dtype, true, tune.tile);
     if (!ws || ws_bytes < w.total) return PCM_ERR_WORKSPACE;
     if (!aligned16(ws)) return PCM_ERR_ARG;
     void* z = ws;
@@ -501,7 +597,9 @@ pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void
     m.n_tgt = paths->n_tgt;
     m.K = K;
     m.R_src = m.R_tgt = R;
-    hipError_t e = launch_mix((const float*)u, z, zscale, m, T, F, s);
+    hipError_t e = stage_event(tuning, 0, s);
+    if (e == hipSuccess) e = launch_mix((const float*)u, z, zscale, m, T, F, s);
+    if (e == hipSuccess) e = stage_event(tuning, 1, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
     GemmArgs g{};
     g.a = z;
@@ -515,9 +613,20 @@ pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void
     g.N = H;
     g.ksplit = w.ksplit;
     g.rows_total = R;
-    e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s) : launch_gemm_f32(kDownStore, g, R, s);
+    e = bf16 ? launch_gemm_bf16(kDownStore, g, R, s, tune) : launch_gemm_f32(kDownStore, g, R, s);
+    if (e == hipSuccess) e = stage_event(tuning, 2, s);
     if (e != hipSuccess) return PCM_ERR_HIP;
-    return from_hip(launch_combine(o, w.ksplit, m, T, H, y, accumulate, s));
+    e = launch_combine(o, w.ksplit, m, T, H, y, accumulate, s);
+    if (e == hipSuccess) e = stage_event(tuning, 3, s);
+    return from_hip(e);
+}
+
+pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void* w_down,
+                                      const pcm_scored_paths* paths, int64_t T, int H, int F, int n,
+                                      int K, float* y, int accumulate, void* ws, size_t ws_bytes,
+                                      void* stream) {
+    return pcm_project_combine_scored_tuned(dtype, u, w_down, paths, T, H, F, n, K, y, accumulate,
+                                            ws, ws_bytes, stream, nullptr);
 }
 
 }  // extern "C"

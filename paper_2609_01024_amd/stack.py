@@ -45,7 +45,8 @@ class MoEStack:
         """One layer on hidden states h [T,H] (updated in place); returns the layer output y."""
         L, p = self.layers[l], self.plan
         if keep_logits:
-            self.logits = torch.empty((self.T, self.n), dtype=torch.float32, device=h.device)
+            with b._on(stream):
+                self.logits = torch.empty((self.T, self.n), dtype=torch.float32, device=h.device)
         b.pcm_route_logits(h, L.w_router, self.k, logits=self.logits if keep_logits else None,
                            topk_ids=p.ids, topk_w=p.w, ws=self.ws_router, stream=stream)
         b.pcm_build_paths(p.ids, p.w, L.mask, p.beta_mode, out=p.paths, ws=p.ws_paths, stream=stream)

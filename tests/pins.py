@@ -496,6 +496,69 @@ def pin_scored_relabel_and_edges(L):
     assert L.pcmo_route_scored(0, 0, 0.5, 0, 0, 1, 16, 9, 0, 0, 0, 0) != 0, "K > 8 must be rejected"
 
 
+def fp32_nearest(q) -> np.float32:
+    """The float32 nearest to the exact rational q, ties to the even significand (IEEE
+    round-to-nearest-even), from integer arithmetic on q's numerator and denominator."""
+    from fractions import Fraction
+    q = Fraction(q)
+    if q == 0:
+        return np.float32(0.0)
+    sign, a = (-1, -q) if q < 0 else (1, q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()   # 2^e <= a < 2^(e+2)
+    if a < Fraction(2) ** e:
+        e -= 1
+    elif a >= Fraction(2) ** (e + 1):
+        e += 1
+    quantum = max(e - 23, -149)                                  # 24 significant bits; subnormals
+    m = a / Fraction(2) ** quantum
+    fl = m.numerator // m.denominator
+    rem = m - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    v = Fraction(fl) * Fraction(2) ** quantum
+    assert v <= Fraction(float(np.finfo(np.float32).max)), "overflow"
+    return np.float32(sign * float(v))                           # exact: v has <= 24 bits
+
+
+def fma_f32(a, b, c) -> np.float32:
+    """a * b + c for float32 operands, rounded once to float32 (exact rational arithmetic)."""
+    from fractions import Fraction
+    return fp32_nearest(Fraction(float(a)) * Fraction(float(b)) + Fraction(float(c)))
+
+
+def pin_scored_general_lambda(L):
+    """The path score at a weight lambda that is not a power of two (so lambda * g_tgt is not
+    exact in float32): every score equals g_base_i + b_ij (one float32 addition) plus
+    lambda * g_tgt_j, the sum rounded once, computed here in exact rational arithmetic; the
+    selection is the stable descending sort of those scores and the weights their softmax."""
+    for lam, (T, n, K, d) in ((0.3, (12, 16, 8, 0.4)), (0.7, (10, 8, 4, 0.6)),
+                              (-1.25, (10, 12, 6, 0.5))):
+        gb = RNG.standard_normal((T, n)).astype(np.float32)
+        gt = RNG.standard_normal((T, n)).astype(np.float32)
+        mask = (RNG.random((n, n)) < d).astype(np.uint8)
+        bias = eq9_bias(n)
+        lam32 = np.float32(lam)
+        src, tgt, sc, beta = oracle.route_scored(gb, gt, lam, bias, mask, K, L=L)
+        active = (mask != 0) | np.eye(n, dtype=bool)
+        rounded_twice = 0
+        for t in range(T):
+            s = np.full((n, n), -np.inf)
+            for i in range(n):
+                for j in range(n):
+                    if active[i, j]:
+                        c = gb[t, i] + bias[i, j]          # float32 + float32: one rounding
+                        s[i, j] = fma_f32(lam32, gt[t, j], c)
+                        rounded_twice += s[i, j] != np.float32(np.float32(lam32 * gt[t, j]) + c)
+            order = np.argsort(-s.ravel(), kind="stable")[:K]
+            what = f"lambda={lam} token {t}"
+            assert list(src[t]) == list(order // n) and list(tgt[t]) == list(order % n), what
+            assert np.array_equal(sc[t], s.ravel()[order].astype(np.float32)), f"scores {what}"
+            e = np.exp(s.ravel()[order] - s.ravel()[order[0]])
+            _close(beta[t], e / e.sum(), 1e-14, f"weights {what}")
+        # the case is informative: rounding the product separately changes some scores
+        assert rounded_twice > 0, f"lambda={lam}: no score tells one rounding from two"
+
+
 def pin_router_logits(L):
     """Router scores: one-hot router rows read single features; a scaled row scales its
     score; a brute-force sum over h on small integers is exact; bf16 widening is exact."""
@@ -525,4 +588,4 @@ ALL_PINS = [pin_topk_bruteforce, pin_path_bits_bruteforce, pin_beta_closed_forms
             pin_expansion_rows, pin_relabel_invariance, pin_bf16_widening, pin_edge_cases,
             pin_scored_bruteforce, pin_scored_reduces_to_vanilla, pin_scored_single_source,
             pin_scored_target_prior, pin_scored_groups_and_dispatch, pin_scored_relabel_and_edges,
-            pin_router_logits]
+            pin_scored_general_lambda, pin_router_logits]

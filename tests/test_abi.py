@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert L.pcm_abi_version() == 110
+    assert L.pcm_abi_version() == 120
     for s in (OK, ARG, UNSUP, WS, HIP):
         assert L.pcm_status_string(s).decode().startswith("PCM_")
     assert L.pcm_status_string(77) == b"unknown pcm_status"
@@ -101,6 +101,61 @@ def test_expand_and_project_validation(L):
     assert L.pcm_dense_swiglu(1, FAKE, FAKE, FAKE, FAKE, 16, 128, 200, FAKE, 0, FAKE, needd,
                               None) == UNSUP
     assert L.pcm_dense_swiglu(1, None, None, None, None, 0, 128, 256, None, 0, None, 0, None) == OK
+
+
+def test_build_paths_rejects_misaligned_pointers(L):
+    p = _paths()
+    need = L.pcm_workspace_bytes(binding.OP_BUILD_PATHS, 5000, 0, 0, 64, 8, 0)
+    mis = ctypes.c_void_p(0x10004)
+    for i in range(3):   # topk_ids, topk_w, mask
+        args = [FAKE, FAKE, FAKE]
+        args[i] = mis
+        assert L.pcm_build_paths(*args, 5000, 64, 8, 0, ctypes.byref(p), FAKE, need, None) == ARG
+    for f, _ in binding.PcmPaths._fields_:
+        vals = {g: 0x10000 for g, _ in binding.PcmPaths._fields_}
+        vals[f] = 0x10008
+        q = binding.PcmPaths(**vals)
+        assert L.pcm_build_paths(FAKE, FAKE, FAKE, 5000, 64, 8, 0, ctypes.byref(q), FAKE, need,
+                                 None) == ARG, f
+    assert L.pcm_build_paths(FAKE, FAKE, FAKE, 5000, 64, 8, 0, ctypes.byref(p), mis, need,
+                             None) == ARG                                    # workspace
+
+
+def test_tuning_validation(L):
+    p = _paths()
+    bp = ctypes.byref(p)
+    args = (1, FAKE, FAKE, FAKE, bp, 4, 128, 128, 8, 2, FAKE, None, 0, None)
+    for field, bad in (("tile", ord("X")), ("order_expand", 3), ("order_down", -2),
+                       ("em_window", -1), ("group_n", -1), ("stream_depth", 5)):
+        t = binding.Tuning().struct()
+        setattr(t, field, bad)
+        assert L.pcm_expand_tuned(*args, ctypes.byref(t)) == ARG, field
+        assert L.pcm_project_workspace_layout(1, 4, 128, 128, 8, 2, ctypes.byref(t),
+                                              *(ctypes.byref(ctypes.c_size_t()) for _ in range(3)),
+                                              ctypes.byref(ctypes.c_int())) == ARG, field
+    # a valid tuning passes validation (T = 0 is a no-op), NULL tuning is the plain call
+    t = binding.Tuning(tile="L", order_expand=2, em_window=5, stream_depth=0).struct()
+    assert L.pcm_expand_tuned(1, None, None, None, None, 0, 128, 128, 8, 2, None, None, 0, None,
+                              ctypes.byref(t)) == OK
+    assert L.pcm_expand_tuned(1, FAKE, FAKE, FAKE, bp, 4, 100, 128, 8, 2, FAKE, None, 0, None,
+                              None) == UNSUP
+
+
+def test_project_workspace_layout(L):
+    al = lambda v: (v + 255) // 256 * 256
+    T, H, F, n, k = 4, 128, 128, 8, 2
+    R = T * k
+    lay = binding.project_workspace_layout(T, H, F, n, k, binding.PCM_BF16)
+    assert lay == {"z": 0, "zscale": al(R * F * 2), "o": al(R * F * 2) + al(R * 4), "ksplit": 1}
+    need = L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, T, H, F, n, k, 1)
+    assert need == lay["o"] + al(lay["ksplit"] * R * H * 4)
+    lay = binding.project_workspace_layout(T, H, F, n, k, binding.PCM_F32)
+    assert lay == {"z": 0, "zscale": 0, "o": al(R * F * 4), "ksplit": 1}
+    # a long F with few output tiles: two K slices of o, unless a forced tile kernel runs
+    big = binding.project_workspace_layout(300, 256, 4096, 4, 2, binding.PCM_BF16)
+    assert big["ksplit"] == 2
+    assert binding.project_workspace_layout(300, 256, 4096, 4, 2, binding.PCM_BF16,
+                                            binding.Tuning(tile="M"))["ksplit"] == 1
 
 
 def test_workspace_bytes_invalid(L):

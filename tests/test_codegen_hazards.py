@@ -11,7 +11,8 @@ generated assembly to check them:
 * an inline-assembly MFMA's accumulator is not read by ``v_accvgpr_read`` within 18 wait
   states (more than the 16-pass MFMA latency).
 
-Wait states are counted as issued instructions, ``s_nop N`` counting N + 1.
+Wait states are counted as issued instructions, ``s_nop N`` counting N + 1, along the
+listing and along every branch into its target (a loop's back edge).
 """
 import os
 import re
@@ -36,25 +37,18 @@ def _regs(tok, prefix):
     return {int(m.group(1))} if m else set()
 
 
-def scan(asm_text):
-    """Return a list of (kernel, rule, instruction) violations."""
-    bad = []
-    kernel, in_asm = None, False
-    valu_writes = []   # per issue slot: VGPRs written by VALU
-    mfma_dsts = []     # per issue slot: AGPRs written by an inline-assembly MFMA
-    def push(vw, md, n=1):
-        for _ in range(n):
-            valu_writes.append(vw)
-            mfma_dsts.append(md)
-        del valu_writes[:-MFMA_TO_ACC_READ]
-        del mfma_dsts[:-MFMA_TO_ACC_READ]
+def parse(asm_text):
+    """The kernels of an assembly listing: {name: [entry]}, each entry ("label", name) or
+    ("ins", op, operands, inside_inline_asm, text)."""
+    kernels, cur, in_asm = {}, None, False
     for line in asm_text.splitlines():
         s = line.strip()
         m = re.match(r"^(_Z\S+):", s)
         if m:
-            kernel, in_asm = m.group(1), False
-            valu_writes.clear()
-            mfma_dsts.clear()
+            cur, in_asm = [], False
+            kernels[m.group(1)] = cur
+            continue
+        if cur is None:
             continue
         if s.startswith(";;#ASMSTART"):
             in_asm = True
@@ -62,34 +56,94 @@ def scan(asm_text):
         if s.startswith(";;#ASMEND"):
             in_asm = False
             continue
+        m = re.match(r"^(\.?L\w+):", s)
+        if m:
+            cur.append(("label", m.group(1)))
+            continue
         if not s or s.startswith(";") or s.startswith("."):
             continue
         parts = s.replace(",", " ").split()
-        op = parts[0]
-        if op.startswith("s_nop"):
-            push(set(), set(), int(parts[1], 0) + 1 if len(parts) > 1 else 1)
-            continue
-        if op.startswith("v_mfma"):
-            if in_asm:
-                srcs = _regs(parts[2], "v") | _regs(parts[3], "v")
-                recent = set().union(*valu_writes[-VALU_TO_MFMA:]) if valu_writes else set()
-                if srcs & recent:
-                    bad.append((kernel, "VALU write -> MFMA read", s))
-                push(set(), _regs(parts[1], "a"))
-            else:
-                push(set(), set())
-            continue
-        if op.startswith("v_accvgpr_read"):
-            src = _regs(parts[2], "a")
-            if src & set().union(*mfma_dsts):
-                bad.append((kernel, "MFMA write -> accvgpr read", s))
-            push(_regs(parts[1], "v"), set())
-            continue
-        if op.startswith("v_") and not op.startswith("v_cmp") and len(parts) > 1:
-            push(_regs(parts[1], "v"), set())
-            continue
-        push(set(), set())
-    return bad
+        cur.append(("ins", parts[0], parts, in_asm, s))
+    return kernels
+
+
+class Window:
+    """The last MFMA_TO_ACC_READ issue slots: VGPRs written by VALU and AGPRs written by an
+    inline-assembly MFMA in each."""
+
+    def __init__(self, valu=None, mfma=None):
+        self.valu, self.mfma = list(valu or []), list(mfma or [])
+
+    def copy(self):
+        return Window(self.valu, self.mfma)
+
+    def push(self, vw, md, n=1):
+        for _ in range(n):
+            self.valu.append(vw)
+            self.mfma.append(md)
+        del self.valu[:-MFMA_TO_ACC_READ]
+        del self.mfma[:-MFMA_TO_ACC_READ]
+
+
+def step(win, op, parts, in_asm):
+    """Issue one instruction after the slots in `win`; returns the rule it breaks, or None,
+    and the number of issue slots it took."""
+    if op.startswith("s_nop"):
+        n = int(parts[1], 0) + 1 if len(parts) > 1 else 1
+        win.push(set(), set(), n)
+        return None, n
+    if op.startswith("v_mfma"):
+        rule = None
+        if in_asm:
+            srcs = _regs(parts[2], "v") | _regs(parts[3], "v")
+            recent = set().union(*win.valu[-VALU_TO_MFMA:]) if win.valu else set()
+            if srcs & recent:
+                rule = "VALU write -> MFMA read"
+            win.push(set(), _regs(parts[1], "a"))
+        else:
+            win.push(set(), set())
+        return rule, 1
+    if op.startswith("v_accvgpr_read"):
+        rule = "MFMA write -> accvgpr read" if _regs(parts[2], "a") & set().union(*win.mfma) else None
+        win.push(_regs(parts[1], "v"), set())
+        return rule, 1
+    if op.startswith("v_") and not op.startswith("v_cmp") and len(parts) > 1:
+        win.push(_regs(parts[1], "v"), set())
+        return None, 1
+    win.push(set(), set())
+    return None, 1
+
+
+def scan(asm_text):
+    """Return a list of (kernel, rule, instruction) violations: along the listing, and along
+    every branch into its target (a loop's back edge carries the end of the loop body to the
+    instructions after the loop head)."""
+    bad = set()
+    for kernel, entries in parse(asm_text).items():
+        labels = {e[1]: i for i, e in enumerate(entries) if e[0] == "label"}
+        win, edges = Window(), []
+        for e in entries:
+            if e[0] != "ins":
+                continue
+            _, op, parts, in_asm, text = e
+            rule, _ = step(win, op, parts, in_asm)
+            if rule:
+                bad.add((kernel, rule, text))
+            if op.startswith(("s_branch", "s_cbranch")) and len(parts) > 1 and parts[1] in labels:
+                edges.append((labels[parts[1]], win.copy()))
+        for start, w in edges:   # the slots right after each branch target, entered by the branch
+            used = 0
+            for e in entries[start:]:
+                if used >= MFMA_TO_ACC_READ:
+                    break
+                if e[0] != "ins":
+                    continue
+                _, op, parts, in_asm, text = e
+                rule, n = step(w, op, parts, in_asm)
+                used += n
+                if rule:
+                    bad.add((kernel, rule, text))
+    return sorted(bad)
 
 
 @pytest.fixture(scope="module")
@@ -128,6 +182,22 @@ def test_scanner_flags_planted_hazards():
     rules = sorted(r for _, r, _ in scan(bad))
     assert rules == ["MFMA write -> accvgpr read", "VALU write -> MFMA read"]
     assert scan(good) == []
+    # a loop whose last VALU write feeds the inline MFMA at its head: only the back edge
+    # shows it (the listing runs the write last and falls out of the loop)
+    loop = """_Zk:
+.LBB0_1:
+\t;;#ASMSTART
+\tv_mfma_f32_16x16x32_f16 a[0:3], v[2:5], v[8:11], a[0:3]
+\t;;#ASMEND
+\ts_nop 7
+\ts_nop 7
+\ts_nop 7
+\tv_cvt_pk_f16_f32 v2, v6, v7
+{gap}\ts_cbranch_scc1 .LBB0_1
+\ts_endpgm
+"""
+    assert [r for _, r, _ in scan(loop.format(gap=""))] == ["VALU write -> MFMA read"]
+    assert scan(loop.format(gap="\ts_nop 0\n")) == []
 
 
 def test_inline_mfma_hazards_absent(gemm_asm):

@@ -17,7 +17,7 @@ import paper_2609_01024_amd as pcm
 from paper_2609_01024_amd import binding
 from workloads import CONFIGS, make_inputs, make_scored_inputs, scaled, stress_config
 
-from test_gpu_parity import SMALL, assert_y_close, dev
+from test_gpu_parity import SMALL, assert_y_close, block_tokens, dev, poison
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -72,15 +72,18 @@ def scored_inputs(cfg, seed):
     return inp, s
 
 
-def run_layer(d, g_tgt, lam, bias, K, layout=None):
+def run_layer(d, g_tgt, lam, bias, K, tuning=None, plan_out=None):
     T, H = d["x"].shape
     n, F, _ = d["w_gate"].shape
     plan = pcm.ScoredLayerPlan(T, H, F, n, K, d["x"].dtype, DEV,
                                d["shared"][0].shape[0] if "shared" in d else 0)
+    poison(plan)
     plan.build_layout(d["mask"], t(bias))
     y = plan.forward(d["x"], d["logits"], t(g_tgt), lam, d["w_gate"], d["w_up"], d["w_down"],
-                     d.get("shared"))
+                     d.get("shared"), tuning=tuning)
     torch.cuda.synchronize()
+    if plan_out is not None:
+        plan_out.append(plan)
     return y.cpu().numpy()
 
 
@@ -121,7 +124,11 @@ def test_route_scored_full_size(name):
 
 @pytest.mark.parametrize("T,n,K,d,lam", [(1, 1, 1, 0.0, 0.5), (5, 4, 4, 1.0, 2.0), (256, 8, 2, 0.5, 0.5),
                                          (257, 64, 8, 0.25, 0.0), (1025, 64, 8, 0.3, 1.0),
-                                         (700, 256, 8, 0.2, 0.5), (64, 8, 8, 1.0, 64.0)])
+                                         (700, 256, 8, 0.2, 0.5), (64, 8, 8, 1.0, 64.0),
+                                         # weights that are not powers of two: lambda * g_tgt is
+                                         # rounded inside the fused multiply-add
+                                         (513, 64, 8, 0.3, 0.3), (300, 16, 6, 0.6, 0.7),
+                                         (1100, 60, 4, 0.3, -1.25)])
 def test_route_scored_shapes(T, n, K, d, lam):
     rng = np.random.default_rng(T + n)
     gb = rng.standard_normal((T, n)).astype(np.float32)
@@ -167,15 +174,27 @@ def test_route_scored_diagonal_is_vanilla_topk():
 # ------------------------------------------------------------------ whole layer
 @pytest.mark.parametrize("tile", ["auto", "S", "M", "L"])
 @pytest.mark.parametrize("name", sorted(SMALL))
-def test_scored_layer_small(name, tile, monkeypatch):
-    if tile != "auto":
-        monkeypatch.setenv("PCM_GEMM_TILE", tile)
+def test_scored_layer_small(name, tile):
+    tuning = pcm.Tuning(tile=tile) if tile != "auto" else None
     cfg = SMALL[name]
     say(f"scored layer {name} tile {tile}")
     inp, s = scored_inputs(cfg, 1)
     d = dev(inp)
-    y = run_layer(d, s.g_tgt, s.lam, s.bias, cfg.k)
+    y = run_layer(d, s.g_tgt, s.lam, s.bias, cfg.k, tuning=tuning)
     assert_y_close(y, oracle_layer(inp, s), cfg.dtype, f"scored {name}/{tile}")
+
+
+@pytest.mark.parametrize("lam", [0.3, 0.7, -1.25])
+def test_scored_layer_general_lambda(lam):
+    """The whole scored layer at target-prior weights that are not powers of two."""
+    cfg = SMALL["olmoe_s"]
+    inp, s = scored_inputs(cfg, 4)
+    d = dev(inp)
+    check_route(inp.logits, s.g_tgt, lam, s.bias, inp.mask, cfg.k, f"lambda {lam}")
+    y = run_layer(d, s.g_tgt, lam, s.bias, cfg.k)
+    ref = oracle.layer_scored(inp.x, inp.logits, s.g_tgt, lam, s.bias, inp.mask, inp.w_gate,
+                              inp.w_up, inp.w_down, cfg.k)
+    assert_y_close(y, ref, cfg.dtype, f"scored lambda {lam}")
 
 
 def test_scored_layer_single_source_paths():
@@ -228,15 +247,25 @@ def test_scored_layer_is_deterministic():
 @pytest.mark.slow
 @pytest.mark.parametrize("name", ["tiny", "mixtral", "olmoe", "finegrained_shared", "decode"])
 def test_scored_layer_full_size(name):
+    """The scored layer at the workload's size with every buffer NaN first; y against the
+    oracle on the tokens of the first and last row of every 256-row block of both dispatch
+    layouts (the expansion's and the projection's M tiles) plus a random sample."""
     cfg = CONFIGS[name]
     say(f"scored full-size {name}: inputs")
     inp, s = scored_inputs(cfg, 0)
     d = dev(inp)
     say(f"scored full-size {name}: layer")
-    y = run_layer(d, s.g_tgt, s.lam, s.bias, cfg.k)
+    plans = []
+    y = run_layer(d, s.g_tgt, s.lam, s.bias, cfg.k, plan_out=plans)
+    assert np.isfinite(y).all(), f"{name}: unwritten or non-finite outputs"
+    p = plans[0].paths
     rng = np.random.default_rng(12)
     nsample = cfg.T if cfg.T <= 64 else 24
-    tokens = np.unique(np.concatenate([[0, cfg.T - 1], rng.choice(cfg.T, nsample, replace=False)]))
+    tokens = np.unique(np.concatenate([
+        [0, cfg.T - 1], rng.choice(cfg.T, nsample, replace=False),
+        block_tokens(p.src_offsets.cpu().numpy(), p.src_row_token.cpu().numpy()),
+        block_tokens(p.tgt_offsets.cpu().numpy(), p.tgt_row_token.cpu().numpy())]))
     say(f"scored full-size {name}: oracle on {tokens.size} tokens")
     assert_y_close(y[tokens], oracle_layer(inp, s, tokens), cfg.dtype, name)
-    assert np.isfinite(y).all()
+
+

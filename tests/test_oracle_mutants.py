@@ -50,6 +50,8 @@ MUTANTS = {
                               "return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)j * n + i]);"),
     "score_target_prior_on_source": ("return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)i * n + j]);",
                                      "return fmaf(lambda, gt[i], gb[i] + bias[(int64_t)i * n + j]);"),
+    "score_product_rounded_first": ("return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)i * n + j]);",
+                                    "return (float)(lambda * gt[j]) + (gb[i] + bias[(int64_t)i * n + j]);"),
     "score_base_on_target": ("return fmaf(lambda, gt[j], gb[i] + bias[(int64_t)i * n + j]);",
                              "return fmaf(lambda, gt[j], gb[j] + bias[(int64_t)i * n + j]);"),
     "scored_mask_ignored": ("if (i != j && !mask[(int64_t)i * n + j]) continue;   /* outside A */",
