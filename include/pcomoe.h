@@ -19,7 +19,8 @@
  * Conventions for every call:
  *   - Pointers named as device pointers must be device memory of the current HIP device,
  *     16-byte aligned; arrays are dense and row-major. The caller owns every buffer; the
- *     library never allocates or frees memory and holds no mutable global state.
+ *     library never allocates or frees memory and holds no mutable global state (except
+ *     pcm_project_combine_noalloc's per-GPU scratch array and its looked-up addresses).
  *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued and the call
  *     returns without synchronising. Device-side faults surface at the caller's next sync.
  *   - Arguments are validated on the host before anything is enqueued. On error nothing
@@ -148,6 +149,23 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
                                const pcm_paths* paths, int64_t T, int H, int F, int n, int k,
                                float* y, int accumulate, void* ws, size_t ws_bytes,
                                void* stream);
+
+/* pcm_project_combine for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops such as a decode step, harnesses that forbid allocation): the
+ * same computation, kernels and result, with z, its scales and o kept in a scratch array
+ * inside the library instead of a caller workspace. It allocates nothing. The array holds
+ * PCM_NOALLOC_SCRATCH_BYTES (16 MiB) per GPU, is reserved on every GPU the library runs on
+ * until the process ends, and its address on a device is looked up on the first call made
+ * with that device current. Sizes whose workspace
+ * (pcm_workspace_bytes(PCM_OP_PROJECT_COMBINE, T, H, F, n, k, dtype)) exceeds the array give
+ * PCM_ERR_UNSUPPORTED (a decode-shaped layer, T = 32, H = 7168, F = 2048, k = 8, needs
+ * 8.0 MiB). All calls on one GPU share its array and each leaves its intermediates there:
+ * calls that overlap on one GPU (other streams, other host threads) race and must be
+ * serialised by the caller. Arguments as pcm_project_combine. */
+#define PCM_NOALLOC_SCRATCH_BYTES (16u << 20)
+pcm_status pcm_project_combine_noalloc(pcm_dtype dtype, const void* u, const void* w_down,
+                                      const pcm_paths* paths, int64_t T, int H, int F, int n,
+                                      int k, float* y, int accumulate, void* stream);
 
 /* A dense SwiGLU FFN applied to every token with weight 1 (Section 2's expert F_e), for an
  * always-on shared expert that sits beside the routed experts and outside the path

@@ -8,7 +8,8 @@ from .binding import (BETA_GLOBAL, BETA_PRODUCT, BETA_SRC_COND, PCM_BF16, PCM_F3
                       PathLayout, PathTable, ScoredLayerPlan, ScoredPathTable, Tuning,
                       layer_forward, lib, project_workspace_layout,
                       pcm_build_paths, pcm_dense_swiglu, pcm_expand, pcm_expand_scored,
-                      pcm_layer_per_path, pcm_path_layout_build, pcm_project_combine, pcm_project_combine_scored,
+                      pcm_layer_per_path, pcm_path_layout_build, pcm_project_combine, pcm_project_combine_noalloc,
+                      pcm_project_combine_scored,
                       pcm_residual_add, pcm_route, pcm_route_logits, pcm_route_scored,
                       workspace_bytes)
 
@@ -16,6 +17,7 @@ __all__ = ["BETA_GLOBAL", "BETA_PRODUCT", "BETA_SRC_COND", "PCM_BF16", "PCM_F32"
            "PathLayout", "PathTable", "ScoredLayerPlan", "ScoredPathTable", "Tuning", "layer_forward",
            "lib", "project_workspace_layout",
            "pcm_build_paths", "pcm_dense_swiglu", "pcm_expand", "pcm_expand_scored",
-           "pcm_layer_per_path", "pcm_path_layout_build", "pcm_project_combine", "pcm_project_combine_scored",
+           "pcm_layer_per_path", "pcm_path_layout_build", "pcm_project_combine", "pcm_project_combine_noalloc",
+           "pcm_project_combine_scored",
            "pcm_residual_add", "pcm_route", "pcm_route_logits", "pcm_route_scored",
            "workspace_bytes"]

@@ -29,7 +29,7 @@ EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_project_combine_scored", "pcm_layer_per_path", "pcm_route_logits",
            "pcm_residual_add", "pcm_expand_tuned", "pcm_project_combine_tuned",
            "pcm_dense_swiglu_tuned", "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
-           "pcm_project_workspace_layout")
+           "pcm_project_workspace_layout", "pcm_project_combine_noalloc")
 
 
 class PcmTuning(ctypes.Structure):
@@ -117,6 +117,8 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
     for name in ("pcm_expand", "pcm_project_combine", "pcm_dense_swiglu", "pcm_expand_scored",
                  "pcm_project_combine_scored"):
         getattr(L, name + "_tuned").argtypes = getattr(L, name).argtypes + [TP]
+    L.pcm_project_combine_noalloc.argtypes = [I, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, P,
+                                              I, P]
     SZP = ctypes.POINTER(SZ)
     L.pcm_project_workspace_layout.argtypes = [I, I64, I, I, I, I, TP, SZP, SZP, SZP,
                                                ctypes.POINTER(I)]
@@ -126,7 +128,7 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
                  "pcm_layer_per_path", "pcm_route_logits", "pcm_residual_add",
                  "pcm_expand_tuned", "pcm_project_combine_tuned", "pcm_dense_swiglu_tuned",
                  "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
-                 "pcm_project_workspace_layout"):
+                 "pcm_project_workspace_layout", "pcm_project_combine_noalloc"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -311,6 +313,21 @@ def pcm_project_combine(u, w_down, paths: PathTable, y=None, accumulate: bool = 
                                          _ptr(y), int(bool(accumulate)), _ptr(ws),
                                          ws.numel() if ws is not None else 0, _stream(stream)],
                  tuning))
+    return y
+
+
+def pcm_project_combine_noalloc(u, w_down, paths: PathTable, y=None, accumulate: bool = False,
+                                stream=None) -> torch.Tensor:
+    """pcm_project_combine with the library's own per-GPU scratch instead of a workspace."""
+    _dev(u, w_down, y)
+    n, H, F = w_down.shape
+    T, k = paths.T, paths.k
+    with _on(stream):
+        y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=u.device)
+    st = paths.struct()
+    _check(lib().pcm_project_combine_noalloc(_dtype_code(w_down), _ptr(u), _ptr(w_down),
+                                             ctypes.byref(st), T, H, F, n, k, _ptr(y),
+                                             int(bool(accumulate)), _stream(stream)))
     return y
 
 

@@ -3,11 +3,39 @@
 // synchronises.
 #include "pcomoe.h"
 
+#include <mutex>
+
 #include "internal.h"
 
 using namespace pcm;
 
+// Scratch of pcm_project_combine_noalloc: z, its row scales and o live here instead of in a
+// caller workspace. Each GPU the library runs on holds its own copy until the process ends.
+// Host code never uses the array's name as an address: the device address of this GPU's copy
+// comes from hipGetSymbolAddress (scratch_on_current_device).
+static __device__ __align__(256) unsigned char scratch[PCM_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch` per device (set once)
+
+// The address of the current device's scratch array, looked up on the first call made with
+// that device current.
+pcm_status scratch_on_current_device(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return PCM_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return PCM_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return PCM_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return PCM_OK;
+}
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -314,6 +342,29 @@ pcm_status pcm_project_combine(pcm_dtype dtype, const void* u, const void* w_dow
                                float* y, int accumulate, void* ws, size_t ws_bytes, void* stream) {
     return pcm_project_combine_tuned(dtype, u, w_down, paths, T, H, F, n, k, y, accumulate, ws,
                                      ws_bytes, stream, nullptr);
+}
+
+pcm_status pcm_project_combine_noalloc(pcm_dtype dtype, const void* u, const void* w_down,
+                                      const pcm_paths* paths, int64_t T, int H, int F, int n,
+                                      int k, float* y, int accumulate, void* stream) {
+    // the same checks, in the same order, as pcm_project_combine_tuned, before the scratch
+    // size (so that bad arguments report PCM_ERR_ARG / UNSUPPORTED as there)
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if ((st = check_dims(H, F)) != PCM_OK) return st;
+    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!u || !w_down || !y || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
+    if (!aligned16(u) || !aligned16(w_down) || !aligned16(y)) return PCM_ERR_ARG;
+    const size_t need = proj_ws((size_t)(T * k), n, H, F, dtype, true).total;
+    if (need > (size_t)PCM_NOALLOC_SCRATCH_BYTES) return PCM_ERR_UNSUPPORTED;
+    void* ws = nullptr;
+    if ((st = scratch_on_current_device(&ws)) != PCM_OK) return st;
+    // every byte of z, the scales and o that the combine reads is written earlier in the same
+    // call (one z row per (token, target) by the mix, every o element by the projection), so
+    // nothing is cleared
+    return pcm_project_combine_tuned(dtype, u, w_down, paths, T, H, F, n, k, y, accumulate, ws,
+                                     need, stream, nullptr);
 }
 
 pcm_status pcm_project_workspace_layout(pcm_dtype dtype, int64_t T, int H, int F, int n, int k,

@@ -141,6 +141,27 @@ def test_tuning_validation(L):
                               None) == UNSUP
 
 
+def test_noalloc_validation(L):
+    """The allocation-free projection: the same argument checks as pcm_project_combine, and
+    sizes whose workspace exceeds its 16 MiB scratch rejected before any device call."""
+    p = _paths()
+    bp = ctypes.byref(p)
+    assert L.pcm_project_combine_noalloc(1, FAKE, FAKE, bp, 2048, 512, 256, 8, 8, FAKE, 0,
+                                         None) == UNSUP       # needs 40 MiB
+    assert L.pcm_project_combine_noalloc(1, FAKE, FAKE, bp, 4096, 4096, 14336, 8, 2, FAKE, 0,
+                                         None) == UNSUP
+    assert L.pcm_project_combine_noalloc(1, None, FAKE, bp, 32, 2048, 1024, 64, 8, FAKE, 0,
+                                         None) == ARG
+    assert L.pcm_project_combine_noalloc(1, FAKE, FAKE, None, 32, 2048, 1024, 64, 8, FAKE, 0,
+                                         None) == ARG
+    assert L.pcm_project_combine_noalloc(1, ctypes.c_void_p(0x10004), FAKE, bp, 32, 2048, 1024,
+                                         64, 8, FAKE, 0, None) == ARG
+    assert L.pcm_project_combine_noalloc(1, FAKE, FAKE, bp, 32, 2000, 1024, 64, 8, FAKE, 0,
+                                         None) == UNSUP       # H not a multiple of 64
+    assert L.pcm_project_combine_noalloc(1, None, None, None, 0, 2048, 1024, 64, 8, None, 0,
+                                         None) == OK          # T = 0
+
+
 def test_project_workspace_layout(L):
     al = lambda v: (v + 255) // 256 * 256
     T, H, F, n, k = 4, 128, 128, 8, 2
