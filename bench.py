@@ -7,8 +7,9 @@ workload (Mixtral-shaped) at the top level, and every workload under "workloads"
 
   python bench.py [--steps K] [--warmup W] [--config NAME] [--only] [--router topk|scored]
                   [--no-cpu-baseline]
-  python bench.py --trace-summary DIR     per-kernel durations of the timed launches in a
-                                          rocprofv3 kernel trace written under DIR
+  python bench.py --trace-summary DIR     per-kernel durations (kernel traces) or counter
+                                          means (--pmc runs) of the timed launches in the
+                                          rocprofv3 output written under DIR
 
 Per-kernel times come from HIP events recorded on the stream the kernels run on: around
 each call, and inside pcm_project_combine between the mix, the projection GEMM and the
@@ -69,34 +70,72 @@ def parse():
 
 
 # ------------------------------------------------------------------ trace summary
-def trace_summary(path: str):
-    """Per-kernel launch durations inside each fenced timed region of a rocprofv3 kernel
-    trace (markdown table on stdout)."""
-    files = sorted(glob.glob(os.path.join(path, "**", "*kernel_trace.csv"), recursive=True))
-    if not files:
-        sys.exit(f"no kernel_trace.csv under {path}")
-    rows = []
-    for f in files:
-        with open(f) as fh:
-            rows += list(csv.DictReader(fh))
-    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+def _fenced(rows):
+    """Index ranges (a, b) of the fenced timed regions of time-ordered dispatch rows; the whole
+    list when it has no fences (a plain program such as the copy probe)."""
     fences = [i for i, r in enumerate(rows) if FENCE in r["Kernel_Name"]]
     if len(fences) < 2:
-        sys.exit("the trace has no fenced timed region")
-    for reg, (a, b) in enumerate(zip(fences[0::2], fences[1::2])):
-        stats = {}
-        for r in rows[a + 1:b]:
-            d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-            stats.setdefault(r["Kernel_Name"], []).append(d)
-        span = (int(rows[b]["Start_Timestamp"]) - int(rows[a]["End_Timestamp"])) / 1e3
-        print(f"### timed region {reg}: {span:.1f} us between the fences\n")
-        print("| kernel | launches | avg us | min us | max us | total us |")
-        print("|---|---|---|---|---|---|")
-        for name, ds in sorted(stats.items(), key=lambda kv: -sum(kv[1])):
-            short = name.split("(")[0].replace("void ", "")
-            print(f"| `{short}` | {len(ds)} | {np.mean(ds):.1f} | {min(ds):.1f} | {max(ds):.1f} | "
-                  f"{sum(ds):.1f} |")
-        print()
+        return [(-1, len(rows))]
+    return list(zip(fences[0::2], fences[1::2]))
+
+
+def _short(name: str) -> str:
+    return name.replace("(anonymous namespace)::", "").replace("pcm::", "").split("(")[0] \
+        .replace("void ", "")
+
+
+def trace_summary(path: str):
+    """Per-kernel launch durations (kernel traces) or counter averages (counter collections)
+    inside each fenced timed region of the rocprofv3 output under `path` (markdown tables)."""
+    traces = sorted(glob.glob(os.path.join(path, "**", "*kernel_trace.csv"), recursive=True))
+    counters = sorted(glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True))
+    if not traces and not counters:
+        sys.exit(f"no kernel_trace.csv or counter_collection.csv under {path}")
+    for f in traces:
+        rows = sorted(csv.DictReader(open(f)), key=lambda r: int(r["Start_Timestamp"]))
+        for reg, (a, b) in enumerate(_fenced(rows)):
+            stats = {}
+            for r in rows[a + 1:b]:
+                d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+                stats.setdefault(r["Kernel_Name"], []).append(d)
+            print(f"### kernel trace, timed region {reg} ({os.path.basename(f)})\n")
+            print("| kernel | launches | avg us | min us | max us | total us |")
+            print("|---|---|---|---|---|---|")
+            for name, ds in sorted(stats.items(), key=lambda kv: -sum(kv[1])):
+                print(f"| `{_short(name)}` | {len(ds)} | {np.mean(ds):.1f} | {min(ds):.1f} | "
+                      f"{max(ds):.1f} | {sum(ds):.1f} |")
+            print()
+    for f in counters:
+        disp = {}
+        for r in csv.DictReader(open(f)):
+            d = disp.setdefault(r["Dispatch_Id"], {"name": r["Kernel_Name"],
+                                                  "start": int(r["Start_Timestamp"]),
+                                                  "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"]),
+                                                  "c": {}})
+            d["c"][r["Counter_Name"]] = d["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        rows = sorted(({"Kernel_Name": v["name"], **v} for v in disp.values()), key=lambda v: v["start"])
+        names = sorted({c for v in rows for c in v["c"]})
+        for reg, (a, b) in enumerate(_fenced(rows)):
+            agg = {}
+            for v in rows[a + 1:b]:
+                agg.setdefault(v["name"], []).append(v)
+            print(f"### counters, timed region {reg} ({os.path.basename(f)}; mean per dispatch)\n")
+            extra = []
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in names and "GRBM_GUI_ACTIVE" in names:
+                extra = ["MFMA busy", "clock GHz"]
+            print("| kernel | dispatches | avg us | " + " | ".join(names + extra) + " |")
+            print("|---|---|---|" + "---|" * (len(names) + len(extra)))
+            for name, vs in sorted(agg.items(), key=lambda kv: -sum(v["ns"] for v in kv[1])):
+                m = {c: np.mean([v["c"].get(c, 0.0) for v in vs]) for c in names}
+                ns = np.mean([v["ns"] for v in vs])
+                cells = [f"{m[c]:.6g}" for c in names]
+                if extra:
+                    # 8 XCDs count GRBM_GUI_ACTIVE each; 1024 SIMDs count MFMA-busy cycles
+                    gui = m["GRBM_GUI_ACTIVE"] / 8
+                    cells += [f"{m['SQ_VALU_MFMA_BUSY_CYCLES'] / 1024 / max(gui, 1):.1%}",
+                              f"{gui / max(ns, 1):.2f}"]
+                print(f"| `{_short(name)}` | {len(vs)} | {ns / 1e3:.1f} | " + " | ".join(cells) + " |")
+            print()
 
 
 def copy_probe(mib: int):
