@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--router", choices=("topk", "scored"), default="topk",
                     help="topk: top-k experts, paths among them allowed by the mask; "
                          "scored: scored compositional routing over the active paths")
+    ap.add_argument("--indexing", choices=("fused", "separate"), default="fused",
+                    help="fused: route, path table and dispatch layout in one operation over the "
+                         "layer's packed mask; separate: the route and the path build as two calls")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stack", type=int, default=0, metavar="L",
@@ -247,7 +250,10 @@ def measure(pcm, name, cfg, d, args, flush, scored):
     else:
         sinp = None
         plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, d["dtype"], dev, cfg.shared_F)
-        marks = (["shared"] if shared else []) + ["route", "build_paths", "expand"]
+        fused = args.indexing == "fused"
+        packed = pcm.pcm_mask_pack(mask) if fused else None   # once per layer
+        marks = (["shared"] if shared else []) + (["route_paths"] if fused else
+                                                  ["route", "build_paths"]) + ["expand"]
 
     def new_events():
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(marks) + 1)]
@@ -278,9 +284,13 @@ def measure(pcm, name, cfg, d, args, flush, scored):
             pcm.pcm_project_combine_scored(plan.u, wd, plan.paths, y=plan.y,
                                            accumulate=bool(shared), ws=plan.ws_proj, tuning=tun)
         else:
-            pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
-            mark()
-            pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
+            if fused:
+                pcm.pcm_route_paths(logits, packed, cfg.k, 0, plan.ids, plan.w, out=plan.paths,
+                                    ws=plan.ws_paths)
+            else:
+                pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
+                mark()
+                pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
             mark()
             pcm.pcm_expand(x, wg, wu, plan.paths, u=plan.u)
             mark()
@@ -349,7 +359,9 @@ def workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored):
     hbm = {"mix": acc.mix_bytes(R, R_tgt, cfg.F, cfg.T, K, u_elem, z_elem) / (fl["mix"] * 1e-3) / 1e9,
            "combine": acc.combine_bytes(R_bound, cfg.H, cfg.T, K, ksplit, bool(cfg.shared_F))
            / (fl["combine"] * 1e-3) / 1e9}
-    if not scored:
+    if "route_paths" in fl:
+        hbm["route_paths"] = acc.route_paths_bytes(cfg.T, cfg.n, K) / (fl["route_paths"] * 1e-3) / 1e9
+    elif not scored:
         hbm["route"] = acc.route_bytes(cfg.T, cfg.n, K) / (fl["route"] * 1e-3) / 1e9
         hbm["build_paths"] = acc.paths_bytes(cfg.T, cfg.n, K) / (fl["build_paths"] * 1e-3) / 1e9
     rec = {"ms": round(ms, 4), "tokens_per_s": round(cfg.T / (ms * 1e-3), 1),

@@ -83,7 +83,8 @@ typedef enum pcm_op {
     PCM_OP_DENSE_SWIGLU = 3,
     PCM_OP_ROUTE_SCORED = 4,
     PCM_OP_LAYER_PER_PATH = 5,
-    PCM_OP_ROUTE_LOGITS = 6
+    PCM_OP_ROUTE_LOGITS = 6,
+    PCM_OP_ROUTE_PATHS = 7
 } pcm_op;
 
 /* Path table and grouped dispatch layout of T tokens (caller-owned device buffers).
@@ -125,6 +126,25 @@ pcm_status pcm_route_logits(pcm_dtype dtype, const void* x, const void* w_router
  * ws: device workspace of pcm_workspace_bytes(PCM_OP_BUILD_PATHS, T, 0, 0, n, k, 0). */
 pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const uint8_t* mask,
                            int64_t T, int n, int k, pcm_beta_mode beta_mode,
+                           const pcm_paths* out, void* ws, size_t ws_bytes, void* stream);
+
+/* Offline per-layer layout of the compatibility mask for pcm_route_paths (Section 4.3's
+ * indexing reads a mask fixed per layer, Section 4.2 with m_ii = 1). mask [n,n] u8 (device),
+ * as pcm_build_paths; packed [n, ceil(n/64)] u64 (device, caller-owned): bit j % 64 of word
+ * [i][j / 64] is set iff mask[i][j] != 0 or i == j; bits at j >= n are 0. One launch. */
+pcm_status pcm_mask_pack(const uint8_t* mask, int n, uint64_t* packed, void* stream);
+
+/* Section 4.3's fused indexing operation: pcm_route's top-k and softmax, pcm_build_paths's
+ * path bits and beta, and the grouped dispatch layout, from the logits and a packed mask.
+ * One launch when T <= 64; otherwise a launch that routes, forms the path table and counts
+ * rows per (32-token block, expert), then one that places the rows. Outputs are
+ * bit-identical to pcm_route followed by pcm_build_paths with the mask that packed_mask
+ * was packed from, and deterministic. logits [T,n] f32 (device); packed_mask from
+ * pcm_mask_pack; topk_ids [T,k] i32 and topk_w [T,k] f32 (device) as pcm_route; *out as
+ * pcm_build_paths (all of its arrays written). Limits and errors as pcm_build_paths.
+ * ws: pcm_workspace_bytes(PCM_OP_ROUTE_PATHS, T, 0, 0, n, k, 0) bytes (0 when T <= 64). */
+pcm_status pcm_route_paths(const float* logits, const uint64_t* packed_mask, int64_t T, int n,
+                           int k, pcm_beta_mode beta_mode, int32_t* topk_ids, float* topk_w,
                            const pcm_paths* out, void* ws, size_t ws_bytes, void* stream);
 
 /* Expansion side, once per (token, source) row (Section 4.1 U_e; Section 4.3 reuse):

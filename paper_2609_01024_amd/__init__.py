@@ -11,6 +11,7 @@ from .binding import (BETA_GLOBAL, BETA_PRODUCT, BETA_SRC_COND, PCM_BF16, PCM_F3
                       pcm_layer_per_path, pcm_path_layout_build, pcm_project_combine, pcm_project_combine_noalloc,
                       pcm_project_combine_scored,
                       pcm_residual_add, pcm_route, pcm_route_logits, pcm_route_scored,
+                      pcm_mask_pack, pcm_route_paths,
                       workspace_bytes)
 
 __all__ = ["BETA_GLOBAL", "BETA_PRODUCT", "BETA_SRC_COND", "PCM_BF16", "PCM_F32", "LayerPlan",
@@ -20,4 +21,5 @@ __all__ = ["BETA_GLOBAL", "BETA_PRODUCT", "BETA_SRC_COND", "PCM_BF16", "PCM_F32"
            "pcm_layer_per_path", "pcm_path_layout_build", "pcm_project_combine", "pcm_project_combine_noalloc",
            "pcm_project_combine_scored",
            "pcm_residual_add", "pcm_route", "pcm_route_logits", "pcm_route_scored",
+           "pcm_mask_pack", "pcm_route_paths",
            "workspace_bytes"]

@@ -67,6 +67,13 @@ def paths_bytes(T: int, n: int, k: int) -> int:
     return T * k * 8 + n * n + T * 8 + T * k * k * 4 + T * k * 12 + (n + 1) * 4
 
 
+def route_paths_bytes(T: int, n: int, k: int) -> int:
+    """The fused indexing operation: the logits and the packed mask in; ids and weights, path
+    bits, weights beta, row_token / row_slot / row_of and the offsets out."""
+    return (T * n * 4 + n * ((n + 63) // 64) * 8 + T * k * 8 + T * 8 + T * k * k * 4
+            + T * k * 12 + (n + 1) * 4)
+
+
 def mix_bytes(R_src: int, R_tgt: int, F: int, T: int, K: int, u_elem: int = 4,
               z_elem: int = 2) -> int:
     """z_(t,b) = sum_a beta_ab u_(t,a): every U row in, every z row (and its scale) out, plus

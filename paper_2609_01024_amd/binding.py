@@ -21,7 +21,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpcomoe.
 PCM_F32, PCM_BF16 = 0, 1
 BETA_SRC_COND, BETA_PRODUCT, BETA_GLOBAL = 0, 1, 2
 OP_BUILD_PATHS, OP_EXPAND, OP_PROJECT_COMBINE, OP_DENSE_SWIGLU, OP_ROUTE_SCORED = 0, 1, 2, 3, 4
-OP_LAYER_PER_PATH, OP_ROUTE_LOGITS = 5, 6
+OP_LAYER_PER_PATH, OP_ROUTE_LOGITS, OP_ROUTE_PATHS = 5, 6, 7
 
 EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_dense_swiglu", "pcm_workspace_bytes", "pcm_status_string", "pcm_abi_version",
@@ -29,7 +29,8 @@ EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_project_combine_scored", "pcm_layer_per_path", "pcm_route_logits",
            "pcm_residual_add", "pcm_expand_tuned", "pcm_project_combine_tuned",
            "pcm_dense_swiglu_tuned", "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
-           "pcm_project_workspace_layout", "pcm_project_combine_noalloc")
+           "pcm_project_workspace_layout", "pcm_project_combine_noalloc", "pcm_mask_pack",
+           "pcm_route_paths")
 
 
 class PcmTuning(ctypes.Structure):
@@ -94,6 +95,8 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
     P, I, I64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
     L.pcm_route.argtypes = [P, I64, I, I, P, P, P]
     L.pcm_build_paths.argtypes = [P, P, P, I64, I, I, I, ctypes.POINTER(PcmPaths), P, SZ, P]
+    L.pcm_mask_pack.argtypes = [P, I, P, P]
+    L.pcm_route_paths.argtypes = [P, P, I64, I, I, I, P, P, ctypes.POINTER(PcmPaths), P, SZ, P]
     L.pcm_expand.argtypes = [I, P, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, P, P, SZ, P]
     L.pcm_project_combine.argtypes = [I, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, P, I, P,
                                       SZ, P]
@@ -128,7 +131,8 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
                  "pcm_layer_per_path", "pcm_route_logits", "pcm_residual_add",
                  "pcm_expand_tuned", "pcm_project_combine_tuned", "pcm_dense_swiglu_tuned",
                  "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
-                 "pcm_project_workspace_layout", "pcm_project_combine_noalloc"):
+                 "pcm_project_workspace_layout", "pcm_project_combine_noalloc", "pcm_mask_pack",
+                 "pcm_route_paths"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -282,6 +286,40 @@ def pcm_build_paths(topk_ids, topk_w, mask, beta_mode: int = BETA_SRC_COND, out:
                                  ctypes.byref(st), _ptr(ws), ws.numel() if ws is not None else 0,
                                  _stream(stream)))
     return out
+
+
+def pcm_mask_pack(mask: torch.Tensor, packed: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """The layer's mask [n,n] u8 as the packed [n, ceil(n/64)] int64 bitset of pcm_route_paths
+    (the diagonal set)."""
+    _dev(mask)
+    n = mask.shape[0]
+    with _on(stream):
+        packed = packed if packed is not None else torch.empty((n, (n + 63) // 64), dtype=torch.int64,
+                                                               device=mask.device)
+    _dev(packed)
+    _check(lib().pcm_mask_pack(_ptr(mask), n, _ptr(packed), _stream(stream)))
+    return packed
+
+
+def pcm_route_paths(logits, packed_mask, k: int, beta_mode: int = BETA_SRC_COND, topk_ids=None,
+                    topk_w=None, out: PathTable = None, ws: torch.Tensor = None, stream=None):
+    """Fused indexing: (topk_ids, topk_w, PathTable) from the logits and a packed mask."""
+    _dev(logits, packed_mask)
+    T, n = logits.shape
+    dev = logits.device
+    need = workspace_bytes(OP_ROUTE_PATHS, T, 0, 0, n, k, 0)
+    with _on(stream):
+        ids = topk_ids if topk_ids is not None else torch.empty((T, k), dtype=torch.int32, device=dev)
+        w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=dev)
+        out = out or PathTable.empty(T, n, k, dev)
+        if ws is None:
+            ws = _workspace(need, dev)
+    _dev(ids, w)
+    st = out.struct()
+    _check(lib().pcm_route_paths(_ptr(logits), _ptr(packed_mask), T, n, k, beta_mode, _ptr(ids),
+                                 _ptr(w), ctypes.byref(st), _ptr(ws),
+                                 ws.numel() if ws is not None else 0, _stream(stream)))
+    return ids, w, out
 
 
 def pcm_expand(x, w_gate, w_up, paths: PathTable, u=None, stream=None,
@@ -531,12 +569,24 @@ class LayerPlan:
         self.ids = torch.empty((T, k), dtype=torch.int32, device=device)
         self.w = torch.empty((T, k), dtype=torch.float32, device=device)
         self.paths = PathTable.empty(T, n, k, device)
-        self.ws_paths = _workspace(workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0), device)
+        self.ws_paths = _workspace(max(workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0),
+                                       workspace_bytes(OP_ROUTE_PATHS, T, 0, 0, n, k, 0)), device)
         self.u = torch.empty((T * k, F), dtype=torch.float32, device=device)
         self.ws_proj = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), device)
         self.ws_shared = (_workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, shared_F, 1, 1, dt), device)
                           if shared_F else None)
         self.y = torch.empty((T, H), dtype=torch.float32, device=device)
+
+    def index(self, logits, mask, stream=None):
+        """Route and build the path table: one fused operation when `mask` is the packed
+        int64 layout of pcm_mask_pack, else pcm_route then pcm_build_paths over the u8 mask."""
+        if mask.dtype == torch.int64:
+            pcm_route_paths(logits, mask, self.k, self.beta_mode, self.ids, self.w, out=self.paths,
+                            ws=self.ws_paths, stream=stream)
+        else:
+            pcm_route(logits, self.k, self.ids, self.w, stream=stream)
+            pcm_build_paths(self.ids, self.w, mask, self.beta_mode, out=self.paths, ws=self.ws_paths,
+                            stream=stream)
 
     def forward(self, x, logits, mask, w_gate, w_up, w_down, shared=None, stream=None,
                 tuning: Optional[Tuning] = None):
@@ -546,9 +596,7 @@ class LayerPlan:
         if shared is not None:
             pcm_dense_swiglu(x, *shared, y=self.y, accumulate=False, ws=self.ws_shared, stream=stream,
                              tuning=tuning)
-        pcm_route(logits, self.k, self.ids, self.w, stream=stream)
-        pcm_build_paths(self.ids, self.w, mask, self.beta_mode, out=self.paths, ws=self.ws_paths,
-                        stream=stream)
+        self.index(logits, mask, stream)
         pcm_expand(x, w_gate, w_up, self.paths, u=self.u, stream=stream, tuning=tuning)
         pcm_project_combine(self.u, w_down, self.paths, y=self.y, accumulate=shared is not None,
                             ws=self.ws_proj, stream=stream, tuning=tuning)

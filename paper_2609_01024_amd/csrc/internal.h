@@ -24,6 +24,39 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
 }
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
+// Largest 32-bit value across the wavefront, the same on every lane (all 64 lanes active):
+// DPP moves that pair lane i with i^1, i^2, its mirror in 8 and its mirror in 16 leave each
+// row of 16 lanes with its maximum (each move folds into the max instruction), then the
+// four row maxima are read into scalar registers and compared there.
+template <int CTRL>
+__device__ inline uint32_t dpp_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
+}
+__device__ inline uint32_t wave_max_u32(uint32_t v) {
+    v = max(v, dpp_u32<0xB1>(v));   // quad_perm [1,0,3,2]: lane ^ 1
+    v = max(v, dpp_u32<0x4E>(v));   // quad_perm [2,3,0,1]: lane ^ 2
+    v = max(v, dpp_u32<0x141>(v));  // row_half_mirror: the other quad of 8
+    v = max(v, dpp_u32<0x140>(v));  // row_mirror: the other half of 16
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+// Largest 64-bit value across the wavefront: the largest high word, then, when more than
+// one lane holds it, the largest low word among those lanes.
+__device__ inline uint64_t wave_max_u64(uint64_t v) {
+    const uint32_t hv = (uint32_t)(v >> 32), lv = (uint32_t)v;
+    const uint32_t hi = wave_max_u32(hv);
+    const uint64_t holders = __ballot(hv == hi);
+    uint32_t lo;
+    if (__popcll(holders) == 1)
+        lo = (uint32_t)__builtin_amdgcn_readlane((int)lv, __ffsll((unsigned long long)holders) - 1);
+    else
+        lo = wave_max_u32(hv == hi ? lv : 0u);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 // Launchers (each returns hipGetLastError() of its launches).
 hipError_t launch_route(const float* logits, int64_t T, int n, int k, int32_t* ids, float* w,
                         hipStream_t s);
@@ -37,6 +70,14 @@ hipError_t launch_build_paths(const int32_t* ids, const float* w, const uint8_t*
                               int32_t* offsets, int32_t* row_token, int32_t* row_slot,
                               int32_t* row_of, int32_t* block_counts, hipStream_t s);
 size_t build_paths_ws_bytes(int64_t T, int n);
+// The fused indexing operation (route, path table, dispatch layout) over a packed mask
+// [n][ceil(n/64)] u64, and the packing of a u8 mask.
+hipError_t launch_mask_pack(const uint8_t* mask, int n, uint64_t* packed, hipStream_t s);
+hipError_t launch_route_paths(const float* logits, const uint64_t* packed, int64_t T, int n, int k,
+                              int beta_mode, int32_t* ids, float* w, uint64_t* bits, float* beta,
+                              int32_t* offsets, int32_t* row_token, int32_t* row_slot,
+                              int32_t* row_of, int32_t* block_counts, hipStream_t s);
+size_t route_paths_ws_bytes(int64_t T, int n);
 
 enum GemmMode { kExpand = 0, kDownStore = 1, kDownAccum = 2 };
 

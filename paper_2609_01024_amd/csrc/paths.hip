@@ -87,7 +87,8 @@ __global__ __launch_bounds__(kPathBlock) void paths_kernel(
             for (int a = 0; a < kMaxK; ++a)
 #pragma unroll
                 for (int b = 0; b < kMaxK; ++b)
-                    if (a < k && b < k && ((bits >> (a * k + b)) & 1)) global += p[a] * p[b];
+                    if (a < k && b < k && ((bits >> (a * k + b)) & 1))
+                        global = fmaf(p[a], p[b], global);  // explicit: one rounding per term
             float* bt = beta_out + t * k * k;
 #pragma unroll
             for (int a = 0; a < kMaxK; ++a) {

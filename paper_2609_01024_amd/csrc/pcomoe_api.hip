@@ -149,7 +149,7 @@ PathWs path_ws(int64_t T, int H, int F, int n, int k, pcm_dtype dt) {
 
 extern "C" {
 
-int pcm_abi_version(void) { return 120; }
+int pcm_abi_version(void) { return 121; }
 
 const char* pcm_status_string(pcm_status s) {
     switch (s) {
@@ -166,6 +166,7 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
     if (T < 0 || n < 1 || k < 1) return 0;
     switch (op) {
         case PCM_OP_BUILD_PATHS: return build_paths_ws_bytes(T, n);
+        case PCM_OP_ROUTE_PATHS: return route_paths_ws_bytes(T, n);
         case PCM_OP_EXPAND: return 0;
         case PCM_OP_PROJECT_COMBINE:
             if (H < 1 || F < 1) return 0;
@@ -243,6 +244,36 @@ pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const u
     if (need && !aligned16(ws)) return PCM_ERR_ARG;
     return from_hip(launch_build_paths(topk_ids, topk_w, mask, T, n, k, (int)beta_mode,
                                        out->path_bits, out->beta, out->expert_offsets,
+                                       out->row_token, out->row_slot, out->row_of, (int32_t*)ws,
+                                       (hipStream_t)stream));
+}
+
+pcm_status pcm_mask_pack(const uint8_t* mask, int n, uint64_t* packed, void* stream) {
+    if (n < 1) return PCM_ERR_ARG;
+    if (n > kMaxN) return PCM_ERR_UNSUPPORTED;
+    if (!mask || !packed || !aligned16(mask) || !aligned16(packed)) return PCM_ERR_ARG;
+    return from_hip(launch_mask_pack(mask, n, packed, (hipStream_t)stream));
+}
+
+pcm_status pcm_route_paths(const float* logits, const uint64_t* packed_mask, int64_t T, int n,
+                           int k, pcm_beta_mode beta_mode, int32_t* topk_ids, float* topk_w,
+                           const pcm_paths* out, void* ws, size_t ws_bytes, void* stream) {
+    pcm_status st = check_shape(T, n, k);
+    if (st != PCM_OK) return st;
+    if (beta_mode < PCM_BETA_SRC_COND || beta_mode > PCM_BETA_GLOBAL) return PCM_ERR_ARG;
+    if (T == 0) return PCM_OK;
+    if (!logits || !packed_mask || !topk_ids || !topk_w || check_paths(out) != PCM_OK)
+        return PCM_ERR_ARG;
+    if (!aligned16(logits) || !aligned16(packed_mask) || !aligned16(topk_ids) ||
+        !aligned16(topk_w) || !aligned16(out->path_bits) || !aligned16(out->beta) ||
+        !aligned16(out->expert_offsets) || !aligned16(out->row_token) ||
+        !aligned16(out->row_slot) || !aligned16(out->row_of))
+        return PCM_ERR_ARG;
+    const size_t need = route_paths_ws_bytes(T, n);
+    if (ws_bytes < need || (need && !ws)) return PCM_ERR_WORKSPACE;
+    if (need && !aligned16(ws)) return PCM_ERR_ARG;
+    return from_hip(launch_route_paths(logits, packed_mask, T, n, k, (int)beta_mode, topk_ids,
+                                       topk_w, out->path_bits, out->beta, out->expert_offsets,
                                        out->row_token, out->row_slot, out->row_of, (int32_t*)ws,
                                        (hipStream_t)stream));
 }

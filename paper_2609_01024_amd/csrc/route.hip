@@ -35,11 +35,7 @@ __device__ inline void route_token(const float* l, int n, int k, int lane, int32
         uint64_t best = key[0];
 #pragma unroll
         for (int j = 1; j < EPL; ++j) best = key[j] > best ? key[j] : best;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            const uint64_t o = __shfl_xor(best, off);
-            best = o > best ? o : best;
-        }
+        best = wave_max_u64(best);
         sel[a] = best;
 #pragma unroll
         for (int j = 0; j < EPL; ++j)
@@ -57,6 +53,279 @@ __device__ inline void route_token(const float* l, int n, int k, int lane, int32
             ids_t[a] = (int32_t)(0xFFFFFFFFu - (uint32_t)sel[a]);
             w_t[a] = expf(from_orderable((uint32_t)(sel[a] >> 32)) - top) / s;
         }
+    }
+}
+
+// ------------------------------------------------------------- fused indexing
+// Section 4.3's single indexing operation over the layer's packed mask: route, path filter,
+// path weights and the dispatch layout. A workgroup of 16 waves owns a block of BT tokens
+// (32, or 64 when one block holds every token); wave w takes tokens w, w + 16, ... of it,
+// with all their logits and the packed mask loaded before any store (a wave's loads
+// complete in order with its stores, so a load behind a store would wait for it). Per
+// token, in compact per-lane state (runtime loops over the k slots keep the code small):
+//   - top-k: k rounds of a wave maximum over 64-bit keys as in route_token; lane a keeps
+//     slot a's key, then lanes a < k take their exponentials and the softmax denominator
+//     is summed in slot order, as route_token sums it;
+//   - paths: lane a*k + b < k^2 tests (a, b) against the mask (diagonal set); one ballot
+//     gives the token's bits; the same lane forms beta_ab in the path build's order of
+//     operations (slot weights broadcast by readlane), so both give the same bits;
+//   - dispatch: lane a < k ORs the token's bit into an LDS bitset of its expert.
+// Popcounts of the bitsets are the block's rows per expert, and a row's rank among its
+// expert's rows in the block is the popcount of the bits below its token, so no
+// order-dependent atomic decides an index. A single block (T <= 64) finishes the layout in
+// the same launch; otherwise each block writes its counts and route_scatter_kernel places
+// the rows.
+constexpr int kIdxCount = 32;    // tokens per counting block
+constexpr int kIdxFused = 64;    // tokens of the single-launch case
+constexpr int kIdxScatter = 128; // tokens per placing block (whole counting blocks)
+constexpr int kIdxWaves = 16;
+constexpr int kIdxThreads = 64 * kIdxWaves;
+static_assert(kIdxScatter % kIdxCount == 0 && kIdxScatter * kMaxK == kIdxThreads, "layout");
+
+__device__ inline float readlane_f32(float v, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Exclusive scan of v over threads 0..kMaxN-1 of the workgroup (the first four waves; every
+// thread of the workgroup must call it): wave scans by shuffles, then the wave totals.
+// Returns the exclusive prefix to threads < kMaxN and the total in *total for all threads.
+__device__ inline int scan_columns(int v, int* wave_tot, int* total) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int incl = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int o = __shfl_up(incl, d);
+        if (lane >= d) incl += o;
+    }
+    if (tid < kMaxN && lane == 63) wave_tot[wave] = incl;
+    __syncthreads();
+    int base = 0, all = 0;
+#pragma unroll
+    for (int q = 0; q < kMaxN / 64; ++q) {
+        const int c = wave_tot[q];
+        base += q < wave ? c : 0;
+        all += c;
+    }
+    *total = all;
+    return base + incl - v;
+}
+
+template <int EPL, bool FUSED>
+__global__ __launch_bounds__(kIdxThreads) void route_paths_kernel(
+    const float* __restrict__ logits, const uint64_t* __restrict__ packed, int64_t T, int n, int k,
+    int beta_mode, int32_t* __restrict__ ids, float* __restrict__ w, uint64_t* __restrict__ bits_out,
+    float* __restrict__ beta_out, int32_t* __restrict__ offsets, int32_t* __restrict__ row_token,
+    int32_t* __restrict__ row_slot, int32_t* __restrict__ row_of, int32_t* __restrict__ block_counts) {
+    constexpr int BT = FUSED ? kIdxFused : kIdxCount;
+    constexpr int PER = BT / kIdxWaves;  // tokens per wave, one after another
+    __shared__ unsigned long long words[kMaxN];
+    __shared__ uint64_t mask_s[kMaxN * (kMaxN / 64)];
+    __shared__ int tok_e[FUSED ? BT : 1][kMaxK];
+    __shared__ int scan[FUSED ? kMaxN : 1];
+    __shared__ int wave_tot[kMaxN / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int x = tid; x < kMaxN; x += kIdxThreads) words[x] = 0ull;
+    const int W = (n + 63) / 64;  // packed words per mask row
+    const int64_t t0 = (int64_t)blockIdx.x * BT;
+    float lv[PER][EPL];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int64_t t = t0 + j * kIdxWaves + wave;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+            const int x = lane + 64 * q;
+            lv[j][q] = (t < T && x < n) ? logits[t * n + x] : 0.0f;
+        }
+    }
+    for (int x = tid; x < n * W; x += kIdxThreads) mask_s[x] = packed[x];
+    __syncthreads();  // words cleared, mask staged
+    const int pa_ = lane / k, pb_ = lane - (lane / k) * k;  // path (a, b) of this lane
+    const bool in = lane < k * k;
+    for (int j = 0; j < PER; ++j) {
+        const int tib = j * kIdxWaves + wave;
+        const int64_t t = t0 + tib;
+        if (t >= T) break;  // wave-uniform
+        uint64_t key[EPL];
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+            const int x = lane + 64 * q;
+            key[q] = x < n ? ((uint64_t)orderable(lv[0][q]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)x)
+                           : 0ull;  // every real key is > 0
+        }
+#pragma unroll
+        for (int jj = 0; jj + 1 < PER; ++jj)  // the next token's logits move up
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) lv[jj][q] = lv[jj + 1][q];
+        uint64_t mine = 0ull, first = 0ull;  // slot `lane`'s key (lanes < k), slot 0's key
+        for (int a = 0; a < k; ++a) {
+            uint64_t best = key[0];
+#pragma unroll
+            for (int q = 1; q < EPL; ++q) best = key[q] > best ? key[q] : best;
+            best = wave_max_u64(best);
+            if (a == 0) first = best;
+            if (lane == a) mine = best;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q)
+                if (key[q] == best) key[q] = 0ull;
+        }
+        // softmax over the selected logits, shifted by the largest, summed in slot order
+        const float top = from_orderable((uint32_t)(first >> 32));
+        const float ex = lane < k ? expf(from_orderable((uint32_t)(mine >> 32)) - top) : 0.0f;
+        float s = 0.0f;
+        for (int a = 0; a < k; ++a) s += readlane_f32(ex, a);
+        const int e = lane < k ? (int)(0xFFFFFFFFu - (uint32_t)mine) : 0;
+        const float p = lane < k ? ex / s : 0.0f;
+        if (lane < k) {
+            ids[t * k + lane] = e;
+            w[t * k + lane] = p;
+        }
+        // path (a, b) of this lane: the slots' experts and weights by cross-lane reads
+        const int ea = __shfl(e, pa_), eb = __shfl(e, pb_);
+        const float pa = __shfl(p, pa_), pb = __shfl(p, pb_);
+        const bool on = in && (pa_ == pb_ || ((mask_s[ea * W + (eb >> 6)] >> (eb & 63)) & 1ull));
+        const uint64_t bits = __ballot(on);
+        if (lane == 0) bits_out[t] = bits;
+        float den = 1.0f;
+        if (beta_mode == 0) {
+            den = 0.0f;  // sum of p over the targets of this lane's source a, b ascending
+            const int row = in ? pa_ * k : 0;
+            for (int bb = 0; bb < k; ++bb) {
+                const float pbb = readlane_f32(p, bb);
+                if ((bits >> (row + bb)) & 1) den += pbb;
+            }
+        } else if (beta_mode == 2) {
+            den = 0.0f;  // sum of p_a' p_b' over the token's paths, (a', b') ascending
+            for (int aa = 0; aa < k; ++aa) {
+                const float paa = readlane_f32(p, aa);
+                for (int bb = 0; bb < k; ++bb) {
+                    const float pbb = readlane_f32(p, bb);
+                    if ((bits >> (aa * k + bb)) & 1) den = fmaf(paa, pbb, den);
+                }
+            }
+        }
+        if (in) {
+            float v = 0.0f;
+            if (on) v = beta_mode == 0 ? pa * (pb / den) : (beta_mode == 1 ? pa * pb : pa * pb / den);
+            beta_out[t * k * k + lane] = v;
+        }
+        if (lane < k) {
+            atomicOr(&words[e], 1ull << tib);
+            if constexpr (FUSED) tok_e[tib][lane] = e;
+        }
+    }
+    __syncthreads();
+    if constexpr (!FUSED) {
+        for (int x = tid; x < n; x += kIdxThreads)
+            block_counts[(int64_t)blockIdx.x * n + x] = __popcll(words[x]);
+    } else {
+        // the one block holds every token: exclusive scan of its counts, then every row
+        const int own = tid < n ? __popcll(words[tid]) : 0;
+        int total;
+        const int excl = scan_columns(own, wave_tot, &total);
+        if (tid < kMaxN) scan[tid] = excl;
+        if (tid < n) offsets[tid] = excl;
+        if (tid == 0) offsets[n] = total;
+        __syncthreads();
+        const int ntok = (int)T;
+        for (int i = tid; i < ntok * k; i += kIdxThreads) {
+            const int tib = i / k, a = i - (i / k) * k;
+            const int x = tok_e[tib][a];
+            const int pos = scan[x] + __popcll(words[x] & ((1ull << tib) - 1ull));
+            row_token[pos] = (int32_t)tib;
+            row_slot[pos] = a;
+            row_of[(int64_t)tib * k + a] = pos;
+        }
+    }
+}
+
+// Rows of kIdxScatter tokens (whole counting blocks) once every counting block has written
+// its counts [NB][n]: each workgroup reduces the count table itself (column totals, and the
+// column sums over the counting blocks before its own; integer sums, so the order of the
+// LDS atomics does not matter), scans the totals into the expert offsets (written by
+// workgroup 0), rebuilds its bitsets from the top-k ids (one 64-bit word per 64 tokens) and
+// places its rows.
+__global__ __launch_bounds__(kIdxThreads) void route_scatter_kernel(
+    const int32_t* __restrict__ ids, int64_t T, int n, int k, const int32_t* __restrict__ block_counts,
+    int64_t NB, int32_t* __restrict__ offsets, int32_t* __restrict__ row_token,
+    int32_t* __restrict__ row_slot, int32_t* __restrict__ row_of) {
+    constexpr int NW = kIdxScatter / 64;
+    constexpr int UN = 16;  // count loads in flight per thread
+    __shared__ unsigned long long words[NW][kMaxN];
+    __shared__ int tot[kMaxN];
+    __shared__ int before[kMaxN];
+    __shared__ int first[kMaxN];
+    __shared__ int wave_tot[kMaxN / 64];
+    const int tid = threadIdx.x;
+    const int64_t me = blockIdx.x;
+    const int64_t b_me = me * (kIdxScatter / kIdxCount);  // first counting block of this one
+    // this thread's row (token tib, slot a), loaded ahead of the count table
+    const int tib = tid / kMaxK, a = tid - (tid / kMaxK) * kMaxK;
+    const int64_t t = me * kIdxScatter + tib;
+    const bool valid = a < k && t < T;
+    int e = 0;
+    if (valid) {
+        const int v = ids[t * k + a];
+        e = v < 0 ? 0 : (v >= n ? n - 1 : v);
+    }
+    int np = 1;
+    while (np < n) np <<= 1;
+    const int G = kIdxThreads / np;  // groups of counting blocks per column, >= 4
+    const int x = tid % np, g = tid / np;
+    for (int i = tid; i < NW * kMaxN; i += kIdxThreads) (&words[0][0])[i] = 0ull;
+    for (int i = tid; i < kMaxN; i += kIdxThreads) tot[i] = before[i] = 0;
+    __syncthreads();
+    int st = 0, sb = 0;
+    if (x < n) {
+        for (int64_t b0 = g; b0 < NB; b0 += (int64_t)UN * G) {
+            int c[UN];
+#pragma unroll
+            for (int u = 0; u < UN; ++u) {
+                const int64_t b = b0 + (int64_t)u * G;
+                c[u] = b < NB ? block_counts[b * n + x] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < UN; ++u) {
+                st += c[u];
+                sb += b0 + (int64_t)u * G < b_me ? c[u] : 0;
+            }
+        }
+        if (st) atomicAdd(&tot[x], st);
+        if (sb) atomicAdd(&before[x], sb);
+    }
+    __syncthreads();
+    const int own = tid < n ? tot[tid] : 0;
+    int total;
+    const int excl = scan_columns(own, wave_tot, &total);
+    if (me == 0) {
+        if (tid < n) offsets[tid] = excl;
+        if (tid == 0) offsets[n] = total;
+    }
+    if (tid < n) first[tid] = excl + before[tid];
+    if (valid) atomicOr(&words[tib >> 6][e], 1ull << (tib & 63));
+    __syncthreads();
+    if (valid) {
+        const int wd = tib >> 6;
+        int pos = first[e] + __popcll(words[wd][e] & ((1ull << (tib & 63)) - 1ull));
+#pragma unroll
+        for (int q = 0; q < NW; ++q)
+            if (q < wd) pos += __popcll(words[q][e]);
+        row_token[pos] = (int32_t)t;
+        row_slot[pos] = a;
+        row_of[t * k + a] = pos;
+    }
+}
+
+// Offline per-layer mask layout: bit j % 64 of word [i][j / 64] is set when path i -> j is
+// allowed (mask[i][j] != 0, or i == j).
+__global__ __launch_bounds__(256) void mask_pack_kernel(const uint8_t* __restrict__ mask, int n,
+                                                        uint64_t* __restrict__ packed) {
+    const int W = (n + 63) / 64;
+    const int i = blockIdx.x;  // one mask row per workgroup
+    for (int wd = threadIdx.x / 64; wd < W; wd += 4) {
+        const int j = wd * 64 + (threadIdx.x & 63);
+        const bool on = j < n && (j == i || mask[(int64_t)i * n + j] != 0);
+        const uint64_t b = __ballot(on);
+        if ((threadIdx.x & 63) == 0) packed[(int64_t)i * W + wd] = b;
     }
 }
 
@@ -201,6 +470,49 @@ hipError_t launch_route(const float* logits, int64_t T, int n, int k, int32_t* i
         case 3: route_kernel<3><<<grid, block, 0, s>>>(logits, T, n, k, ids, w); break;
         default: route_kernel<4><<<grid, block, 0, s>>>(logits, T, n, k, ids, w); break;
     }
+    return hipGetLastError();
+}
+
+size_t route_paths_ws_bytes(int64_t T, int n) {
+    if (T <= kIdxFused) return 0;
+    return align_up((size_t)ceil_div(T, kIdxCount) * n * sizeof(int32_t), 256);
+}
+
+hipError_t launch_mask_pack(const uint8_t* mask, int n, uint64_t* packed, hipStream_t s) {
+    mask_pack_kernel<<<(unsigned)n, 256, 0, s>>>(mask, n, packed);
+    return hipGetLastError();
+}
+
+hipError_t launch_route_paths(const float* logits, const uint64_t* packed, int64_t T, int n, int k,
+                              int beta_mode, int32_t* ids, float* w, uint64_t* bits, float* beta,
+                              int32_t* offsets, int32_t* row_token, int32_t* row_slot,
+                              int32_t* row_of, int32_t* block_counts, hipStream_t s) {
+    const int epl = (int)ceil_div(n, 64);
+    auto go = [&](auto kern, int64_t blocks) {
+        kern<<<(unsigned)blocks, kIdxThreads, 0, s>>>(logits, packed, T, n, k, beta_mode, ids, w,
+                                                      bits, beta, offsets, row_token, row_slot,
+                                                      row_of, block_counts);
+    };
+    if (T <= kIdxFused) {
+        switch (epl) {
+            case 1: go(route_paths_kernel<1, true>, 1); break;
+            case 2: go(route_paths_kernel<2, true>, 1); break;
+            case 3: go(route_paths_kernel<3, true>, 1); break;
+            default: go(route_paths_kernel<4, true>, 1); break;
+        }
+        return hipGetLastError();
+    }
+    const int64_t NB = ceil_div(T, kIdxCount);
+    switch (epl) {
+        case 1: go(route_paths_kernel<1, false>, NB); break;
+        case 2: go(route_paths_kernel<2, false>, NB); break;
+        case 3: go(route_paths_kernel<3, false>, NB); break;
+        default: go(route_paths_kernel<4, false>, NB); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    route_scatter_kernel<<<(unsigned)ceil_div(T, kIdxScatter), kIdxThreads, 0, s>>>(
+        ids, T, n, k, block_counts, NB, offsets, row_token, row_slot, row_of);
     return hipGetLastError();
 }
 

@@ -31,16 +31,6 @@ __device__ inline float from_orderable(uint32_t k) {
     return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
-__device__ inline uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const uint32_t lo = __shfl_xor((uint32_t)v, off), hi = __shfl_xor((uint32_t)(v >> 32), off);
-        const uint64_t o = ((uint64_t)hi << 32) | lo;
-        v = o > v ? o : v;
-    }
-    return v;
-}
-
 // Active pairs of the [n,n] mask (diagonal always active) in ascending i*n + j, one row
 // per step of a single 256-thread workgroup (one thread per column).
 __global__ __launch_bounds__(256) void layout_kernel(const uint8_t* __restrict__ mask,

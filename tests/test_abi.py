@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert L.pcm_abi_version() == 120
+    assert L.pcm_abi_version() == 121
     for s in (OK, ARG, UNSUP, WS, HIP):
         assert L.pcm_status_string(s).decode().startswith("PCM_")
     assert L.pcm_status_string(77) == b"unknown pcm_status"
@@ -119,6 +119,44 @@ def test_build_paths_rejects_misaligned_pointers(L):
                                  None) == ARG, f
     assert L.pcm_build_paths(FAKE, FAKE, FAKE, 5000, 64, 8, 0, ctypes.byref(p), mis, need,
                              None) == ARG                                    # workspace
+
+
+def test_mask_pack_and_route_paths_validation(L):
+    mis = ctypes.c_void_p(0x10008)
+    assert L.pcm_mask_pack(FAKE, 0, FAKE, None) == ARG                 # n < 1
+    assert L.pcm_mask_pack(FAKE, 300, FAKE, None) == UNSUP             # n > 256
+    assert L.pcm_mask_pack(None, 8, FAKE, None) == ARG
+    assert L.pcm_mask_pack(FAKE, 8, mis, None) == ARG                  # misaligned packed
+    p = _paths()
+    bp = ctypes.byref(p)
+    # up to 64 tokens need no workspace; more hold the counts [ceil(T / 32)][n] i32
+    assert L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 64, 0, 0, 256, 8, 0) == 0
+    assert L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 65, 0, 0, 60, 4, 0) == 768
+    need = L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 8192, 0, 0, 64, 8, 0)
+    assert need == 256 * 64 * 4
+    args = lambda T=8192, n=64, k=8, beta=0, q=bp, ws=FAKE, wsb=need: (
+        FAKE, FAKE, T, n, k, beta, FAKE, FAKE, q, ws, wsb, None)
+    assert L.pcm_route_paths(*args(k=9)) == UNSUP                      # k > 8
+    assert L.pcm_route_paths(*args(n=300)) == UNSUP                    # n > 256
+    assert L.pcm_route_paths(*args(n=4)) == ARG                        # k > n
+    assert L.pcm_route_paths(*args(beta=3)) == ARG
+    assert L.pcm_route_paths(*args(wsb=need - 1)) == WS
+    assert L.pcm_route_paths(*args(ws=None)) == WS
+    assert L.pcm_route_paths(*args(ws=mis)) == ARG
+    assert L.pcm_route_paths(*args(T=0, q=None, ws=None, wsb=0)) == OK  # T = 0 no-op
+    for f, _ in binding.PcmPaths._fields_:
+        q = _paths(f)
+        assert L.pcm_route_paths(*args(q=ctypes.byref(q))) == ARG, f
+        vals = {g: 0x10000 for g, _ in binding.PcmPaths._fields_}
+        vals[f] = 0x10008
+        q = binding.PcmPaths(**vals)
+        assert L.pcm_route_paths(*args(q=ctypes.byref(q))) == ARG, f
+    for i in (0, 1, 6, 7):  # logits, packed mask, topk_ids, topk_w
+        a = list(args())
+        a[i] = None
+        assert L.pcm_route_paths(*a) == ARG, i
+        a[i] = mis
+        assert L.pcm_route_paths(*a) == ARG, i
 
 
 def test_tuning_validation(L):
