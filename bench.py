@@ -286,7 +286,7 @@ def measure(pcm, name, cfg, d, args, flush, scored):
         else:
             if fused:
                 pcm.pcm_route_paths(logits, packed, cfg.k, 0, plan.ids, plan.w, out=plan.paths,
-                                    ws=plan.ws_paths)
+                                    ws=plan.ws_index)
             else:
                 pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
                 mark()

@@ -136,13 +136,18 @@ pcm_status pcm_mask_pack(const uint8_t* mask, int n, uint64_t* packed, void* str
 
 /* Section 4.3's fused indexing operation: pcm_route's top-k and softmax, pcm_build_paths's
  * path bits and beta, and the grouped dispatch layout, from the logits and a packed mask.
- * One launch when T <= 64; otherwise a launch that routes, forms the path table and counts
- * rows per (32-token block, expert), then one that places the rows. Outputs are
+ * One launch when T <= 64 (one token per wavefront; the last workgroup to finish builds the
+ * dispatch layout); otherwise a launch that routes, forms the path table and counts rows
+ * per (32-token block, expert), then one that places the rows. Outputs are
  * bit-identical to pcm_route followed by pcm_build_paths with the mask that packed_mask
  * was packed from, and deterministic. logits [T,n] f32 (device); packed_mask from
  * pcm_mask_pack; topk_ids [T,k] i32 and topk_w [T,k] f32 (device) as pcm_route; *out as
  * pcm_build_paths (all of its arrays written). Limits and errors as pcm_build_paths.
- * ws: pcm_workspace_bytes(PCM_OP_ROUTE_PATHS, T, 0, 0, n, k, 0) bytes (0 when T <= 64). */
+ * ws: pcm_workspace_bytes(PCM_OP_ROUTE_PATHS, T, 0, 0, n, k, 0) bytes (device, 16-byte
+ * aligned; 256 when T <= 64). Its first 256 bytes hold a completion counter of the
+ * single-launch case: they must be zero before the first call that uses this workspace,
+ * and every call leaves them zero (the rest needs no initialisation). Calls that overlap
+ * in time must not share a workspace. */
 pcm_status pcm_route_paths(const float* logits, const uint64_t* packed_mask, int64_t T, int n,
                            int k, pcm_beta_mode beta_mode, int32_t* topk_ids, float* topk_w,
                            const pcm_paths* out, void* ws, size_t ws_bytes, void* stream);

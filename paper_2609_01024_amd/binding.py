@@ -301,6 +301,13 @@ def pcm_mask_pack(mask: torch.Tensor, packed: torch.Tensor = None, stream=None) 
     return packed
 
 
+def route_paths_workspace(T: int, n: int, k: int, device) -> torch.Tensor:
+    """A workspace for pcm_route_paths, zero-filled (its completion counter starts at zero and
+    every call leaves it there, so the workspace can be reused as it is)."""
+    return torch.zeros((workspace_bytes(OP_ROUTE_PATHS, T, 0, 0, n, k, 0),), dtype=torch.uint8,
+                       device=device)
+
+
 def pcm_route_paths(logits, packed_mask, k: int, beta_mode: int = BETA_SRC_COND, topk_ids=None,
                     topk_w=None, out: PathTable = None, ws: torch.Tensor = None, stream=None):
     """Fused indexing: (topk_ids, topk_w, PathTable) from the logits and a packed mask."""
@@ -313,7 +320,7 @@ def pcm_route_paths(logits, packed_mask, k: int, beta_mode: int = BETA_SRC_COND,
         w = topk_w if topk_w is not None else torch.empty((T, k), dtype=torch.float32, device=dev)
         out = out or PathTable.empty(T, n, k, dev)
         if ws is None:
-            ws = _workspace(need, dev)
+            ws = route_paths_workspace(T, n, k, dev)
     _dev(ids, w)
     st = out.struct()
     _check(lib().pcm_route_paths(_ptr(logits), _ptr(packed_mask), T, n, k, beta_mode, _ptr(ids),
@@ -569,8 +576,8 @@ class LayerPlan:
         self.ids = torch.empty((T, k), dtype=torch.int32, device=device)
         self.w = torch.empty((T, k), dtype=torch.float32, device=device)
         self.paths = PathTable.empty(T, n, k, device)
-        self.ws_paths = _workspace(max(workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0),
-                                       workspace_bytes(OP_ROUTE_PATHS, T, 0, 0, n, k, 0)), device)
+        self.ws_paths = _workspace(workspace_bytes(OP_BUILD_PATHS, T, 0, 0, n, k, 0), device)
+        self.ws_index = route_paths_workspace(T, n, k, device)
         self.u = torch.empty((T * k, F), dtype=torch.float32, device=device)
         self.ws_proj = _workspace(workspace_bytes(OP_PROJECT_COMBINE, T, H, F, n, k, dt), device)
         self.ws_shared = (_workspace(workspace_bytes(OP_DENSE_SWIGLU, T, H, shared_F, 1, 1, dt), device)
@@ -582,7 +589,7 @@ class LayerPlan:
         int64 layout of pcm_mask_pack, else pcm_route then pcm_build_paths over the u8 mask."""
         if mask.dtype == torch.int64:
             pcm_route_paths(logits, mask, self.k, self.beta_mode, self.ids, self.w, out=self.paths,
-                            ws=self.ws_paths, stream=stream)
+                            ws=self.ws_index, stream=stream)
         else:
             pcm_route(logits, self.k, self.ids, self.w, stream=stream)
             pcm_build_paths(self.ids, self.w, mask, self.beta_mode, out=self.paths, ws=self.ws_paths,

@@ -76,7 +76,7 @@ hipError_t launch_mask_pack(const uint8_t* mask, int n, uint64_t* packed, hipStr
 hipError_t launch_route_paths(const float* logits, const uint64_t* packed, int64_t T, int n, int k,
                               int beta_mode, int32_t* ids, float* w, uint64_t* bits, float* beta,
                               int32_t* offsets, int32_t* row_token, int32_t* row_slot,
-                              int32_t* row_of, int32_t* block_counts, hipStream_t s);
+                              int32_t* row_of, void* ws, hipStream_t s);
 size_t route_paths_ws_bytes(int64_t T, int n);
 
 enum GemmMode { kExpand = 0, kDownStore = 1, kDownAccum = 2 };

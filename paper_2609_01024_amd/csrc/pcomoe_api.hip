@@ -270,11 +270,11 @@ pcm_status pcm_route_paths(const float* logits, const uint64_t* packed_mask, int
         !aligned16(out->row_slot) || !aligned16(out->row_of))
         return PCM_ERR_ARG;
     const size_t need = route_paths_ws_bytes(T, n);
-    if (ws_bytes < need || (need && !ws)) return PCM_ERR_WORKSPACE;
-    if (need && !aligned16(ws)) return PCM_ERR_ARG;
+    if (ws_bytes < need || !ws) return PCM_ERR_WORKSPACE;
+    if (!aligned16(ws)) return PCM_ERR_ARG;
     return from_hip(launch_route_paths(logits, packed_mask, T, n, k, (int)beta_mode, topk_ids,
                                        topk_w, out->path_bits, out->beta, out->expert_offsets,
-                                       out->row_token, out->row_slot, out->row_of, (int32_t*)ws,
+                                       out->row_token, out->row_slot, out->row_of, ws,
                                        (hipStream_t)stream));
 }
 

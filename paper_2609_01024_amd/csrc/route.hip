@@ -58,35 +58,40 @@ __device__ inline void route_token(const float* l, int n, int k, int lane, int32
 
 // ------------------------------------------------------------- fused indexing
 // Section 4.3's single indexing operation over the layer's packed mask: route, path filter,
-// path weights and the dispatch layout. A workgroup of 16 waves owns a block of BT tokens
-// (32, or 64 when one block holds every token); wave w takes tokens w, w + 16, ... of it,
-// with all their logits and the packed mask loaded before any store (a wave's loads
-// complete in order with its stores, so a load behind a store would wait for it). Per
-// token, in compact per-lane state (runtime loops over the k slots keep the code small):
+// path weights and the dispatch layout. Per token, one wavefront, in compact per-lane state
+// (runtime loops over the k slots keep the code small), index_token:
 //   - top-k: k rounds of a wave maximum over 64-bit keys as in route_token; lane a keeps
 //     slot a's key, then lanes a < k take their exponentials and the softmax denominator
 //     is summed in slot order, as route_token sums it;
 //   - paths: lane a*k + b < k^2 tests (a, b) against the mask (diagonal set); one ballot
 //     gives the token's bits; the same lane forms beta_ab in the path build's order of
-//     operations (slot weights broadcast by readlane), so both give the same bits;
-//   - dispatch: lane a < k ORs the token's bit into an LDS bitset of its expert.
-// Popcounts of the bitsets are the block's rows per expert, and a row's rank among its
-// expert's rows in the block is the popcount of the bits below its token, so no
-// order-dependent atomic decides an index. A single block (T <= 64) finishes the layout in
-// the same launch; otherwise each block writes its counts and route_scatter_kernel places
-// the rows.
-constexpr int kIdxCount = 32;    // tokens per counting block
-constexpr int kIdxFused = 64;    // tokens of the single-launch case
+//     operations (slot weights broadcast by readlane), so both give the same bits.
+// The dispatch layout orders rows by (expert, token): a token's bit in a per-expert LDS
+// bitset, popcounts for counts, and the popcount of the bits below a token for its rank, so
+// no order-dependent atomic decides an index. Two launch shapes:
+//   - T <= 64: one token per wave, 4 waves per workgroup; after its tokens each workgroup
+//     takes a ticket, and the last one reads every token's experts back and builds the
+//     whole layout (one launch);
+//   - otherwise workgroups of 16 waves own kIdxCount tokens each, write their per-expert
+//     counts, and route_scatter_kernel places the rows (two launches).
+// Every workgroup loads its logits and the packed mask before its first store (a wave's
+// loads complete in order with its stores, so a load behind a store would wait for it).
+#ifndef PCM_IDX_COUNT
+#define PCM_IDX_COUNT 32
+#endif
+constexpr int kIdxCount = PCM_IDX_COUNT;    // tokens per counting block
+constexpr int kIdxSmall = 64;    // largest T of the single-launch case
 constexpr int kIdxScatter = 128; // tokens per placing block (whole counting blocks)
 constexpr int kIdxWaves = 16;
 constexpr int kIdxThreads = 64 * kIdxWaves;
+constexpr int kIdxSmallWaves = 4;
 static_assert(kIdxScatter % kIdxCount == 0 && kIdxScatter * kMaxK == kIdxThreads, "layout");
 
 __device__ inline float readlane_f32(float v, int lane) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// Exclusive scan of v over threads 0..kMaxN-1 of the workgroup (the first four waves; every
+// Exclusive scan of v over threads 0..kMaxN-1 of the workgroup (its first four waves; every
 // thread of the workgroup must call it): wave scans by shuffles, then the wave totals.
 // Returns the exclusive prefix to threads < kMaxN and the total in *total for all threads.
 __device__ inline int scan_columns(int v, int* wave_tot, int* total) {
@@ -110,130 +115,198 @@ __device__ inline int scan_columns(int v, int* wave_tot, int* total) {
     return base + incl - v;
 }
 
-template <int EPL, bool FUSED>
+// Logits of token t (zeros past T) as this lane's EPL values.
+template <int EPL>
+__device__ inline void load_logits(const float* logits, int64_t t, int64_t T, int n, int lane,
+                                   float (&lv)[EPL]) {
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+        const int x = lane + 64 * q;
+        lv[q] = (t < T && x < n) ? logits[t * n + x] : 0.0f;
+    }
+}
+
+// One token by one wavefront (all 64 lanes active): writes its top-k ids and weights, path
+// bits and beta; returns its slot expert to lanes < k (0 elsewhere). mask_s: the packed mask
+// in LDS, W words per row. pa_ = lane / k, pb_ = lane % k.
+template <int EPL>
+__device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s, int W, int n,
+                                  int k, int beta_mode, int64_t t, int lane, int pa_, int pb_,
+                                  int32_t* ids, float* w, uint64_t* bits_out, float* beta_out) {
+    uint64_t key[EPL];
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+        const int x = lane + 64 * q;
+        key[q] = x < n ? ((uint64_t)orderable(lv[q]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)x)
+                       : 0ull;  // every real key is > 0
+    }
+    // the lane's keys in descending order, so that each round looks at key[0] only and the
+    // lane holding the round's maximum pops it
+    auto order = [&](int i, int j) {
+        const uint64_t hi = key[i] > key[j] ? key[i] : key[j], lo = key[i] > key[j] ? key[j] : key[i];
+        key[i] = hi;
+        key[j] = lo;
+    };
+    if constexpr (EPL == 2) order(0, 1);
+    if constexpr (EPL == 3) { order(0, 1); order(1, 2); order(0, 1); }
+    if constexpr (EPL == 4) { order(0, 1); order(2, 3); order(0, 2); order(1, 3); order(1, 2); }
+    uint64_t mine = 0ull, first = 0ull;  // slot `lane`'s key (lanes < k), slot 0's key
+    for (int a = 0; a < k; ++a) {
+        const uint64_t best = wave_max_u64(key[0]);
+        if (a == 0) first = best;
+        if (lane == a) mine = best;
+        if (key[0] == best) {
+#pragma unroll
+            for (int q = 0; q + 1 < EPL; ++q) key[q] = key[q + 1];
+            key[EPL - 1] = 0ull;
+        }
+    }
+    // softmax over the selected logits, shifted by the largest, summed in slot order
+    const float top = from_orderable((uint32_t)(first >> 32));
+    const float ex = lane < k ? expf(from_orderable((uint32_t)(mine >> 32)) - top) : 0.0f;
+    float s = 0.0f;
+    for (int a = 0; a < k; ++a) s += readlane_f32(ex, a);
+    const int e = lane < k ? (int)(0xFFFFFFFFu - (uint32_t)mine) : 0;
+    const float p = lane < k ? ex / s : 0.0f;
+    if (lane < k) {
+        ids[t * k + lane] = e;
+        w[t * k + lane] = p;
+    }
+    // path (a, b) of this lane: the slots' experts and weights by cross-lane reads
+    const bool in = lane < k * k;
+    const int ea = __shfl(e, pa_), eb = __shfl(e, pb_);
+    const float pa = __shfl(p, pa_), pb = __shfl(p, pb_);
+    const bool on = in && (pa_ == pb_ || ((mask_s[ea * W + (eb >> 6)] >> (eb & 63)) & 1ull));
+    const uint64_t bits = __ballot(on);
+    if (lane == 0) bits_out[t] = bits;
+    float den = 1.0f;
+    if (beta_mode == 0) {
+        den = 0.0f;  // sum of p over the targets of this lane's source a, b ascending
+        const int row = in ? pa_ * k : 0;
+        for (int bb = 0; bb < k; ++bb) {
+            const float pbb = readlane_f32(p, bb);
+            if ((bits >> (row + bb)) & 1) den += pbb;
+        }
+    } else if (beta_mode == 2) {
+        den = 0.0f;  // sum of p_a' p_b' over the token's paths, (a', b') ascending
+        for (int aa = 0; aa < k; ++aa) {
+            const float paa = readlane_f32(p, aa);
+            for (int bb = 0; bb < k; ++bb) {
+                const float pbb = readlane_f32(p, bb);
+                if ((bits >> (aa * k + bb)) & 1) den = fmaf(paa, pbb, den);
+            }
+        }
+    }
+    if (in) {
+        float v = 0.0f;
+        if (on) v = beta_mode == 0 ? pa * (pb / den) : (beta_mode == 1 ? pa * pb : pa * pb / den);
+        beta_out[t * k * k + lane] = v;
+    }
+    return e;
+}
+
+// T > 64: kIdxCount tokens per workgroup of 16 waves (wave w takes tokens w, w + 16, ...);
+// writes the block's rows per expert to block_counts[blockIdx][n].
+template <int EPL>
 __global__ __launch_bounds__(kIdxThreads) void route_paths_kernel(
     const float* __restrict__ logits, const uint64_t* __restrict__ packed, int64_t T, int n, int k,
     int beta_mode, int32_t* __restrict__ ids, float* __restrict__ w, uint64_t* __restrict__ bits_out,
-    float* __restrict__ beta_out, int32_t* __restrict__ offsets, int32_t* __restrict__ row_token,
-    int32_t* __restrict__ row_slot, int32_t* __restrict__ row_of, int32_t* __restrict__ block_counts) {
-    constexpr int BT = FUSED ? kIdxFused : kIdxCount;
-    constexpr int PER = BT / kIdxWaves;  // tokens per wave, one after another
+    float* __restrict__ beta_out, int32_t* __restrict__ block_counts) {
+    constexpr int PER = kIdxCount / kIdxWaves;  // tokens per wave, one after another
     __shared__ unsigned long long words[kMaxN];
     __shared__ uint64_t mask_s[kMaxN * (kMaxN / 64)];
-    __shared__ int tok_e[FUSED ? BT : 1][kMaxK];
-    __shared__ int scan[FUSED ? kMaxN : 1];
-    __shared__ int wave_tot[kMaxN / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int x = tid; x < kMaxN; x += kIdxThreads) words[x] = 0ull;
     const int W = (n + 63) / 64;  // packed words per mask row
-    const int64_t t0 = (int64_t)blockIdx.x * BT;
+    const int64_t t0 = (int64_t)blockIdx.x * kIdxCount;
     float lv[PER][EPL];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int64_t t = t0 + j * kIdxWaves + wave;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-            const int x = lane + 64 * q;
-            lv[j][q] = (t < T && x < n) ? logits[t * n + x] : 0.0f;
-        }
-    }
+    for (int j = 0; j < PER; ++j) load_logits<EPL>(logits, t0 + j * kIdxWaves + wave, T, n, lane, lv[j]);
     for (int x = tid; x < n * W; x += kIdxThreads) mask_s[x] = packed[x];
     __syncthreads();  // words cleared, mask staged
-    const int pa_ = lane / k, pb_ = lane - (lane / k) * k;  // path (a, b) of this lane
-    const bool in = lane < k * k;
+    const int pa_ = lane / k, pb_ = lane - (lane / k) * k;
+#pragma unroll
     for (int j = 0; j < PER; ++j) {
         const int tib = j * kIdxWaves + wave;
         const int64_t t = t0 + tib;
         if (t >= T) break;  // wave-uniform
-        uint64_t key[EPL];
+        const int e = index_token<EPL>(lv[j], mask_s, W, n, k, beta_mode, t, lane, pa_, pb_, ids, w,
+                                       bits_out, beta_out);
+        if (lane < k) atomicOr(&words[e], 1ull << tib);
+    }
+    __syncthreads();
+    for (int x = tid; x < n; x += kIdxThreads)
+        block_counts[(int64_t)blockIdx.x * n + x] = __popcll(words[x]);
+}
+
+// T <= 64: one token per wave, kIdxSmallWaves waves per workgroup. Each workgroup, after its
+// tokens' outputs, takes a ticket from *ticket (agent-scope acquire-release, so the last
+// workgroup sees every other workgroup's top-k ids); the last one builds the layout from
+// those ids and sets *ticket back to 0 for the next call.
+template <int EPL>
+__global__ __launch_bounds__(64 * kIdxSmallWaves) void route_paths_small_kernel(
+    const float* __restrict__ logits, const uint64_t* __restrict__ packed, int64_t T, int n, int k,
+    int beta_mode, int32_t* __restrict__ ids, float* __restrict__ w, uint64_t* __restrict__ bits_out,
+    float* __restrict__ beta_out, int32_t* __restrict__ offsets, int32_t* __restrict__ row_token,
+    int32_t* __restrict__ row_slot, int32_t* __restrict__ row_of, uint32_t* __restrict__ ticket) {
+    constexpr int NT = 64 * kIdxSmallWaves;
+    constexpr int RPT = kIdxSmall * kMaxK / NT;  // rows per thread of the layout
+    __shared__ unsigned long long words[kMaxN];
+    __shared__ uint64_t mask_s[kMaxN * (kMaxN / 64)];
+    __shared__ int scan[kMaxN];
+    __shared__ int wave_tot[kMaxN / 64];
+    __shared__ int last;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int W = (n + 63) / 64;
+    const int64_t t = (int64_t)blockIdx.x * kIdxSmallWaves + wave;
+    float lv[EPL];
+    load_logits<EPL>(logits, t, T, n, lane, lv);
+    for (int x = tid; x < n * W; x += NT) mask_s[x] = packed[x];
+    for (int x = tid; x < kMaxN; x += NT) words[x] = 0ull;
+    __syncthreads();
+    if (t < T)  // wave-uniform
+        index_token<EPL>(lv, mask_s, W, n, k, beta_mode, t, lane, lane / k, lane - (lane / k) * k,
+                         ids, w, bits_out, beta_out);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this wave's outputs, device-wide
+    __syncthreads();
+    if (tid == 0)
+        last = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
+               gridDim.x - 1;
+    __syncthreads();
+    if (!last) return;  // workgroup-uniform
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    // every token's experts, ORed into the per-expert bitsets
+    int e[RPT];
 #pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-            const int x = lane + 64 * q;
-            key[q] = x < n ? ((uint64_t)orderable(lv[0][q]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)x)
-                           : 0ull;  // every real key is > 0
-        }
-#pragma unroll
-        for (int jj = 0; jj + 1 < PER; ++jj)  // the next token's logits move up
-#pragma unroll
-            for (int q = 0; q < EPL; ++q) lv[jj][q] = lv[jj + 1][q];
-        uint64_t mine = 0ull, first = 0ull;  // slot `lane`'s key (lanes < k), slot 0's key
-        for (int a = 0; a < k; ++a) {
-            uint64_t best = key[0];
-#pragma unroll
-            for (int q = 1; q < EPL; ++q) best = key[q] > best ? key[q] : best;
-            best = wave_max_u64(best);
-            if (a == 0) first = best;
-            if (lane == a) mine = best;
-#pragma unroll
-            for (int q = 0; q < EPL; ++q)
-                if (key[q] == best) key[q] = 0ull;
-        }
-        // softmax over the selected logits, shifted by the largest, summed in slot order
-        const float top = from_orderable((uint32_t)(first >> 32));
-        const float ex = lane < k ? expf(from_orderable((uint32_t)(mine >> 32)) - top) : 0.0f;
-        float s = 0.0f;
-        for (int a = 0; a < k; ++a) s += readlane_f32(ex, a);
-        const int e = lane < k ? (int)(0xFFFFFFFFu - (uint32_t)mine) : 0;
-        const float p = lane < k ? ex / s : 0.0f;
-        if (lane < k) {
-            ids[t * k + lane] = e;
-            w[t * k + lane] = p;
-        }
-        // path (a, b) of this lane: the slots' experts and weights by cross-lane reads
-        const int ea = __shfl(e, pa_), eb = __shfl(e, pb_);
-        const float pa = __shfl(p, pa_), pb = __shfl(p, pb_);
-        const bool on = in && (pa_ == pb_ || ((mask_s[ea * W + (eb >> 6)] >> (eb & 63)) & 1ull));
-        const uint64_t bits = __ballot(on);
-        if (lane == 0) bits_out[t] = bits;
-        float den = 1.0f;
-        if (beta_mode == 0) {
-            den = 0.0f;  // sum of p over the targets of this lane's source a, b ascending
-            const int row = in ? pa_ * k : 0;
-            for (int bb = 0; bb < k; ++bb) {
-                const float pbb = readlane_f32(p, bb);
-                if ((bits >> (row + bb)) & 1) den += pbb;
-            }
-        } else if (beta_mode == 2) {
-            den = 0.0f;  // sum of p_a' p_b' over the token's paths, (a', b') ascending
-            for (int aa = 0; aa < k; ++aa) {
-                const float paa = readlane_f32(p, aa);
-                for (int bb = 0; bb < k; ++bb) {
-                    const float pbb = readlane_f32(p, bb);
-                    if ((bits >> (aa * k + bb)) & 1) den = fmaf(paa, pbb, den);
-                }
-            }
-        }
-        if (in) {
-            float v = 0.0f;
-            if (on) v = beta_mode == 0 ? pa * (pb / den) : (beta_mode == 1 ? pa * pb : pa * pb / den);
-            beta_out[t * k * k + lane] = v;
-        }
-        if (lane < k) {
-            atomicOr(&words[e], 1ull << tib);
-            if constexpr (FUSED) tok_e[tib][lane] = e;
+    for (int r = 0; r < RPT; ++r) {
+        const int i = tid + r * NT;
+        e[r] = 0;
+        if (i < T * k) {
+            const int v = __hip_atomic_load(ids + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            e[r] = v < 0 ? 0 : (v >= n ? n - 1 : v);
+            atomicOr(&words[e[r]], 1ull << (i / k));
         }
     }
     __syncthreads();
-    if constexpr (!FUSED) {
-        for (int x = tid; x < n; x += kIdxThreads)
-            block_counts[(int64_t)blockIdx.x * n + x] = __popcll(words[x]);
-    } else {
-        // the one block holds every token: exclusive scan of its counts, then every row
-        const int own = tid < n ? __popcll(words[tid]) : 0;
-        int total;
-        const int excl = scan_columns(own, wave_tot, &total);
-        if (tid < kMaxN) scan[tid] = excl;
-        if (tid < n) offsets[tid] = excl;
-        if (tid == 0) offsets[n] = total;
-        __syncthreads();
-        const int ntok = (int)T;
-        for (int i = tid; i < ntok * k; i += kIdxThreads) {
-            const int tib = i / k, a = i - (i / k) * k;
-            const int x = tok_e[tib][a];
+    const int own = tid < n ? __popcll(words[tid]) : 0;
+    int total;
+    const int excl = scan_columns(own, wave_tot, &total);
+    if (tid < kMaxN) scan[tid] = excl;
+    if (tid < n) offsets[tid] = excl;
+    if (tid == 0) {
+        offsets[n] = total;
+        __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int i = tid + r * NT;
+        if (i < T * k) {
+            const int tib = i / k, a = i - (i / k) * k, x = e[r];
             const int pos = scan[x] + __popcll(words[x] & ((1ull << tib) - 1ull));
-            row_token[pos] = (int32_t)tib;
+            row_token[pos] = tib;
             row_slot[pos] = a;
-            row_of[(int64_t)tib * k + a] = pos;
+            row_of[i] = pos;
         }
     }
 }
@@ -474,8 +547,8 @@ hipError_t launch_route(const float* logits, int64_t T, int n, int k, int32_t* i
 }
 
 size_t route_paths_ws_bytes(int64_t T, int n) {
-    if (T <= kIdxFused) return 0;
-    return align_up((size_t)ceil_div(T, kIdxCount) * n * sizeof(int32_t), 256);
+    // the single-launch ticket, then (T > 64) the counts [ceil(T / kIdxCount)][n]
+    return 256 + (T <= kIdxSmall ? 0 : align_up((size_t)ceil_div(T, kIdxCount) * n * sizeof(int32_t), 256));
 }
 
 hipError_t launch_mask_pack(const uint8_t* mask, int n, uint64_t* packed, hipStream_t s) {
@@ -486,28 +559,35 @@ hipError_t launch_mask_pack(const uint8_t* mask, int n, uint64_t* packed, hipStr
 hipError_t launch_route_paths(const float* logits, const uint64_t* packed, int64_t T, int n, int k,
                               int beta_mode, int32_t* ids, float* w, uint64_t* bits, float* beta,
                               int32_t* offsets, int32_t* row_token, int32_t* row_slot,
-                              int32_t* row_of, int32_t* block_counts, hipStream_t s) {
+                              int32_t* row_of, void* ws, hipStream_t s) {
     const int epl = (int)ceil_div(n, 64);
-    auto go = [&](auto kern, int64_t blocks) {
-        kern<<<(unsigned)blocks, kIdxThreads, 0, s>>>(logits, packed, T, n, k, beta_mode, ids, w,
-                                                      bits, beta, offsets, row_token, row_slot,
-                                                      row_of, block_counts);
-    };
-    if (T <= kIdxFused) {
+    uint32_t* ticket = (uint32_t*)ws;
+    if (T <= kIdxSmall) {
+        const unsigned blocks = (unsigned)ceil_div(T, kIdxSmallWaves);
+        auto go = [&](auto kern) {
+            kern<<<blocks, 64 * kIdxSmallWaves, 0, s>>>(logits, packed, T, n, k, beta_mode, ids, w,
+                                                        bits, beta, offsets, row_token, row_slot,
+                                                        row_of, ticket);
+        };
         switch (epl) {
-            case 1: go(route_paths_kernel<1, true>, 1); break;
-            case 2: go(route_paths_kernel<2, true>, 1); break;
-            case 3: go(route_paths_kernel<3, true>, 1); break;
-            default: go(route_paths_kernel<4, true>, 1); break;
+            case 1: go(route_paths_small_kernel<1>); break;
+            case 2: go(route_paths_small_kernel<2>); break;
+            case 3: go(route_paths_small_kernel<3>); break;
+            default: go(route_paths_small_kernel<4>); break;
         }
         return hipGetLastError();
     }
+    int32_t* block_counts = (int32_t*)((char*)ws + 256);
     const int64_t NB = ceil_div(T, kIdxCount);
+    auto go = [&](auto kern) {
+        kern<<<(unsigned)NB, kIdxThreads, 0, s>>>(logits, packed, T, n, k, beta_mode, ids, w, bits,
+                                                  beta, block_counts);
+    };
     switch (epl) {
-        case 1: go(route_paths_kernel<1, false>, NB); break;
-        case 2: go(route_paths_kernel<2, false>, NB); break;
-        case 3: go(route_paths_kernel<3, false>, NB); break;
-        default: go(route_paths_kernel<4, false>, NB); break;
+        case 1: go(route_paths_kernel<1>); break;
+        case 2: go(route_paths_kernel<2>); break;
+        case 3: go(route_paths_kernel<3>); break;
+        default: go(route_paths_kernel<4>); break;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

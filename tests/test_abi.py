@@ -129,11 +129,11 @@ def test_mask_pack_and_route_paths_validation(L):
     assert L.pcm_mask_pack(FAKE, 8, mis, None) == ARG                  # misaligned packed
     p = _paths()
     bp = ctypes.byref(p)
-    # up to 64 tokens need no workspace; more hold the counts [ceil(T / 32)][n] i32
-    assert L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 64, 0, 0, 256, 8, 0) == 0
-    assert L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 65, 0, 0, 60, 4, 0) == 768
+    # 256 bytes of completion counter, then (T > 64) the counts [ceil(T / 32)][n] i32
+    assert L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 64, 0, 0, 256, 8, 0) == 256
+    assert L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 65, 0, 0, 60, 4, 0) == 256 + 768
     need = L.pcm_workspace_bytes(binding.OP_ROUTE_PATHS, 8192, 0, 0, 64, 8, 0)
-    assert need == 256 * 64 * 4
+    assert need == 256 + 256 * 64 * 4
     args = lambda T=8192, n=64, k=8, beta=0, q=bp, ws=FAKE, wsb=need: (
         FAKE, FAKE, T, n, k, beta, FAKE, FAKE, q, ws, wsb, None)
     assert L.pcm_route_paths(*args(k=9)) == UNSUP                      # k > 8
@@ -142,6 +142,7 @@ def test_mask_pack_and_route_paths_validation(L):
     assert L.pcm_route_paths(*args(beta=3)) == ARG
     assert L.pcm_route_paths(*args(wsb=need - 1)) == WS
     assert L.pcm_route_paths(*args(ws=None)) == WS
+    assert L.pcm_route_paths(*args(T=64, ws=None, wsb=0)) == WS      # the counter is needed
     assert L.pcm_route_paths(*args(ws=mis)) == ARG
     assert L.pcm_route_paths(*args(T=0, q=None, ws=None, wsb=0)) == OK  # T = 0 no-op
     for f, _ in binding.PcmPaths._fields_:

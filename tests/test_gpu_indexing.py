@@ -50,8 +50,12 @@ def fused(logits, packed, k, beta_mode=0):
     for f in FIELDS:
         getattr(out, f).view(torch.uint8).fill_(0xFF)
     ws_bytes = pcm.workspace_bytes(pcm.binding.OP_ROUTE_PATHS, T, 0, 0, n, k, 0)
-    ws = torch.full((max(ws_bytes, 1),), 0xFF, dtype=torch.uint8, device=DEV) if ws_bytes else None
-    return pcm.pcm_route_paths(logits, packed, k, beta_mode, ids, w, out=out, ws=ws)
+    ws = torch.full((ws_bytes,), 0xFF, dtype=torch.uint8, device=DEV)
+    ws[:256].zero_()   # the completion counter starts at zero; the rest is scratch
+    r = pcm.pcm_route_paths(logits, packed, k, beta_mode, ids, w, out=out, ws=ws)
+    torch.cuda.synchronize()
+    assert not ws[:256].any(), "the call left its completion counter nonzero"
+    return r
 
 
 def check_fused(logits_np, mask_np, k, beta_mode=0, what=""):
@@ -142,6 +146,31 @@ def test_route_paths_heavy_ties_and_signed_zeros():
         l[1::7] = 0.0
         mask = (rng.random((n, n)) < 0.5).astype(np.uint8)
         check_fused(l, mask, min(n, 8), what=f"ties n={n}")
+
+
+@pytest.mark.parametrize("T,n,k", [(1, 8, 2), (3, 256, 8), (32, 256, 8), (61, 64, 8), (64, 60, 4),
+                                   (65, 64, 8)])
+def test_route_paths_reused_workspace(T, n, k):
+    """Back-to-back calls on one workspace (the single-launch case's completion counter must
+    come back to zero after each), alternating two inputs, each checked against the oracle."""
+    rng = np.random.default_rng(T + 31 * n)
+    ls = [rng.standard_normal((T, n)).astype(np.float32) for _ in range(2)]
+    mask = (rng.random((n, n)) < 0.3).astype(np.uint8)
+    packed = pcm.pcm_mask_pack(torch.from_numpy(mask).to(DEV))
+    ws = pcm.binding.route_paths_workspace(T, n, k, DEV)
+    outs = []
+    for r in range(6):
+        lg = torch.from_numpy(ls[r % 2]).to(DEV)
+        ids, w, p = pcm.pcm_route_paths(lg, packed, k, ws=ws)
+        outs.append((ids.clone(), p.row_token.clone(), p.row_of.clone(), p.expert_offsets.clone()))
+    torch.cuda.synchronize()
+    assert not ws[:256].any()
+    for r in range(6):
+        ids_ref, _ = oracle.route(ls[r % 2], k)
+        off_ref, rt_ref, _, ro_ref = oracle.permute(ids_ref, n)
+        ids, rt, ro, off = (t.cpu().numpy() for t in outs[r])
+        assert np.array_equal(ids, ids_ref) and np.array_equal(off, off_ref), r
+        assert np.array_equal(rt, rt_ref) and np.array_equal(ro, ro_ref), r
 
 
 def test_layer_plan_with_packed_mask_is_bit_identical():
