@@ -133,10 +133,12 @@ def trace_summary(path: str):
                 ns = np.mean([v["ns"] for v in vs])
                 cells = [f"{m[c]:.6g}" for c in names]
                 if extra:
-                    # 8 XCDs count GRBM_GUI_ACTIVE each; 1024 SIMDs count MFMA-busy cycles
+                    # 8 XCDs count GRBM_GUI_ACTIVE each; 1024 SIMDs count MFMA-busy cycles. The
+                    # busy window of a dispatch includes a fixed start-up of a few microseconds,
+                    # so the clock is shown for dispatches of 50 us or more only
                     gui = m["GRBM_GUI_ACTIVE"] / 8
                     cells += [f"{m['SQ_VALU_MFMA_BUSY_CYCLES'] / 1024 / max(gui, 1):.1%}",
-                              f"{gui / max(ns, 1):.2f}"]
+                              f"{gui / max(ns, 1):.2f}" if ns >= 50e3 else "—"]
                 print(f"| `{_short(name)}` | {len(vs)} | {ns / 1e3:.1f} | " + " | ".join(cells) + " |")
             print()
 
