@@ -181,12 +181,20 @@ __device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s
     if (lane == 0) bits_out[t] = bits;
     float den = 1.0f;
     if (beta_mode == 0) {
-        den = 0.0f;  // sum of p over the targets of this lane's source a, b ascending
-        const int row = in ? pa_ * k : 0;
-        for (int bb = 0; bb < k; ++bb) {
-            const float pbb = readlane_f32(p, bb);
-            if ((bits >> (row + bb)) & 1) den += pbb;
+        // the sum of p over the targets of this lane's source a, b ascending (the path build's
+        // order of additions): a running sum along lanes a*k .. a*k+k-1, lane a*k+b holding
+        // p_b where (a, b) is a path and 0 elsewhere (adding +0 to a sum of non-negative terms
+        // leaves it unchanged). At step j the lanes with b >= j add their term to the value of
+        // the lane before them (a DPP shift by one lane across the wave), so the lane with
+        // b = j ends with ((p_0 + p_1) + ...) + p_j; the row's last lane holds the sum.
+        const float v = on ? pb : 0.0f;
+        float run = v;
+        for (int j = 1; j < k; ++j) {
+            const float prev =
+                __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(run), 0x138, 0xF, 0xF, true));
+            run = pb_ >= j ? prev + v : run;
         }
+        den = __shfl(run, pa_ * k + k - 1);
     } else if (beta_mode == 2) {
         den = 0.0f;  // sum of p_a' p_b' over the token's paths, (a', b') ascending
         for (int aa = 0; aa < k; ++aa) {
@@ -344,22 +352,32 @@ __global__ __launch_bounds__(kIdxThreads) void route_scatter_kernel(
     while (np < n) np <<= 1;
     const int G = kIdxThreads / np;  // groups of counting blocks per column, >= 4
     const int x = tid % np, g = tid / np;
+    // the first UN of this thread's count-table entries are loaded with the row's id, before
+    // the barrier (the rest, for tables of more than UN * G blocks, after it)
+    int c[UN];
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+        const int64_t b = g + (int64_t)u * G;
+        c[u] = (x < n && b < NB) ? block_counts[b * n + x] : 0;
+    }
     for (int i = tid; i < NW * kMaxN; i += kIdxThreads) (&words[0][0])[i] = 0ull;
     for (int i = tid; i < kMaxN; i += kIdxThreads) tot[i] = before[i] = 0;
     __syncthreads();
+    if (valid) atomicOr(&words[tib >> 6][e], 1ull << (tib & 63));
     int st = 0, sb = 0;
     if (x < n) {
-        for (int64_t b0 = g; b0 < NB; b0 += (int64_t)UN * G) {
-            int c[UN];
-#pragma unroll
-            for (int u = 0; u < UN; ++u) {
-                const int64_t b = b0 + (int64_t)u * G;
-                c[u] = b < NB ? block_counts[b * n + x] : 0;
-            }
+        for (int64_t b0 = g;; ) {
 #pragma unroll
             for (int u = 0; u < UN; ++u) {
                 st += c[u];
                 sb += b0 + (int64_t)u * G < b_me ? c[u] : 0;
+            }
+            b0 += (int64_t)UN * G;
+            if (b0 >= NB) break;
+#pragma unroll
+            for (int u = 0; u < UN; ++u) {
+                const int64_t b = b0 + (int64_t)u * G;
+                c[u] = b < NB ? block_counts[b * n + x] : 0;
             }
         }
         if (st) atomicAdd(&tot[x], st);
@@ -374,7 +392,6 @@ __global__ __launch_bounds__(kIdxThreads) void route_scatter_kernel(
         if (tid == 0) offsets[n] = total;
     }
     if (tid < n) first[tid] = excl + before[tid];
-    if (valid) atomicOr(&words[tib >> 6][e], 1ull << (tib & 63));
     __syncthreads();
     if (valid) {
         const int wd = tib >> 6;
