@@ -1,12 +1,14 @@
 """Benchmark of the path-compositional MoE layer on one MI355X.
 
-A step is one forward pass of the whole layer (route, build paths, expand, project
-and combine, plus the shared expert when the workload has one) over one batch of
-synthetic, seeded inputs already resident in HBM. Prints ONE JSON line: the headline
-workload (Mixtral-shaped) at the top level, and every workload under "workloads".
+A step is one forward pass of the whole layer (the fused indexing operation over the
+layer's packed mask, expand, project and combine, plus the shared expert when the workload
+has one) over one batch of synthetic, seeded inputs already resident in HBM. Prints ONE JSON
+line: the headline workload (Mixtral-shaped) at the top level with its ablation (the same
+layer per path, with and without source reuse, and the vanilla top-k layer), and every
+workload under "workloads".
 
   python bench.py [--steps K] [--warmup W] [--config NAME] [--only] [--router topk|scored]
-                  [--no-cpu-baseline]
+                  [--indexing fused|separate] [--no-cpu-baseline] [--no-ablation]
   python bench.py --trace-summary DIR     per-kernel durations (kernel traces) or counter
                                           means (--pmc runs) of the timed launches in the
                                           rocprofv3 output written under DIR
@@ -14,8 +16,8 @@ workload (Mixtral-shaped) at the top level, and every workload under "workloads"
 Per-kernel times come from HIP events recorded on the stream the kernels run on: around
 each call, and inside pcm_project_combine between the mix, the projection GEMM and the
 combine (pcm_tuning's stage events). A second pass over the same steps writes a 512 MB
-buffer before each step, so that the memory-bound stages (route, path build, mix,
-combine) read from HBM rather than from the 256 MB MALL; their GB/s come from that pass.
+buffer before each step, so that the memory-bound stages (indexing, mix, combine)
+read from HBM rather than from the 256 MB MALL; their GB/s come from that pass.
 The timed region is fenced by two short spin kernels, which --trace-summary uses to keep
 only the timed launches of a rocprofv3 trace. The CPU baseline times the float64 oracle on
 a bounded sample of the headline workload's tokens.
@@ -60,9 +62,9 @@ def parse():
                     help="time a decode step through L layers of the workload's shape (router GEMM, "
                          "paths, experts, residual; the first two layers diagonal-only); "
                          "reported as a separate JSON line")
-    ap.add_argument("--ablation", action="store_true",
-                    help="also time the same layer executed per path (with and without source "
-                         "reuse) and the vanilla top-k layer (diagonal-only mask)")
+    ap.add_argument("--no-ablation", action="store_true",
+                    help="skip the headline workload's ablation (the same layer executed per path, "
+                         "with and without source reuse, and the vanilla top-k layer)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -352,6 +354,12 @@ def workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored):
         off = plan.paths.expert_offsets.cpu().numpy()
         touched = touched_src = touched_tgt = int(np.count_nonzero(np.diff(off)))
         R = R_tgt = R_bound = cfg.R
+    if scored:
+        per_expert = np.diff(src_off)
+        n_paths = int(R_bound)
+    else:
+        per_expert = np.diff(off)
+        n_paths = int(np.unpackbits(plan.paths.path_bits.cpu().numpy().view(np.uint8)).sum())
     f = acc.gemm_flops(R, cfg.H, cfg.F, cfg.T, cfg.shared_F, R_tgt)
     peak = acc.BF16_PEAK_TFLOPS if bf16 else acc.FP32_PEAK_TFLOPS
     gemm_ms = st["expand"] + st["project_combine"] + st.get("shared", 0.0)
@@ -368,6 +376,8 @@ def workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored):
         hbm["build_paths"] = acc.paths_bytes(cfg.T, cfg.n, K) / (fl["build_paths"] * 1e-3) / 1e9
     rec = {"ms": round(ms, 4), "tokens_per_s": round(cfg.T / (ms * 1e-3), 1),
            "rows": R, "touched_experts": touched,
+           "rows_per_expert_min": int(per_expert.min()), "rows_per_expert_max": int(per_expert.max()),
+           "paths": n_paths,
            "gemm_tflops": round(f["total"] / (gemm_ms * 1e-3) / 1e12, 1),
            "gemm_frac_peak": round(f["total"] / (gemm_ms * 1e-3) / 1e12 / peak, 4),
            "stages_ms": {k: round(v, 4) for k, v in st.items()},
@@ -490,17 +500,18 @@ def ablation(pcm, plan, cfg, d, args):
                      device=x.device)
     y = torch.empty_like(plan.y)
 
+    packed = pcm.pcm_mask_pack(mask)   # every variant indexes through the fused operation
+
     def per_path(reuse):
         def fn():
             if shared:
                 pcm.pcm_dense_swiglu(x, *shared, y=y, accumulate=False, ws=plan.ws_shared)
-            pcm.pcm_route(logits, cfg.k, plan.ids, plan.w)
-            pcm.pcm_build_paths(plan.ids, plan.w, mask, 0, out=plan.paths, ws=plan.ws_paths)
+            plan.index(logits, packed)
             pcm.pcm_layer_per_path(x, wg, wu, wd, plan.paths, reuse=reuse, y=y,
                                    accumulate=bool(shared), ws=ws)
         return fn
 
-    eye = torch.eye(cfg.n, dtype=torch.uint8, device=x.device)
+    eye = pcm.pcm_mask_pack(torch.eye(cfg.n, dtype=torch.uint8, device=x.device))
 
     def mixed(m):
         def fn():
@@ -508,7 +519,7 @@ def ablation(pcm, plan, cfg, d, args):
         return fn
 
     out = {"paths": n_paths, "expansion_rows_reused": cfg.R,
-           "ms_target_mix": round(timed(mixed(mask)), 4),
+           "ms_target_mix": round(timed(mixed(packed)), 4),
            "ms_per_path_reuse": round(timed(per_path(True)), 4),
            "ms_per_path_no_reuse": round(timed(per_path(False)), 4),
            "ms_vanilla_topk": round(timed(mixed(eye)), 4)}
@@ -585,7 +596,7 @@ def main():
                 "stages_ms": rec["stages_ms"], "hbm_GBps": rec["hbm_GBps"], "roofline": roof,
             }
             line["router_gemm"] = router_gemm(pcm, cfg, d["x"], args)
-            if args.ablation and not scored:
+            if not args.no_ablation and not scored:
                 line["ablation"] = ablation(pcm, plan, cfg, d, args)
             if not args.no_cpu_baseline:
                 print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
