@@ -26,8 +26,10 @@ __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b 
 
 // Largest 32-bit value across the wavefront, the same on every lane (all 64 lanes active):
 // DPP moves that pair lane i with i^1, i^2, its mirror in 8 and its mirror in 16 leave each
-// row of 16 lanes with its maximum (each move folds into the max instruction), then the
-// four row maxima are read into scalar registers and compared there.
+// row of 16 lanes with its maximum (each move folds into the max instruction); two row
+// broadcasts then fold row 0 into row 1 and row 2 into row 3 (lane 15 of a row to the next
+// row), and rows 0-1 into rows 2-3 (lane 31 to both), so lane 63 holds the wave's maximum,
+// which one read into a scalar register hands to every lane.
 template <int CTRL>
 __device__ inline uint32_t dpp_u32(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
@@ -37,11 +39,17 @@ __device__ inline uint32_t wave_max_u32(uint32_t v) {
     v = max(v, dpp_u32<0x4E>(v));   // quad_perm [2,3,0,1]: lane ^ 2
     v = max(v, dpp_u32<0x141>(v));  // row_half_mirror: the other quad of 8
     v = max(v, dpp_u32<0x140>(v));  // row_mirror: the other half of 16
-    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
-    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
-    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
-    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
-    return max(max(r0, r1), max(r2, r3));
+    // The row broadcasts write only the rows their row mask names, the other rows keep v, which
+    // the compiler's DPP intrinsics would express as a copy, a move and a max; as one
+    // instruction each (the two wait states a DPP read of a VALU result needs come first).
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_max_u32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_u32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+        "s_nop 1"
+        : "+v"(v));
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 // Largest 64-bit value across the wavefront: the largest high word, then, when more than
 // one lane holds it, the largest low word among those lanes.

@@ -60,9 +60,10 @@ __device__ inline void route_token(const float* l, int n, int k, int lane, int32
 // Section 4.3's single indexing operation over the layer's packed mask: route, path filter,
 // path weights and the dispatch layout. Per token, one wavefront, in compact per-lane state
 // (runtime loops over the k slots keep the code small), index_token:
-//   - top-k: k rounds of a wave maximum over 64-bit keys as in route_token; lane a keeps
-//     slot a's key, then lanes a < k take their exponentials and the softmax denominator
-//     is summed in slot order, as route_token sums it;
+//   - top-k: k rounds of a wave maximum over 64-bit keys as in route_token (with one logit
+//     per lane, over the 32-bit logit keys, the lowest lane holding the maximum winning);
+//     lane a keeps slot a's key, then lanes a < k take their exponentials and the softmax
+//     denominator is summed in slot order, as route_token sums it;
 //   - paths: lane a*k + b < k^2 tests (a, b) against the mask (diagonal set); one ballot
 //     gives the token's bits; the same lane forms beta_ab in the path build's order of
 //     operations (slot weights broadcast by readlane), so both give the same bits.
@@ -126,13 +127,37 @@ __device__ inline void load_logits(const float* logits, int64_t t, int64_t T, in
     }
 }
 
+// Per-lane constants of index_token, formed once per wave: the lane's path (a, b) =
+// (lane / k, lane % k) and the byte addresses (for ds_bpermute) of the lanes it reads: slot a,
+// slot b, and the last lane of path row a, which ends that row's running sum. Lanes at or past
+// k * k read in-range lanes whose values they do not use.
+struct PathLane {
+    int pa, pb, at_a, at_b, at_row_end;
+};
+__device__ inline PathLane path_lane(int lane, int k) {
+    PathLane q;
+    q.pa = lane / k;
+    q.pb = lane - q.pa * k;
+    q.at_a = (q.pa & 63) << 2;
+    q.at_b = q.pb << 2;
+    q.at_row_end = ((q.pa * k + k - 1) & 63) << 2;
+    // kept in registers: otherwise the compiler recomputes the division for every token
+    asm volatile("" : "+v"(q.pa), "+v"(q.pb), "+v"(q.at_a), "+v"(q.at_b), "+v"(q.at_row_end));
+    return q;
+}
+__device__ inline int bperm_i32(int at, int v) { return __builtin_amdgcn_ds_bpermute(at, v); }
+__device__ inline float bperm_f32(int at, float v) {
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(at, __float_as_int(v)));
+}
+
 // One token by one wavefront (all 64 lanes active): writes its top-k ids and weights, path
 // bits and beta; returns its slot expert to lanes < k (0 elsewhere). mask_s: the packed mask
-// in LDS, W words per row. pa_ = lane / k, pb_ = lane % k.
+// in LDS, ceil(n / 64) = EPL words per row; pl from path_lane(lane, k).
 template <int EPL>
-__device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s, int W, int n,
-                                  int k, int beta_mode, int64_t t, int lane, int pa_, int pb_,
+__device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s, int n,
+                                  int k, int beta_mode, int64_t t, int lane, const PathLane& pl,
                                   int32_t* ids, float* w, uint64_t* bits_out, float* beta_out) {
+    const int pa_ = pl.pa, pb_ = pl.pb;
     uint64_t key[EPL];
 #pragma unroll
     for (int q = 0; q < EPL; ++q) {
@@ -140,25 +165,55 @@ __device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s
         key[q] = x < n ? ((uint64_t)orderable(lv[q]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)x)
                        : 0ull;  // every real key is > 0
     }
-    // the lane's keys in descending order, so that each round looks at key[0] only and the
-    // lane holding the round's maximum pops it
-    auto order = [&](int i, int j) {
-        const uint64_t hi = key[i] > key[j] ? key[i] : key[j], lo = key[i] > key[j] ? key[j] : key[i];
-        key[i] = hi;
-        key[j] = lo;
-    };
-    if constexpr (EPL == 2) order(0, 1);
-    if constexpr (EPL == 3) { order(0, 1); order(1, 2); order(0, 1); }
-    if constexpr (EPL == 4) { order(0, 1); order(2, 3); order(0, 2); order(1, 3); order(1, 2); }
     uint64_t mine = 0ull, first = 0ull;  // slot `lane`'s key (lanes < k), slot 0's key
-    for (int a = 0; a < k; ++a) {
-        const uint64_t best = wave_max_u64(key[0]);
-        if (a == 0) first = best;
-        if (lane == a) mine = best;
-        if (key[0] == best) {
+    if constexpr (EPL == 1) {
+        // one logit per lane and lane = expert id: the largest high word (the orderable logit),
+        // and the lowest lane holding it (the first bit of a ballot) is the lower id, which is
+        // the order of the 64-bit keys. The round's winner, slot a's key and its removal are
+        // single-lane writes from scalar registers.
+        uint32_t kv = (uint32_t)(key[0] >> 32), mhi = 0u, mlo = 0u, fhi = 0u;
+        for (int a = 0; a < k; ++a) {
+            const uint32_t m = wave_max_u32(kv);
+            const int sl = __builtin_amdgcn_readfirstlane(
+                __ffsll((unsigned long long)__ballot(kv == m)) - 1);
+            if (a == 0) fhi = m;
+            const uint32_t id_key = 0xFFFFFFFFu - (uint32_t)sl;
+            // (the lane select goes through m0: a scalar value and a scalar lane select in two
+            // other registers would exceed the instruction's one constant-bus read; two wait
+            // states after the last write, since the next round's first DPP reads kv)
+            asm volatile(
+                "s_mov_b32 m0, %3\n\t"
+                "v_writelane_b32 %0, 0, m0\n\t"
+                "s_mov_b32 m0, %5\n\t"
+                "v_writelane_b32 %1, %4, m0\n\t"
+                "v_writelane_b32 %2, %6, m0\n\t"
+                "s_nop 1"
+                : "+v"(kv), "+v"(mhi), "+v"(mlo)
+                : "s"(sl), "s"(m), "s"(a), "s"(id_key)
+                : "m0");
+        }
+        mine = ((uint64_t)mhi << 32) | mlo;
+        first = (uint64_t)fhi << 32;
+    } else {
+        // the lane's keys in descending order, so that each round looks at key[0] only and the
+        // lane holding the round's maximum pops it
+        auto order = [&](int i, int j) {
+            const uint64_t hi = key[i] > key[j] ? key[i] : key[j], lo = key[i] > key[j] ? key[j] : key[i];
+            key[i] = hi;
+            key[j] = lo;
+        };
+        if constexpr (EPL == 2) order(0, 1);
+        if constexpr (EPL == 3) { order(0, 1); order(1, 2); order(0, 1); }
+        if constexpr (EPL == 4) { order(0, 1); order(2, 3); order(0, 2); order(1, 3); order(1, 2); }
+        for (int a = 0; a < k; ++a) {
+            const uint64_t best = wave_max_u64(key[0]);
+            if (a == 0) first = best;
+            if (lane == a) mine = best;
+            if (key[0] == best) {
 #pragma unroll
-            for (int q = 0; q + 1 < EPL; ++q) key[q] = key[q + 1];
-            key[EPL - 1] = 0ull;
+                for (int q = 0; q + 1 < EPL; ++q) key[q] = key[q + 1];
+                key[EPL - 1] = 0ull;
+            }
         }
     }
     // softmax over the selected logits, shifted by the largest, summed in slot order
@@ -169,14 +224,16 @@ __device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s
     const int e = lane < k ? (int)(0xFFFFFFFFu - (uint32_t)mine) : 0;
     const float p = lane < k ? ex / s : 0.0f;
     if (lane < k) {
-        ids[t * k + lane] = e;
-        w[t * k + lane] = p;
+        int32_t* const ids_t = ids + t * k;  // scalar base, lane offset
+        float* const w_t = w + t * k;
+        ids_t[lane] = e;
+        w_t[lane] = p;
     }
     // path (a, b) of this lane: the slots' experts and weights by cross-lane reads
     const bool in = lane < k * k;
-    const int ea = __shfl(e, pa_), eb = __shfl(e, pb_);
-    const float pa = __shfl(p, pa_), pb = __shfl(p, pb_);
-    const bool on = in && (pa_ == pb_ || ((mask_s[ea * W + (eb >> 6)] >> (eb & 63)) & 1ull));
+    const int ea = bperm_i32(pl.at_a, e), eb = bperm_i32(pl.at_b, e);
+    const float pa = bperm_f32(pl.at_a, p), pb = bperm_f32(pl.at_b, p);
+    const bool on = in && (pa_ == pb_ || ((mask_s[ea * EPL + (eb >> 6)] >> (eb & 63)) & 1ull));
     const uint64_t bits = __ballot(on);
     if (lane == 0) bits_out[t] = bits;
     float den = 1.0f;
@@ -194,7 +251,7 @@ __device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s
                 __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(run), 0x138, 0xF, 0xF, true));
             run = pb_ >= j ? prev + v : run;
         }
-        den = __shfl(run, pa_ * k + k - 1);
+        den = bperm_f32(pl.at_row_end, run);
     } else if (beta_mode == 2) {
         den = 0.0f;  // sum of p_a' p_b' over the token's paths, (a', b') ascending
         for (int aa = 0; aa < k; ++aa) {
@@ -208,7 +265,8 @@ __device__ inline int index_token(const float (&lv)[EPL], const uint64_t* mask_s
     if (in) {
         float v = 0.0f;
         if (on) v = beta_mode == 0 ? pa * (pb / den) : (beta_mode == 1 ? pa * pb : pa * pb / den);
-        beta_out[t * k * k + lane] = v;
+        float* const beta_t = beta_out + t * k * k;
+        beta_t[lane] = v;
     }
     return e;
 }
@@ -223,7 +281,8 @@ __global__ __launch_bounds__(kIdxThreads) void route_paths_kernel(
     constexpr int PER = kIdxCount / kIdxWaves;  // tokens per wave, one after another
     __shared__ unsigned long long words[kMaxN];
     __shared__ uint64_t mask_s[kMaxN * (kMaxN / 64)];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the wave index in a scalar register, so that token indices and store addresses are too
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     for (int x = tid; x < kMaxN; x += kIdxThreads) words[x] = 0ull;
     const int W = (n + 63) / 64;  // packed words per mask row
     const int64_t t0 = (int64_t)blockIdx.x * kIdxCount;
@@ -232,13 +291,13 @@ __global__ __launch_bounds__(kIdxThreads) void route_paths_kernel(
     for (int j = 0; j < PER; ++j) load_logits<EPL>(logits, t0 + j * kIdxWaves + wave, T, n, lane, lv[j]);
     for (int x = tid; x < n * W; x += kIdxThreads) mask_s[x] = packed[x];
     __syncthreads();  // words cleared, mask staged
-    const int pa_ = lane / k, pb_ = lane - (lane / k) * k;
+    const PathLane pl = path_lane(lane, k);
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
         const int tib = j * kIdxWaves + wave;
         const int64_t t = t0 + tib;
         if (t >= T) break;  // wave-uniform
-        const int e = index_token<EPL>(lv[j], mask_s, W, n, k, beta_mode, t, lane, pa_, pb_, ids, w,
+        const int e = index_token<EPL>(lv[j], mask_s, n, k, beta_mode, t, lane, pl, ids, w,
                                        bits_out, beta_out);
         if (lane < k) atomicOr(&words[e], 1ull << tib);
     }
@@ -264,7 +323,7 @@ __global__ __launch_bounds__(64 * kIdxSmallWaves) void route_paths_small_kernel(
     __shared__ int scan[kMaxN];
     __shared__ int wave_tot[kMaxN / 64];
     __shared__ int last;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int W = (n + 63) / 64;
     const int64_t t = (int64_t)blockIdx.x * kIdxSmallWaves + wave;
     float lv[EPL];
@@ -273,8 +332,8 @@ __global__ __launch_bounds__(64 * kIdxSmallWaves) void route_paths_small_kernel(
     for (int x = tid; x < kMaxN; x += NT) words[x] = 0ull;
     __syncthreads();
     if (t < T)  // wave-uniform
-        index_token<EPL>(lv, mask_s, W, n, k, beta_mode, t, lane, lane / k, lane - (lane / k) * k,
-                         ids, w, bits_out, beta_out);
+        index_token<EPL>(lv, mask_s, n, k, beta_mode, t, lane, path_lane(lane, k), ids, w,
+                         bits_out, beta_out);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this wave's outputs, device-wide
     __syncthreads();
     if (tid == 0)
