@@ -92,12 +92,7 @@ __device__ bool find_tile(const int32_t* __restrict__ offsets, int n, int64_t a_
             lo[j] = b;
             local += c;
         }
-        int incl = local;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int v = __shfl_up(incl, d);
-            if (lane >= d) incl += v;
-        }
+        const int incl = wave_incl_scan_i32(local);
         int start = incl - local;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -646,15 +641,10 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
             suml += nl[j];
             sums += ns[j];
         }
-        int incl = suml, incs = sums;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int vl = __shfl_up(incl, d), vs = __shfl_up(incs, d);
-            if (lane >= d) { incl += vl; incs += vs; }
-        }
+        const int incl = wave_incl_scan_i32(suml), incs = wave_incl_scan_i32(sums);
         // 32-bit arithmetic throughout: the host keeps item counts (times 8) within range
         // the short list in halves: 2 * nt N-tiles of half width
-        const int Lt = __shfl(incl, 63), St = __shfl(incs, 63);
+        const int Lt = __builtin_amdgcn_readlane(incl, 63), St = __builtin_amdgcn_readlane(incs, 63);
         const int LT = Lt * nt * g.ksplit, ST = St * 2 * nt * g.ksplit;
         const int x8 = (int)(blockIdx.x % 8), j8 = (int)(blockIdx.x / 8);
         const int l0 = x8 * LT / 8, l1 = (x8 + 1) * LT / 8;
@@ -733,14 +723,9 @@ __device__ bool em_item(const GemmArgs& g, int nt, int window, int* s_item) {
             m[j] = (c + BM - 1) / BM;
             local += m[j] * nt;
         }
-        int incl = local;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int v = __shfl_up(incl, d);
-            if (lane >= d) incl += v;
-        }
+        const int incl = wave_incl_scan_i32(local);
         // 32-bit arithmetic throughout: the host keeps item counts (times 8) within range
-        const int Tt = __shfl(incl, 63), TT = Tt * g.ksplit;
+        const int Tt = __builtin_amdgcn_readlane(incl, 63), TT = Tt * g.ksplit;
         const int x8 = (int)(blockIdx.x % 8), j8 = (int)(blockIdx.x / 8);
         const int l0 = x8 * TT / 8, l1 = (x8 + 1) * TT / 8;
         const bool valid = j8 < l1 - l0;

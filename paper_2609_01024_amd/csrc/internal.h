@@ -51,6 +51,29 @@ __device__ inline uint32_t wave_max_u32(uint32_t v) {
         : "+v"(v));
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
+// Inclusive prefix sum across the wavefront (all 64 lanes active): lane l gets v[0] + ... +
+// v[l]. Within each row of 16 lanes, adds of the value shifted by 1, 2 and 3 lanes (lanes
+// shifted in from outside the row read 0) leave sums of up to 4 lanes; adds of the running sum
+// shifted by 4 into the upper three banks of 4 lanes and by 8 into the upper two complete each
+// row; the row broadcasts used by wave_max_u32 then carry rows 0 and 2 into rows 1 and 3, and
+// rows 0-1 into rows 2-3.
+__device__ inline int wave_incl_scan_i32(int v) {
+    int s = v + __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);  // row_shr:1
+    s += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);          // row_shr:2
+    s += __builtin_amdgcn_update_dpp(0, v, 0x113, 0xF, 0xF, true);          // row_shr:3
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_add_u32_dpp %0, %0, %0 row_shr:4 bank_mask:0xe\n\t"
+        "s_nop 1\n\t"
+        "v_add_u32_dpp %0, %0, %0 row_shr:8 bank_mask:0xc\n\t"
+        "s_nop 1\n\t"
+        "v_add_u32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa\n\t"
+        "s_nop 1\n\t"
+        "v_add_u32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc\n\t"
+        "s_nop 1"
+        : "+v"(s));
+    return s;
+}
 // Largest 64-bit value across the wavefront: the largest high word, then, when more than
 // one lane holds it, the largest low word among those lanes.
 __device__ inline uint64_t wave_max_u64(uint64_t v) {

@@ -93,16 +93,11 @@ __device__ inline float readlane_f32(float v, int lane) {
 }
 
 // Exclusive scan of v over threads 0..kMaxN-1 of the workgroup (its first four waves; every
-// thread of the workgroup must call it): wave scans by shuffles, then the wave totals.
+// thread of the workgroup must call it): wave scans by DPP, then the wave totals.
 // Returns the exclusive prefix to threads < kMaxN and the total in *total for all threads.
 __device__ inline int scan_columns(int v, int* wave_tot, int* total) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    int incl = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int o = __shfl_up(incl, d);
-        if (lane >= d) incl += o;
-    }
+    const int incl = wave_incl_scan_i32(v);
     if (tid < kMaxN && lane == 63) wave_tot[wave] = incl;
     __syncthreads();
     int base = 0, all = 0;
