@@ -2,13 +2,17 @@
 
 A step is one forward pass of the whole layer (the fused indexing operation over the
 layer's packed mask, expand, project and combine, plus the shared expert when the workload
-has one) over one batch of synthetic, seeded inputs already resident in HBM. Prints ONE JSON
+has one) over one batch of synthetic, seeded inputs already resident in HBM (bf16 layers keep
+their projection weights as float16, widened once before the steps by pcm_widen_f16, which
+gives the same output bits as the bf16 weights; --down-weights bf16 times the bf16 weights,
+widened by the kernels per fragment). Prints ONE JSON
 line: the headline workload (Mixtral-shaped) at the top level with its ablation (the same
 layer per path, with and without source reuse, and the vanilla top-k layer), and every
 workload under "workloads".
 
   python bench.py [--steps K] [--warmup W] [--config NAME] [--only] [--router topk|scored]
-                  [--indexing fused|separate] [--no-cpu-baseline] [--no-ablation]
+                  [--indexing fused|separate] [--down-weights f16|bf16] [--no-cpu-baseline]
+                  [--no-ablation]
   python bench.py --trace-summary DIR     per-kernel durations (kernel traces) or counter
                                           means (--pmc runs) of the timed launches in the
                                           rocprofv3 output written under DIR
@@ -62,6 +66,10 @@ def parse():
                     help="time a decode step through L layers of the workload's shape (router GEMM, "
                          "paths, experts, residual; the first two layers diagonal-only); "
                          "reported as a separate JSON line")
+    ap.add_argument("--down-weights", choices=("f16", "bf16"), default="f16",
+                    help="projection weights of bf16 layers: float16, widened once from the bf16 "
+                         "weights by pcm_widen_f16 before the timed steps (the layer's output bits "
+                         "are the same), or the bf16 weights, widened by the kernels per fragment")
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the headline workload's ablation (the same layer executed per path, "
                          "with and without source reuse, and the vanilla top-k layer)")
@@ -232,6 +240,16 @@ def device_inputs(cfg, seed: int, host_weights: bool):
         d["shared"] = ((rnd(cfg.shared_F, cfg.H), rnd(cfg.shared_F, cfg.H), rnd(cfg.H, cfg.shared_F))
                        if cfg.shared_F else None)
     return d
+
+
+def widen_down_weights(pcm, d):
+    """Projection weights (routed and shared) as float16, widened once from the bf16 weights:
+    a per-layer weight layout prepared before any step, like the packed mask. The bf16 copies
+    are released."""
+    d["wd"] = pcm.pcm_widen_f16(d["wd"])
+    if d["shared"] is not None:
+        g, u, dn = d["shared"]
+        d["shared"] = (g, u, pcm.pcm_widen_f16(dn))
 
 
 # ------------------------------------------------------------------ one workload
@@ -558,6 +576,8 @@ def main():
         cfg = CONFIGS[name]
         t0 = time.time()
         d = device_inputs(cfg, args.seed, host_weights=(name == head))
+        if cfg.dtype == "bf16" and args.down_weights == "f16":
+            widen_down_weights(pcm, d)
         print(f"[bench] {name}: inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
         plan, sinp, ms, st, fl = measure(pcm, name, cfg, d, args, flush, scored)
         rec, f, R, touched_src = workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored)
@@ -590,6 +610,8 @@ def main():
                                        + (f" shared F={cfg.shared_F}" if cfg.shared_F else ""),
                            "tokens": cfg.T, "rows": R, "touched_experts": rec["touched_experts"],
                            "router": args.router,
+                           "down_weights": ("float16, widened once from the bf16 weights"
+                                            if bf16 and args.down_weights == "f16" else cfg.dtype),
                            **({"projection_rows": rec["projection_rows"], "lambda": sinp.lam}
                               if scored else {})},
                 "gemm_tflops": rec["gemm_tflops"], "gemm_frac_peak": rec["gemm_frac_peak"],

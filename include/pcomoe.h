@@ -50,7 +50,7 @@ typedef enum pcm_status {
 
 typedef enum pcm_dtype {
     PCM_F32 = 0,   /* x and weights float32; FMA on the vector ALUs */
-    PCM_BF16 = 1   /* x and weights bfloat16; float32 accumulate throughout. The expansion
+    PCM_BF16 = 1,  /* x and weights bfloat16; float32 accumulate throughout. The expansion
                       runs on bf16 MFMA and keeps u in float32; the projection input z is
                       carried as row-scaled float16 (11 significant bits) and the bf16
                       projection weights are widened to float16 in registers, so the
@@ -61,6 +61,12 @@ typedef enum pcm_dtype {
                       normal and upper subnormal range keep); smaller values round to the nearest
                       multiple of 2^-24 (float16's subnormal spacing; absolute error <= 2^-25),
                       so that magnitudes of 2^-25 or less become 0 */
+    PCM_BF16_F16DOWN = 2  /* a PCM_BF16 layer whose projection weights (w_down, and the shared
+                      expert's w_down) are passed as float16, widened once from the bf16
+                      weights by pcm_widen_f16: the projection then uses them as read instead
+                      of widening every fragment it loads, with bit-identical results. Every
+                      other operand is as for PCM_BF16; calls that take no projection weights
+                      treat this value as PCM_BF16. */
 } pcm_dtype;
 
 /* Path weights beta_ab for (a, b) in Pi (p = the renormalised router weights).
@@ -208,6 +214,13 @@ pcm_status pcm_dense_swiglu(pcm_dtype dtype, const void* x, const void* w_gate,
  * round to nearest even). h [T,H] of `dtype`, y [T,H] f32 (device); H a multiple of 64. */
 pcm_status pcm_residual_add(pcm_dtype dtype, void* h, const float* y, int64_t T, int H,
                             void* stream);
+
+/* Offline weight layout for PCM_BF16_F16DOWN (projection weights are fixed per layer, like the
+ * packed mask of pcm_mask_pack): w_f16[i] = w_bf16[i] rounded to float16, to nearest even,
+ * exactly as the projection kernels widen each bf16 weight fragment for PCM_BF16 (so the
+ * PCM_BF16 precondition on w_down applies). w_bf16 and w_f16 are device arrays of `count`
+ * 16-bit values (count >= 0; 16-byte aligned; they must not overlap). One launch. */
+pcm_status pcm_widen_f16(const void* w_bf16, int64_t count, void* w_f16, void* stream);
 
 /* Per-path execution of the layer, a baseline for the target-mixed projection above: the
  * path-level aggregation of Section 4.1 evaluated one projection per path, as in Section

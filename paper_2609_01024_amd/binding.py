@@ -18,7 +18,7 @@ import torch
 
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpcomoe.so")
 
-PCM_F32, PCM_BF16 = 0, 1
+PCM_F32, PCM_BF16, PCM_BF16_F16DOWN = 0, 1, 2
 BETA_SRC_COND, BETA_PRODUCT, BETA_GLOBAL = 0, 1, 2
 OP_BUILD_PATHS, OP_EXPAND, OP_PROJECT_COMBINE, OP_DENSE_SWIGLU, OP_ROUTE_SCORED = 0, 1, 2, 3, 4
 OP_LAYER_PER_PATH, OP_ROUTE_LOGITS, OP_ROUTE_PATHS = 5, 6, 7
@@ -30,7 +30,7 @@ EXPORTS = ("pcm_route", "pcm_build_paths", "pcm_expand", "pcm_project_combine",
            "pcm_residual_add", "pcm_expand_tuned", "pcm_project_combine_tuned",
            "pcm_dense_swiglu_tuned", "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
            "pcm_project_workspace_layout", "pcm_project_combine_noalloc", "pcm_mask_pack",
-           "pcm_route_paths")
+           "pcm_route_paths", "pcm_widen_f16")
 
 
 class PcmTuning(ctypes.Structure):
@@ -114,6 +114,7 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
                                              I, P, I, P, SZ, P]
     L.pcm_route_logits.argtypes = [I, P, P, I64, I, I, I, P, P, P, P, SZ, P]
     L.pcm_residual_add.argtypes = [I, P, P, I64, I, P]
+    L.pcm_widen_f16.argtypes = [P, I64, P, P]
     L.pcm_layer_per_path.argtypes = [I, P, P, P, P, ctypes.POINTER(PcmPaths), I64, I, I, I, I, I, P,
                                      I, P, SZ, P]
     TP = ctypes.POINTER(PcmTuning)
@@ -132,7 +133,7 @@ def lib(path: str = _LIB_PATH) -> ctypes.CDLL:
                  "pcm_expand_tuned", "pcm_project_combine_tuned", "pcm_dense_swiglu_tuned",
                  "pcm_expand_scored_tuned", "pcm_project_combine_scored_tuned",
                  "pcm_project_workspace_layout", "pcm_project_combine_noalloc", "pcm_mask_pack",
-                 "pcm_route_paths"):
+                 "pcm_route_paths", "pcm_widen_f16"):
         getattr(L, name).restype = I
     _lib = L
     return L
@@ -186,7 +187,16 @@ def _dtype_code(t: torch.Tensor) -> int:
         return PCM_BF16
     if t.dtype == torch.float32:
         return PCM_F32
+    if t.dtype == torch.float16:   # projection weights widened once (pcm_widen_f16)
+        return PCM_BF16_F16DOWN
     raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _layer_code(x: torch.Tensor, w_down: torch.Tensor) -> int:
+    """Layer dtype of a call that takes both activations and projection weights."""
+    if x.dtype == torch.bfloat16 and w_down.dtype == torch.float16:
+        return PCM_BF16_F16DOWN
+    return _dtype_code(x)
 
 
 def _dev(*ts):
@@ -243,6 +253,21 @@ def pcm_residual_add(h: torch.Tensor, y: torch.Tensor, stream=None) -> torch.Ten
     T, H = h.shape
     _check(lib().pcm_residual_add(_dtype_code(h), _ptr(h), _ptr(y), T, H, _stream(stream)))
     return h
+
+
+def pcm_widen_f16(w: torch.Tensor, out: torch.Tensor = None, stream=None) -> torch.Tensor:
+    """Projection weights for PCM_BF16_F16DOWN: the bf16 tensor w rounded to float16 (to
+    nearest even, as the projection kernels widen bf16 fragments). A layer passes the result
+    as w_down; the projections then give the same bits as with w."""
+    _dev(w, out)
+    if w.dtype != torch.bfloat16 or not w.is_contiguous():
+        raise TypeError("w must be a contiguous bfloat16 tensor")
+    with _on(stream):
+        out = out if out is not None else torch.empty(w.shape, dtype=torch.float16, device=w.device)
+    if out.dtype != torch.float16 or out.shape != w.shape or not out.is_contiguous():
+        raise TypeError("out must be a contiguous float16 tensor of w's shape")
+    _check(lib().pcm_widen_f16(_ptr(w), w.numel(), _ptr(out), _stream(stream)))
+    return out
 
 
 @dataclass
@@ -382,7 +407,7 @@ def pcm_dense_swiglu(x, w_gate, w_up, w_down, y=None, accumulate: bool = False,
     _dev(x, w_gate, w_up, w_down, y)
     T, H = x.shape
     Fs = w_gate.shape[0]
-    dt = _dtype_code(x)
+    dt = _layer_code(x, w_down)
     with _on(stream):
         y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
         if ws is None:
@@ -401,7 +426,7 @@ def pcm_layer_per_path(x, w_gate, w_up, w_down, paths: PathTable, reuse: bool = 
     T, H = x.shape
     n, F, _ = w_gate.shape
     k = paths.k
-    dt = _dtype_code(x)
+    dt = _layer_code(x, w_down)
     with _on(stream):
         y = y if y is not None else torch.empty((T, H), dtype=torch.float32, device=x.device)
         if ws is None:

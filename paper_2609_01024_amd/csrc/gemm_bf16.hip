@@ -227,7 +227,7 @@ __device__ inline void epilogue(const GemmArgs& g, const floatx4 (&acc)[NBK][MB]
                 *(float4*)((float*)g.out + (int64_t)r * N + f) = make_float4(v[0], v[1], v[2], v[3]);
             }
         }
-    } else if (MODE == kDownAccum && g.accumulate) {
+    } else if (base_mode(MODE) == kDownAccum && g.accumulate) {
         // read-modify-write: each row block's values are loaded before its stores
         float* O = (float*)g.out;
 #pragma unroll
@@ -288,11 +288,13 @@ __device__ inline halfx8 widen_to_f16(const bf16x8& v) {
 template <int MODE>
 struct Frag {
     using T = typename std::conditional<MODE == kExpand, bf16x8, halfx8>::type;
-    __device__ static T weights(const char* p) {
-        const bf16x8 v = *(const bf16x8*)p;
+    // a weight fragment as loaded (8 bf16 values, or 8 float16 values for half_weights)
+    __device__ static T wide(const bf16x8& v) {
         if constexpr (MODE == kExpand) return v;
+        else if constexpr (half_weights(MODE)) return __builtin_bit_cast(halfx8, v);
         else return widen_to_f16(v);
     }
+    __device__ static T weights(const char* p) { return wide(*(const bf16x8*)p); }
     __device__ static T acts(const char* p) { return *(const T*)p; }
 };
 __device__ inline floatx4 mfma_step(const bf16x8& w, const bf16x8& a, floatx4 c) {
@@ -373,6 +375,26 @@ __device__ inline uint32_t widen_pair_asm(uint32_t w) {
         : "=v"(out), "=&v"(lo), "=&v"(hi)
         : "v"(w));
     return out;
+}
+
+// bf16 -> float16 of a weight array (count values) by the same instructions as the widening
+// of each fragment in the projection kernels, so that projecting with the widened copy gives
+// the bits the bf16 weights give: 8 values per thread and step, then the count % 8 last ones.
+__global__ __launch_bounds__(256) void widen_kernel(const uint16_t* __restrict__ src, int64_t count,
+                                                    uint16_t* __restrict__ dst) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t n8 = count / 8, first = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int64_t i = first; i < n8; i += stride) {
+        const uint4 v = ((const uint4*)src)[i];
+        uint4 o;
+        o.x = widen_pair_asm(v.x);
+        o.y = widen_pair_asm(v.y);
+        o.z = widen_pair_asm(v.z);
+        o.w = widen_pair_asm(v.w);
+        ((uint4*)dst)[i] = o;
+    }
+    const int64_t i = n8 * 8 + first;
+    if (i < count) dst[i] = (uint16_t)widen_pair_asm((uint32_t)src[i]);
 }
 
 // One tile of configuration C: rows [row0, row1) of group e, N tile ntile, K slice kslice.
@@ -481,7 +503,7 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
             if (i % R_EVERY == 0 && i / R_EVERY < NR) {
                 const int j = i / R_EVERY;
                 if (j < C::NBK) {
-                    if constexpr (MODE == kExpand) nb_[j] = *(const bf16x8*)b_at(SBr, j, fo);
+                    if constexpr (MODE == kExpand || half_weights(MODE)) nb_[j] = *(const FT*)b_at(SBr, j, fo);
                     else braw[j] = *(const bf16x8*)b_at(SBr, j, fo);
                 } else {
                     na[j - C::NBK] = Frag<MODE>::acts(a_at(SAr, j - C::NBK, fo));
@@ -489,7 +511,7 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
             }
             if constexpr (decltype(loads)::value)
                 if (i % L_EVERY == 1 && i / L_EVERY < C::LPW) load(i / L_EVERY, ksa, ksb, la, lb);
-            if constexpr (MODE != kExpand) {
+            if constexpr (MODE != kExpand && !half_weights(MODE)) {
 #pragma unroll
                 for (int w = 0; w < WPS; ++w) {
                     const int d = (i - W_FROM) * WPS + w;
@@ -553,7 +575,7 @@ __device__ __forceinline__ void il_tile(const GemmArgs& g, char* lds, int e, int
     GemmArgs gs = g;
     if (kslice) gs.out = (float*)g.out + (int64_t)kslice * g.rows_total * g.N;
     // the expansion, and a projection that adds into its output: the shared epilogue
-    if (MODE == kExpand || (MODE == kDownAccum && g.accumulate)) {
+    if (MODE == kExpand || (base_mode(MODE) == kDownAccum && g.accumulate)) {
         epilogue<MODE, C::MB, C::NBK, C::WTM, C::WTN, kOutCols>(gs, acc, row0, row1, ntile, wm, wn, lane);
         return;
     }
@@ -987,7 +1009,7 @@ __global__ __launch_bounds__(SWAVES * 64) void gemm_stream_kernel(GemmArgs g, in
             } else {
                 const halfx8 a16 = __builtin_bit_cast(halfx8, abuf[j]);
 #pragma unroll
-                for (int b = 0; b < NB; ++b) acc[b] = mfma_step(widen_to_f16(wbuf[j][b]), a16, acc[b]);
+                for (int b = 0; b < NB; ++b) acc[b] = mfma_step(Frag<MODE>::wide(wbuf[j][b]), a16, acc[b]);
             }
             if (kt + SDP < KT) load(j, kt + SDP);
         }
@@ -1014,7 +1036,7 @@ __global__ __launch_bounds__(SWAVES * 64) void gemm_stream_kernel(GemmArgs g, in
             if (h >= N) continue;
             float4 v = make_float4(acc[b][0] * sc, acc[b][1] * sc, acc[b][2] * sc, acc[b][3] * sc);
             float4* dst = (float4*)((float*)g.out + (int64_t)r * N + h);
-            if (MODE == kDownAccum && g.accumulate) {
+            if (base_mode(MODE) == kDownAccum && g.accumulate) {
                 const float4 o = *dst;
                 v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
             }
@@ -1133,7 +1155,7 @@ __device__ __forceinline__ void lstream_tile(const GemmArgs& g, char* lds, int e
                     const halfx8 a16 = __builtin_bit_cast(halfx8, av);
 #pragma unroll
                     for (int b = 0; b < NB; ++b)
-                        acc[b] = mfma_step(widen_to_f16(*(const bf16x8*)(slot + b * 2048 + fo)), a16, acc[b]);
+                        acc[b] = mfma_step(Frag<MODE>::weights(slot + b * 2048 + fo), a16, acc[b]);
                 }
             }
         }
@@ -1159,7 +1181,7 @@ __device__ __forceinline__ void lstream_tile(const GemmArgs& g, char* lds, int e
             if (h >= N) continue;
             float4 v = make_float4(acc[b][0] * sc, acc[b][1] * sc, acc[b][2] * sc, acc[b][3] * sc);
             float4* dst = (float4*)((float*)g.out + (int64_t)r * N + h);
-            if (MODE == kDownAccum && g.accumulate) {
+            if (base_mode(MODE) == kDownAccum && g.accumulate) {
                 const float4 o = *dst;
                 v.x = __fadd_rn(o.x, v.x); v.y = __fadd_rn(o.y, v.y);
                 v.z = __fadd_rn(o.z, v.z); v.w = __fadd_rn(o.w, v.w);
@@ -1308,6 +1330,15 @@ int down_ksplit(int64_t R, int n, int H, int F, char tile) {
     return (tiles < 4 * 256 && (F / 2) % 64 == 0 && F / 32 >= 128) ? 2 : 1;
 }
 
+namespace {
+template <int MODE>
+hipError_t launch_mode(const GemmArgs& g, int64_t R, hipStream_t s, const GemmTune& tune, char t) {
+    if (t == 'S') return launch_stream<MODE>(g, R, s, tune.stream_depth);
+    if (t == 'M') return launch_cfg<MediumStaged, MODE, false>(g, R, s, tune);
+    return launch_cfg<LargeIl, MODE, true>(g, R, s, tune);
+}
+}  // namespace
+
 hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStream_t s,
                             const GemmTune& tune) {
     GemmArgs g = g0;
@@ -1315,19 +1346,22 @@ hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStr
     const char t = pick_tile(R, g.offsets ? g.n : 1, g.a_rows * g.K * 2, (int64_t)g.N * g.K * 2, tune.tile);
     if (g.ksplit > 1 && (mode != kDownStore || t != 'L')) return hipErrorInvalidValue;
     switch (mode) {
-        case kExpand:
-            if (t == 'S') return launch_stream<kExpand>(g, R, s, tune.stream_depth);
-            if (t == 'M') return launch_cfg<MediumStaged, kExpand, false>(g, R, s, tune);
-            return launch_cfg<LargeIl, kExpand, true>(g, R, s, tune);
+        case kExpand: return launch_mode<kExpand>(g, R, s, tune, t);
         case kDownStore:
-            if (t == 'S') return launch_stream<kDownStore>(g, R, s, tune.stream_depth);
-            if (t == 'M') return launch_cfg<MediumStaged, kDownStore, false>(g, R, s, tune);
-            return launch_cfg<LargeIl, kDownStore, true>(g, R, s, tune);
+            return g.b_f16 ? launch_mode<kDownStore | kHalfW>(g, R, s, tune, t)
+                           : launch_mode<kDownStore>(g, R, s, tune, t);
         default:
-            if (t == 'S') return launch_stream<kDownAccum>(g, R, s, tune.stream_depth);
-            if (t == 'M') return launch_cfg<MediumStaged, kDownAccum, false>(g, R, s, tune);
-            return launch_cfg<LargeIl, kDownAccum, true>(g, R, s, tune);
+            return g.b_f16 ? launch_mode<kDownAccum | kHalfW>(g, R, s, tune, t)
+                           : launch_mode<kDownAccum>(g, R, s, tune, t);
     }
+}
+
+hipError_t launch_widen_f16(const uint16_t* src, int64_t count, uint16_t* dst, hipStream_t s) {
+    if (count <= 0) return hipSuccess;
+    const int64_t n8 = count / 8;
+    const int64_t blocks = n8 > 0 ? (ceil_div(n8, 256) < 8192 ? ceil_div(n8, 256) : 8192) : 1;
+    widen_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(src, count, dst);
+    return hipGetLastError();
 }
 
 }  // namespace pcm

@@ -111,6 +111,12 @@ hipError_t launch_route_paths(const float* logits, const uint64_t* packed, int64
 size_t route_paths_ws_bytes(int64_t T, int n);
 
 enum GemmMode { kExpand = 0, kDownStore = 1, kDownAccum = 2 };
+// Flag on a projection mode inside the bf16 GEMM kernels: the projection weights are already
+// float16 (GemmArgs::b_f16), so the kernels use them as read instead of widening each bf16
+// fragment. The flag only ever sits on kDownStore or kDownAccum.
+constexpr int kHalfW = 4;
+constexpr int base_mode(int mode) { return mode & 3; }
+constexpr bool half_weights(int mode) { return (mode & kHalfW) != 0; }
 
 // Projection input of a bf16 layer. z (float32 in the mix) is stored as float16 after
 // multiplying row r by a power of two chosen from the row's largest |z| (so the largest
@@ -139,6 +145,8 @@ struct GemmArgs {
     int ksplit;                 // down-store: K split into ksplit slices, slice s writes
                                 // out + s * rows_total * N (the combine adds the slices)
     int64_t rows_total;         // rows of `out` per slice (down-store with ksplit > 1)
+    int b_f16;                  // down (bf16 layers): b0 holds float16 weights (widened once,
+                                // as pcm_widen_f16 does) instead of bf16 ones
 };
 
 // Kernel choices of a bf16 GEMM launch that a caller may force (tests and measurement, through
@@ -186,6 +194,9 @@ hipError_t launch_combine(const float* o, int ksplit, const MixMap& m, int64_t T
 
 // h = round(h + y) over N elements (N a multiple of 4; h bf16 or f32).
 hipError_t launch_residual(void* h, const float* y, int64_t N, bool bf16, hipStream_t s);
+// bf16 -> float16 (round to nearest even; the conversion the projection applies to each bf16
+// weight fragment), count values.
+hipError_t launch_widen_f16(const uint16_t* src, int64_t count, uint16_t* dst, hipStream_t s);
 
 // Grouped dispatch of counts[t] <= K distinct experts per token (ids [T,K]).
 hipError_t launch_dispatch(const int32_t* ids, const int32_t* counts, int64_t T, int n, int K,

@@ -100,6 +100,10 @@ hipError_t stage_event(const pcm_tuning* t, int i, hipStream_t s) {
     return hipEventRecord((hipEvent_t)t->stage_events[i], s);
 }
 
+// Layer dtypes: PCM_BF16_F16DOWN is a bf16 layer whose projection weights are float16.
+bool dtype_ok(pcm_dtype d) { return d == PCM_F32 || d == PCM_BF16 || d == PCM_BF16_F16DOWN; }
+bool is_bf16(pcm_dtype d) { return d == PCM_BF16 || d == PCM_BF16_F16DOWN; }
+
 // Workspace of the projection of R rows of n groups: z [R,F] (f16 for bf16 layers, f32
 // otherwise), the per-row inverse scales [R] f32 (bf16 layers), then, when `with_o`, the
 // projected rows o [ksplit, R, H] f32 (K slices of the projection); parts 256-byte aligned.
@@ -109,10 +113,10 @@ struct ProjWs {
 };
 ProjWs proj_ws(size_t R, int n, int H, int F, pcm_dtype dt, bool with_o, char tile = 0) {
     ProjWs w;
-    w.ksplit = (with_o && dt == PCM_BF16) ? down_ksplit((int64_t)R, n, H, F, tile) : 1;
-    const size_t z = align_up(R * F * (dt == PCM_BF16 ? 2 : 4), 256);
+    w.ksplit = (with_o && is_bf16(dt)) ? down_ksplit((int64_t)R, n, H, F, tile) : 1;
+    const size_t z = align_up(R * F * (is_bf16(dt) ? 2 : 4), 256);
     w.zscale_off = z;
-    w.o_off = z + (dt == PCM_BF16 ? align_up(R * sizeof(float), 256) : 0);
+    w.o_off = z + (is_bf16(dt) ? align_up(R * sizeof(float), 256) : 0);
     w.total = w.o_off + (with_o ? align_up((size_t)w.ksplit * R * H * sizeof(float), 256) : 0);
     return w;
 }
@@ -138,8 +142,8 @@ PathWs path_ws(int64_t T, int H, int F, int n, int k, pcm_dtype dt) {
     w.rof_s = take(P * 4);
     w.gather = take(P * 4);
     w.u = take(P * F * 4);
-    w.z = take(P * F * (dt == PCM_BF16 ? 2 : 4));
-    w.zscale = take(dt == PCM_BF16 ? P * 4 : 0);
+    w.z = take(P * F * (is_bf16(dt) ? 2 : 4));
+    w.zscale = take(is_bf16(dt) ? P * 4 : 0);
     w.o = take(P * H * 4);
     w.total = at;
     return w;
@@ -149,7 +153,7 @@ PathWs path_ws(int64_t T, int H, int F, int n, int k, pcm_dtype dt) {
 
 extern "C" {
 
-int pcm_abi_version(void) { return 121; }
+int pcm_abi_version(void) { return 122; }
 
 const char* pcm_status_string(pcm_status s) {
     switch (s) {
@@ -173,7 +177,7 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
             return proj_ws((size_t)T * k, n, H, F, dtype, true).total;
         case PCM_OP_ROUTE_LOGITS:
             if (H < 1 || H % 64) return 0;
-            return dtype == PCM_BF16 ? router_ws_bytes(T, H, n) : 0;
+            return is_bf16(dtype) ? router_ws_bytes(T, H, n) : 0;
         case PCM_OP_LAYER_PER_PATH:
             if (H < 1 || F < 1) return 0;
             return path_ws(T, H, F, n, k, dtype).total;
@@ -182,7 +186,7 @@ size_t pcm_workspace_bytes(pcm_op op, int64_t T, int H, int F, int n, int k, pcm
         case PCM_OP_DENSE_SWIGLU:  // the SwiGLU output u [T,F] f32, then a projection input
             if (H < 1 || F < 1) return 0;
             return align_up((size_t)T * F * sizeof(float), 256) +
-                   (dtype == PCM_BF16 ? proj_ws((size_t)T, 1, H, F, dtype, false).total : 0);
+                   (is_bf16(dtype) ? proj_ws((size_t)T, 1, H, F, dtype, false).total : 0);
     }
     return 0;
 }
@@ -204,16 +208,16 @@ pcm_status pcm_route_logits(pcm_dtype dtype, const void* x, const void* w_router
     if (st != PCM_OK) return st;
     if (H < 1) return PCM_ERR_ARG;
     if (H % 64) return PCM_ERR_UNSUPPORTED;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     if (T == 0) return PCM_OK;
     if (!x || !w_router || !topk_ids || !topk_w) return PCM_ERR_ARG;
     if (!aligned16(x) || !aligned16(w_router) || !aligned16(topk_ids) || !aligned16(topk_w) ||
         (logits && !aligned16(logits)))
         return PCM_ERR_ARG;
-    const size_t need = dtype == PCM_BF16 ? router_ws_bytes(T, H, n) : 0;
+    const size_t need = is_bf16(dtype) ? router_ws_bytes(T, H, n) : 0;
     if (ws_bytes < need || (need && !ws)) return PCM_ERR_WORKSPACE;
     if (need && !aligned16(ws)) return PCM_ERR_ARG;
-    return from_hip(launch_router(dtype == PCM_BF16, x, w_router, T, H, n, k, logits, topk_ids,
+    return from_hip(launch_router(is_bf16(dtype), x, w_router, T, H, n, k, logits, topk_ids,
                                   topk_w, (float*)ws, (hipStream_t)stream));
 }
 
@@ -221,10 +225,18 @@ pcm_status pcm_residual_add(pcm_dtype dtype, void* h, const float* y, int64_t T,
                             void* stream) {
     if (T < 0 || H < 1) return PCM_ERR_ARG;
     if (H % 64) return PCM_ERR_UNSUPPORTED;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     if (T == 0) return PCM_OK;
     if (!h || !y || !aligned16(h) || !aligned16(y)) return PCM_ERR_ARG;
-    return from_hip(launch_residual(h, y, T * (int64_t)H, dtype == PCM_BF16, (hipStream_t)stream));
+    return from_hip(launch_residual(h, y, T * (int64_t)H, is_bf16(dtype), (hipStream_t)stream));
+}
+
+pcm_status pcm_widen_f16(const void* w_bf16, int64_t count, void* w_f16, void* stream) {
+    if (count < 0) return PCM_ERR_ARG;
+    if (count == 0) return PCM_OK;
+    if (!w_bf16 || !w_f16 || !aligned16(w_bf16) || !aligned16(w_f16)) return PCM_ERR_ARG;
+    return from_hip(launch_widen_f16((const uint16_t*)w_bf16, count, (uint16_t*)w_f16,
+                                     (hipStream_t)stream));
 }
 
 pcm_status pcm_build_paths(const int32_t* topk_ids, const float* topk_w, const uint8_t* mask,
@@ -286,7 +298,7 @@ pcm_status pcm_expand_tuned(pcm_dtype dtype, const void* x, const void* w_gate, 
     pcm_status st = check_shape(T, n, k);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     GemmTune tune;
     if ((st = to_tune(tuning, true, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
@@ -305,7 +317,7 @@ pcm_status pcm_expand_tuned(pcm_dtype dtype, const void* x, const void* w_gate, 
     g.N = F;
     const int64_t R = T * k;
     hipStream_t s = (hipStream_t)stream;
-    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s, tune)
+    return from_hip(is_bf16(dtype) ? launch_gemm_bf16(kExpand, g, R, s, tune)
                                       : launch_gemm_f32(kExpand, g, R, s));
 }
 
@@ -323,7 +335,7 @@ pcm_status pcm_project_combine_tuned(pcm_dtype dtype, const void* u, const void*
     pcm_status st = check_shape(T, n, k);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     GemmTune tune;
     if ((st = to_tune(tuning, false, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
@@ -334,7 +346,7 @@ pcm_status pcm_project_combine_tuned(pcm_dtype dtype, const void* u, const void*
     if (!ws || ws_bytes < w.total) return PCM_ERR_WORKSPACE;
     if (!aligned16(ws)) return PCM_ERR_ARG;
     void* z = ws;
-    const bool bf16 = dtype == PCM_BF16;
+    const bool bf16 = is_bf16(dtype);
     float* zscale = bf16 ? (float*)((char*)ws + w.zscale_off) : nullptr;
     float* o = (float*)((char*)ws + w.o_off);
     hipStream_t s = (hipStream_t)stream;
@@ -351,6 +363,7 @@ pcm_status pcm_project_combine_tuned(pcm_dtype dtype, const void* u, const void*
     GemmArgs g{};
     g.a = z;
     g.b0 = w_down;
+    g.b_f16 = dtype == PCM_BF16_F16DOWN;
     g.out = o;
     g.row_scale = zscale;
     g.offsets = paths->expert_offsets;
@@ -383,7 +396,7 @@ pcm_status pcm_project_combine_noalloc(pcm_dtype dtype, const void* u, const voi
     pcm_status st = check_shape(T, n, k);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     if (T == 0) return PCM_OK;
     if (!u || !w_down || !y || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
     if (!aligned16(u) || !aligned16(w_down) || !aligned16(y)) return PCM_ERR_ARG;
@@ -404,13 +417,13 @@ pcm_status pcm_project_workspace_layout(pcm_dtype dtype, int64_t T, int H, int F
     pcm_status st = check_shape(T, n, k);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     GemmTune tune;
     if ((st = to_tune(tuning, false, &tune)) != PCM_OK) return st;
     if (!z_off || !zscale_off || !o_off || !ksplit) return PCM_ERR_ARG;
     const ProjWs w = proj_ws((size_t)(T * k), n, H, F, dtype, true, tune.tile);
     *z_off = 0;
-    *zscale_off = dtype == PCM_BF16 ? w.zscale_off : 0;
+    *zscale_off = is_bf16(dtype) ? w.zscale_off : 0;
     *o_off = w.o_off;
     *ksplit = w.ksplit;
     return PCM_OK;
@@ -423,7 +436,7 @@ pcm_status pcm_dense_swiglu_tuned(pcm_dtype dtype, const void* x, const void* w_
     if (T < 0) return PCM_ERR_ARG;
     pcm_status st = check_dims(H, Fs);
     if (st != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     GemmTune tune_up, tune_down;
     if ((st = to_tune(tuning, true, &tune_up)) != PCM_OK) return st;
     if ((st = to_tune(tuning, false, &tune_down)) != PCM_OK) return st;
@@ -432,7 +445,7 @@ pcm_status pcm_dense_swiglu_tuned(pcm_dtype dtype, const void* x, const void* w_
     if (!x || !w_gate || !w_up || !w_down || !y) return PCM_ERR_ARG;
     if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y))
         return PCM_ERR_ARG;
-    const bool bf16 = dtype == PCM_BF16;
+    const bool bf16 = is_bf16(dtype);
     const size_t u_bytes = align_up((size_t)T * Fs * sizeof(float), 256);
     const ProjWs w = proj_ws((size_t)T, 1, H, Fs, dtype, false);
     const size_t need = u_bytes + (bf16 ? w.total : 0);
@@ -468,6 +481,7 @@ pcm_status pcm_dense_swiglu_tuned(pcm_dtype dtype, const void* x, const void* w_
     d.a = z;
     d.row_scale = zscale;
     d.b0 = w_down;
+    d.b_f16 = dtype == PCM_BF16_F16DOWN;
     d.out = y;
     d.offsets = nullptr;
     d.a_rows = T;
@@ -493,7 +507,7 @@ pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate
     pcm_status st = check_shape(T, n, k);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     if (T * (int64_t)k * k >= ((int64_t)1 << 31)) return PCM_ERR_UNSUPPORTED;
     if (T == 0) return PCM_OK;
     if (!x || !w_gate || !w_up || !w_down || !y || check_paths(paths) != PCM_OK) return PCM_ERR_ARG;
@@ -505,7 +519,7 @@ pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate
     char* b = (char*)ws;
     auto i32 = [&](size_t off) { return (int32_t*)(b + off); };
     const int64_t R = T * k, P = T * (int64_t)k * k;
-    const bool bf16 = dtype == PCM_BF16;
+    const bool bf16 = is_bf16(dtype);
     hipStream_t s = (hipStream_t)stream;
     float* u = (float*)(b + w.u);
     void* z = b + w.z;
@@ -557,6 +571,7 @@ pcm_status pcm_layer_per_path(pcm_dtype dtype, const void* x, const void* w_gate
     GemmArgs d{};
     d.a = z;
     d.b0 = w_down;
+    d.b_f16 = dtype == PCM_BF16_F16DOWN;
     d.out = o;
     d.row_scale = zscale;
     d.offsets = i32(w.off_t);
@@ -617,7 +632,7 @@ pcm_status pcm_expand_scored_tuned(pcm_dtype dtype, const void* x, const void* w
     pcm_status st = check_shape(T, n, K);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     GemmTune tune;
     if ((st = to_tune(tuning, true, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
@@ -636,7 +651,7 @@ pcm_status pcm_expand_scored_tuned(pcm_dtype dtype, const void* x, const void* w
     g.N = F;
     const int64_t R = T * K;  // upper bound: the rows in use are src_offsets[n]
     hipStream_t s = (hipStream_t)stream;
-    return from_hip(dtype == PCM_BF16 ? launch_gemm_bf16(kExpand, g, R, s, tune)
+    return from_hip(is_bf16(dtype) ? launch_gemm_bf16(kExpand, g, R, s, tune)
                                       : launch_gemm_f32(kExpand, g, R, s));
 }
 
@@ -655,7 +670,7 @@ pcm_status pcm_project_combine_scored_tuned(pcm_dtype dtype, const void* u, cons
     pcm_status st = check_shape(T, n, K);
     if (st != PCM_OK) return st;
     if ((st = check_dims(H, F)) != PCM_OK) return st;
-    if (dtype != PCM_F32 && dtype != PCM_BF16) return PCM_ERR_ARG;
+    if (!dtype_ok(dtype)) return PCM_ERR_ARG;
     GemmTune tune;
     if ((st = to_tune(tuning, false, &tune)) != PCM_OK) return st;
     if (T == 0) return PCM_OK;
@@ -666,7 +681,7 @@ pcm_status pcm_project_combine_scored_tuned(pcm_dtype dtype, const void* u, cons
     if (!ws || ws_bytes < w.total) return PCM_ERR_WORKSPACE;
     if (!aligned16(ws)) return PCM_ERR_ARG;
     void* z = ws;
-    const bool bf16 = dtype == PCM_BF16;
+    const bool bf16 = is_bf16(dtype);
     float* zscale = bf16 ? (float*)((char*)ws + w.zscale_off) : nullptr;
     float* o = (float*)((char*)ws + w.o_off);
     hipStream_t s = (hipStream_t)stream;
@@ -686,6 +701,7 @@ pcm_status pcm_project_combine_scored_tuned(pcm_dtype dtype, const void* u, cons
     GemmArgs g{};
     g.a = z;
     g.b0 = w_down;
+    g.b_f16 = dtype == PCM_BF16_F16DOWN;
     g.out = o;
     g.row_scale = zscale;
     g.offsets = paths->tgt_offsets;

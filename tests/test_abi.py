@@ -17,7 +17,7 @@ OK, ARG, UNSUP, WS, HIP = 0, 1, 2, 3, 4
 
 def declared_functions():
     text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
-    return sorted(set(re.findall(r"\b(pcm_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(pcm_[a-z0-9_]+)\s*\(", text)))
 
 
 @pytest.fixture(scope="module")
@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert L.pcm_abi_version() == 121
+    assert L.pcm_abi_version() == 122
     for s in (OK, ARG, UNSUP, WS, HIP):
         assert L.pcm_status_string(s).decode().startswith("PCM_")
     assert L.pcm_status_string(77) == b"unknown pcm_status"
@@ -119,6 +119,26 @@ def test_build_paths_rejects_misaligned_pointers(L):
                                  None) == ARG, f
     assert L.pcm_build_paths(FAKE, FAKE, FAKE, 5000, 64, 8, 0, ctypes.byref(p), mis, need,
                              None) == ARG                                    # workspace
+
+
+def test_widen_f16_and_f16down_dtype(L):
+    mis = ctypes.c_void_p(0x10008)
+    assert L.pcm_widen_f16(FAKE, -1, FAKE, None) == ARG
+    assert L.pcm_widen_f16(None, 0, None, None) == OK                 # count 0: no-op
+    assert L.pcm_widen_f16(None, 8, FAKE, None) == ARG
+    assert L.pcm_widen_f16(FAKE, 8, None, None) == ARG
+    assert L.pcm_widen_f16(mis, 8, FAKE, None) == ARG
+    assert L.pcm_widen_f16(FAKE, 8, mis, None) == ARG
+    # a bf16 layer with float16 projection weights needs the same workspaces as a bf16 layer
+    for op in (binding.OP_PROJECT_COMBINE, binding.OP_DENSE_SWIGLU, binding.OP_LAYER_PER_PATH,
+               binding.OP_ROUTE_LOGITS):
+        assert (L.pcm_workspace_bytes(op, 1000, 1024, 2048, 16, 4, binding.PCM_BF16_F16DOWN) ==
+                L.pcm_workspace_bytes(op, 1000, 1024, 2048, 16, 4, binding.PCM_BF16)), op
+    p = _paths()
+    need = L.pcm_workspace_bytes(binding.OP_PROJECT_COMBINE, 100, 256, 256, 8, 2, 1)
+    for dt, want in ((3, ARG), (-1, ARG)):
+        assert L.pcm_project_combine(dt, FAKE, FAKE, ctypes.byref(p), 100, 256, 256, 8, 2, FAKE, 0,
+                                     FAKE, need, None) == want, dt
 
 
 def test_mask_pack_and_route_paths_validation(L):
