@@ -723,7 +723,8 @@ __device__ bool il_item(const GemmArgs& g, int nt, int GN, int* s_item) {
 // at least 1), the M-tile varying slowest within a block, so that the `window` workgroups
 // an XCD runs at once cover all of a group's rows for a few N-tiles: each weight tile is
 // fetched while every row block that needs it runs, each activation tile once per block.
-// Each XCD (bid % 8) takes a contiguous eighth of the list (every K slice, slice-major).
+// Each XCD (bid % 8) takes a contiguous eighth of the list (every K slice, slice-major), or,
+// for groups of at least 16 N tiles in multiples of 8, every eighth window (below).
 // Wave 0 counts and searches; the result is broadcast through LDS as for il_item.
 template <int BM>
 __device__ bool em_item(const GemmArgs& g, int nt, int window, int* s_item) {
@@ -745,37 +746,84 @@ __device__ bool em_item(const GemmArgs& g, int nt, int window, int* s_item) {
             m[j] = (c + BM - 1) / BM;
             local += m[j] * nt;
         }
-        const int incl = wave_incl_scan_i32(local);
-        // 32-bit arithmetic throughout: the host keeps item counts (times 8) within range
-        const int Tt = __builtin_amdgcn_readlane(incl, 63), TT = Tt * g.ksplit;
         const int x8 = (int)(blockIdx.x % 8), j8 = (int)(blockIdx.x / 8);
-        const int l0 = x8 * TT / 8, l1 = (x8 + 1) * TT / 8;
-        const bool valid = j8 < l1 - l0;
-        if (lane == 0) s_item[5] = valid ? 1 : 0;
-        if (valid) {
-            const int item = l0 + j8;
-            const int kslice = item / Tt;
-            const int id = item - kslice * Tt;
-            int start = incl - local;
+        if (g.ksplit == 1 && nt % 8 == 0 && nt >= 16) {
+            // Window-interleaved assignment: a group's N tiles are cut into windows of gw tiles,
+            // gw the largest divisor of nt / 8 not above window / m (so that every window has
+            // the same width and their number is a multiple of 8), and window i runs on XCD
+            // i % 8. Every XCD then holds exactly an eighth of every group's items and works
+            // through the groups in step with the others (the same mix of tile shapes at the
+            // same time), instead of the XCDs holding different groups whose tiles take
+            // different times (Mixtral-shaped expansion -1.9%); within a window the M-tile
+            // varies slowest. With fewer than 16 N tiles a group's activation rows would be
+            // fetched by every XCD for one N tile each (OLMoE-shaped projection +5%), so the
+            // contiguous eighths below stay.
+            const int n8 = nt / 8;
+            int gw[4], xl = 0;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int items = m[j] * nt;
-                if (id >= start && id < start + items) {
-                    const int l = id - start;
-                    int gn = window / m[j];
-                    gn = gn < 1 ? 1 : (gn > nt ? nt : gn);
-                    const int gsize = gn * m[j];
-                    const int grp = l / gsize, in = l - grp * gsize;
-                    const int gcols = min(gn, nt - grp * gn);
-                    const int mm = in / gcols;
-                    const int r0 = lo[j] + mm * BM;
-                    s_item[0] = lane * 4 + j;
-                    s_item[1] = r0;
-                    s_item[2] = min(lo[j] + cnt[j], r0 + BM);
-                    s_item[3] = grp * gn + (in - mm * gcols);
-                    s_item[4] = kslice;
+                const int lim = m[j] > 0 ? window / m[j] : 1;
+                int d = lim < 1 ? 1 : (lim > n8 ? n8 : lim);
+                while (n8 % d != 0) --d;
+                gw[j] = d;
+                xl += m[j] * n8;
+            }
+            const int xincl = wave_incl_scan_i32(xl);
+            const bool valid = j8 < __builtin_amdgcn_readlane(xincl, 63);
+            if (lane == 0) s_item[5] = valid ? 1 : 0;
+            if (valid) {
+                int start = xincl - xl;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int items = m[j] * n8;
+                    if (j8 >= start && j8 < start + items) {
+                        const int q = j8 - start;
+                        const int gsize = gw[j] * m[j];
+                        const int kw = q / gsize, in = q - kw * gsize;
+                        const int grp = kw * 8 + x8;       // the group's window on this XCD
+                        const int mm = in / gw[j];
+                        const int r0 = lo[j] + mm * BM;
+                        s_item[0] = lane * 4 + j;
+                        s_item[1] = r0;
+                        s_item[2] = min(lo[j] + cnt[j], r0 + BM);
+                        s_item[3] = grp * gw[j] + (in - mm * gw[j]);
+                        s_item[4] = 0;
+                    }
+                    start += items;
                 }
-                start += items;
+            }
+        } else {
+            const int incl = wave_incl_scan_i32(local);
+            // 32-bit arithmetic throughout: the host keeps item counts (times 8) within range
+            const int Tt = __builtin_amdgcn_readlane(incl, 63), TT = Tt * g.ksplit;
+            const int l0 = x8 * TT / 8, l1 = (x8 + 1) * TT / 8;
+            const bool valid = j8 < l1 - l0;
+            if (lane == 0) s_item[5] = valid ? 1 : 0;
+            if (valid) {
+                const int item = l0 + j8;
+                const int kslice = item / Tt;
+                const int id = item - kslice * Tt;
+                int start = incl - local;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int items = m[j] * nt;
+                    if (id >= start && id < start + items) {
+                        const int l = id - start;
+                        int gn = window / m[j];
+                        gn = gn < 1 ? 1 : (gn > nt ? nt : gn);
+                        const int gsize = gn * m[j];
+                        const int grp = l / gsize, in = l - grp * gsize;
+                        const int gcols = min(gn, nt - grp * gn);
+                        const int mm = in / gcols;
+                        const int r0 = lo[j] + mm * BM;
+                        s_item[0] = lane * 4 + j;
+                        s_item[1] = r0;
+                        s_item[2] = min(lo[j] + cnt[j], r0 + BM);
+                        s_item[3] = grp * gn + (in - mm * gcols);
+                        s_item[4] = kslice;
+                    }
+                    start += items;
+                }
             }
         }
     }

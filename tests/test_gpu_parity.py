@@ -196,6 +196,9 @@ SMALL = {
     # one and two 64-wide K stages (H = 64, F = 128): the pipelines' start-up loads past the
     # last stage are clamped re-reads
     "shortk_s": scaled(CONFIGS["mixtral"], T=700, H=64, F=128, n=4, name="shortk_s"),
+    # 16 N tiles per group in the expansion: the expert-major order deals each group's windows
+    # over the 8 XCDs (window-interleaved), with one to four 256-row tiles per expert
+    "wide_s": scaled(CONFIGS["mixtral"], T=1500, H=256, F=2048, name="wide_s"),
 }
 
 
@@ -318,7 +321,7 @@ def test_dense_swiglu_large_tile_tails(T):
     assert_y_close(y.cpu().numpy(), ref, cfg.dtype, f"dense T={T}")
 
 
-@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "splitk_s"])
+@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "splitk_s", "wide_s"])
 def test_large_tile_work_orders_bit_identical(name):
     """The work order of the large tiles (grouped, longest first, expert-major with several
     windows) decides only which workgroup computes which tile: the layer output must be the
