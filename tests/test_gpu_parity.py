@@ -266,6 +266,35 @@ def test_expand_rows_against_oracle():
     assert np.all(np.abs(got - ref) <= 1e-5 * np.abs(ref) + 1e-5 * scale)
 
 
+@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "decode_s", "wide_s"])
+def test_expand_output_bits_across_kernels(name):
+    """Every expansion kernel (streaming at each ring depth and the register ring, medium
+    tiles, large tiles in every work order) writes the same U bits: the same MFMA products in
+    the same order and the same SwiGLU epilogue. U starts as NaN, so an element that no kernel
+    writes shows. mixtral_s has a half-filled last N tile (F = 448)."""
+    cfg = SMALL[name]
+    d = dev(make_inputs(cfg, seed=24))
+    ids, w = pcm.pcm_route(d["logits"], cfg.k)
+    p = pcm.pcm_build_paths(ids, w, d["mask"])
+    u = torch.empty((cfg.T * cfg.k, cfg.F), dtype=torch.float32, device=DEV)
+
+    def run(tuning):
+        u.fill_(float("nan"))
+        pcm.pcm_expand(d["x"], d["w_gate"], d["w_up"], p, u=u, tuning=tuning)
+        torch.cuda.synchronize()
+        return u.cpu().numpy().copy()
+
+    base = run(None)
+    assert np.isfinite(base).all()
+    for t in [dict(tile="S", stream_depth=0), dict(tile="S", stream_depth=2),
+              dict(tile="S", stream_depth=6), dict(tile="M"), dict(tile="L", order_expand=0),
+              dict(tile="L", order_expand=1), dict(tile="L", order_expand=2, em_window=1),
+              dict(tile="L", order_expand=2, em_window=12)]:
+        say(f"expansion kernels {name} {t}")
+        got = run(pcm.Tuning(**t))
+        assert np.array_equal(got.view(np.uint32), base.view(np.uint32)), f"{name} {t}"
+
+
 def test_layer_diagonal_mask_is_vanilla():
     """Only diagonal paths: the GPU layer equals the vanilla top-k MoE of the oracle."""
     cfg = scaled(SMALL["olmoe_s"], density=0.0, name="olmoe_diag")
