@@ -317,8 +317,11 @@ pcm_status pcm_project_combine_scored(pcm_dtype dtype, const void* u, const void
  * each stage on the stream it runs on. Values outside the documented sets give PCM_ERR_ARG. */
 typedef struct pcm_tuning {
     int tile;              /* 0: chosen by the mean rows per expert; 'S' the few-row streaming
-                              kernel, 'M' the medium tiles, 'L' the large tiles (the medium tiles
-                              run instead where 32-bit buffer offsets would not reach) */
+                              kernel, 'M' the medium tiles, 'L' the large tiles on four waves,
+                              'W' the large tiles on eight waves (two per SIMD; the default
+                              for an expansion that takes the large tiles); for 'L' and 'W'
+                              the medium tiles run instead where 32-bit buffer offsets would
+                              not reach */
     int order_expand;      /* work order of the large tiles in expansion GEMMs: -1 by shape,
                               0 grouped, 1 longest first, 2 expert-major */
     int order_down;        /* the same for projection GEMMs */

@@ -45,7 +45,7 @@ class Tuning:
     library's own choices. stage_events: four torch.cuda.Event (created by a first record)
     that the project-and-combine calls record before the mix, the projection GEMM, the combine
     and after it."""
-    tile: str = ""              # "", "S", "M" or "L"
+    tile: str = ""              # "", "S", "M", "L" (four waves) or "W" (eight waves)
     order_expand: int = -1
     order_down: int = -1
     em_window: int = 0

@@ -329,7 +329,7 @@ struct ICfg {
     // schedule of a substep: MFMA i is followed by fragment read i / R_EVERY (weights
     // first), load i / L_EVERY and, from slot W_FROM on, WPS dwords of weight widening
     static constexpr int NM = NBK * MB, NR = NBK + MB;
-    static constexpr int R_EVERY = 3 * (NR - 1) < NM ? 3 : 2;
+    static constexpr int R_EVERY = 3 * (NR - 1) < NM ? 3 : (2 * (NR - 1) < NM ? 2 : 1);
     static constexpr int L_EVERY = NM / LPW;
     static constexpr int W_FROM = R_EVERY * NBK + 2;
     static constexpr int WPS = (4 * NBK + (NM - W_FROM) - 1) / (NM - W_FROM);
@@ -345,6 +345,10 @@ struct ICfg {
 // (each wave 64 x 128), which halves the MFMA work spent on padding rows.
 using LargeIl = ICfg<256, 256, 2, 2>;
 using LargeIlTail = ICfg<128, 256, 2, 2>;
+// The same tiles on eight waves, two per SIMD (each 128 x 64, 128 accumulators): while one
+// wave of a SIMD waits at a barrier or for its fragment reads, the other can issue MFMAs.
+using WideIl = ICfg<256, 256, 2, 4>;
+using WideIlTail = ICfg<128, 256, 2, 4>;
 
 // MFMA through inline assembly with the accumulator pinned to AGPRs ("a" constraint):
 // 256 accumulators per lane exceed what the compiler keeps in AGPRs across a loop without
@@ -1302,12 +1306,12 @@ hipError_t launch_stream(const GemmArgs& g, int64_t R, hipStream_t s, int depth)
 }
 
 // ---------------------------------------------------------------------- launch
-template <class C, int MODE, bool IL>
+template <class C, int MODE, bool IL, class CT = LargeIlTail>
 hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s, const GemmTune& t) {
     // set on every launch (idempotent, and the library keeps no state between calls)
     const void* fn;
     if constexpr (IL)
-        fn = (const void*)gemm_il_kernel<C, LargeIlTail, MODE>;
+        fn = (const void*)gemm_il_kernel<C, CT, MODE>;
     else
         fn = (const void*)gemm_staged_kernel<C, MODE>;
     const hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
@@ -1346,7 +1350,7 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s, const GemmTun
         } else {
             grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
         }
-        gemm_il_kernel<C, LargeIlTail, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(
+        gemm_il_kernel<C, CT, MODE><<<dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, s>>>(
             g, mt_upper, nt, gparam, order);
     } else {
         const int64_t grid = ceil_div(mt_upper * nt, 8) * 8 * g.ksplit;
@@ -1361,7 +1365,8 @@ hipError_t launch_cfg(const GemmArgs& g, int64_t R, hipStream_t s, const GemmTun
 // 4 GiB (a_bytes: all rows of `a`; w_bytes: one group's weights).
 char pick_tile(int64_t R, int groups, int64_t a_bytes, int64_t w_bytes, char tile) {
     const bool large_ok = a_bytes < (int64_t(1) << 32) && w_bytes < (int64_t(1) << 32);
-    if (tile == 'S' || tile == 'M' || tile == 'L') return tile == 'L' && !large_ok ? 'M' : tile;
+    if (tile == 'S' || tile == 'M' || tile == 'L' || tile == 'W')
+        return (tile == 'L' || tile == 'W') && !large_ok ? 'M' : tile;
     // below 16 rows per group the streaming kernel (weights streamed once, little MFMA work
     // wasted on padding); from 16 on the large tiles, which were faster than the medium ones
     // at every size measured (Mixtral-shaped, 1024 tokens: 2.6 -> 0.87 ms for the two GEMMs
@@ -1379,7 +1384,8 @@ int down_ksplit(int64_t R, int n, int H, int F, char tile) {
     // round of the chip the K split doubles the workgroups; from one round on the longest-first
     // order (tail items as halves) fills the last round as well without the second o slice
     // (Mixtral-shaped projection and combine 922 -> 902 us, with 268 MB less o traffic)
-    if (pick_tile(R, n, R * F * 2, (int64_t)H * F * 2, tile) != 'L') return 1;
+    const char t = pick_tile(R, n, R * F * 2, (int64_t)H * F * 2, tile);
+    if (t != 'L' && t != 'W') return 1;
     const int64_t tiles = (ceil_div(R, 256) + n) * ceil_div(H, 256);
     return (tiles < 256 && (F / 2) % 64 == 0 && F / 32 >= 128) ? 2 : 1;
 }
@@ -1389,6 +1395,11 @@ template <int MODE>
 hipError_t launch_mode(const GemmArgs& g, int64_t R, hipStream_t s, const GemmTune& tune, char t) {
     if (t == 'S') return launch_stream<MODE>(g, R, s, tune.stream_depth);
     if (t == 'M') return launch_cfg<MediumStaged, MODE, false>(g, R, s, tune);
+    // the large tiles: eight waves for the expansion, four for the projections (interleaved
+    // A/B, bit-identical: expansion -2.7% / -2.4% / -0.3% on the Mixtral-, OLMoE- and
+    // fine-grained-shaped layers, projections +1% to +1.7%)
+    if (t == 'W' || (t == 'L' && MODE == kExpand && tune.tile != 'L'))
+        return launch_cfg<WideIl, MODE, true, WideIlTail>(g, R, s, tune);
     return launch_cfg<LargeIl, MODE, true>(g, R, s, tune);
 }
 }  // namespace
@@ -1398,7 +1409,7 @@ hipError_t launch_gemm_bf16(GemmMode mode, const GemmArgs& g0, int64_t R, hipStr
     GemmArgs g = g0;
     if (g.ksplit < 1) g.ksplit = 1;
     const char t = pick_tile(R, g.offsets ? g.n : 1, g.a_rows * g.K * 2, (int64_t)g.N * g.K * 2, tune.tile);
-    if (g.ksplit > 1 && (mode != kDownStore || t != 'L')) return hipErrorInvalidValue;
+    if (g.ksplit > 1 && (mode != kDownStore || (t != 'L' && t != 'W'))) return hipErrorInvalidValue;
     switch (mode) {
         case kExpand: return launch_mode<kExpand>(g, R, s, tune, t);
         case kDownStore:

@@ -80,7 +80,8 @@ pcm_status check_layout(const pcm_path_layout* l) {
 pcm_status to_tune(const pcm_tuning* t, bool expansion, GemmTune* out) {
     *out = GemmTune();
     if (!t) return PCM_OK;
-    if (t->tile != 0 && t->tile != 'S' && t->tile != 'M' && t->tile != 'L') return PCM_ERR_ARG;
+    if (t->tile != 0 && t->tile != 'S' && t->tile != 'M' && t->tile != 'L' && t->tile != 'W')
+        return PCM_ERR_ARG;
     if (t->order_expand < -1 || t->order_expand > 2 || t->order_down < -1 || t->order_down > 2)
         return PCM_ERR_ARG;
     if (t->em_window < 0 || t->group_n < 0) return PCM_ERR_ARG;

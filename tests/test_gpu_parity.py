@@ -202,7 +202,7 @@ SMALL = {
 }
 
 
-@pytest.mark.parametrize("tile", ["auto", "S", "M", "L"])
+@pytest.mark.parametrize("tile", ["auto", "S", "M", "L", "W"])
 @pytest.mark.parametrize("name", sorted(SMALL))
 def test_layer_small(name, tile):
     tuning = pcm.Tuning(tile=tile) if tile != "auto" else None
@@ -289,7 +289,9 @@ def test_expand_output_bits_across_kernels(name):
     for t in [dict(tile="S", stream_depth=0), dict(tile="S", stream_depth=2),
               dict(tile="S", stream_depth=6), dict(tile="M"), dict(tile="L", order_expand=0),
               dict(tile="L", order_expand=1), dict(tile="L", order_expand=2, em_window=1),
-              dict(tile="L", order_expand=2, em_window=12)]:
+              dict(tile="L", order_expand=2, em_window=12), dict(tile="W", order_expand=0),
+              dict(tile="W", order_expand=1), dict(tile="W", order_expand=2, em_window=1),
+              dict(tile="W", order_expand=2, em_window=12)]:
         say(f"expansion kernels {name} {t}")
         got = run(pcm.Tuning(**t))
         assert np.array_equal(got.view(np.uint32), base.view(np.uint32)), f"{name} {t}"
@@ -337,14 +339,15 @@ def test_dense_swiglu_accumulate():
 
 
 @pytest.mark.parametrize("T", [513, 640, 641, 767, 768])
-def test_dense_swiglu_large_tile_tails(T):
-    """One group of T rows on the 256 x 256 tiles: the last tile holds T mod 256 rows, and
-    runs on the 128-row tail shape when that remainder is at most 128."""
+@pytest.mark.parametrize("tile", ["L", "W"])
+def test_dense_swiglu_large_tile_tails(T, tile):
+    """One group of T rows on the 256 x 256 tiles (four or eight waves): the last tile holds
+    T mod 256 rows, and runs on the 128-row tail shape when that remainder is at most 128."""
     cfg = scaled(CONFIGS["finegrained_shared"], T=T, H=256, F=64, shared_F=512, name=f"dense{T}")
-    say(f"dense swiglu T={T}")
+    say(f"dense swiglu T={T} tile {tile}")
     inp = make_inputs(cfg, seed=8)
     d = dev(inp)
-    y = pcm.pcm_dense_swiglu(d["x"], *d["shared"], tuning=pcm.Tuning(tile="L"))
+    y = pcm.pcm_dense_swiglu(d["x"], *d["shared"], tuning=pcm.Tuning(tile=tile))
     torch.cuda.synchronize()
     ref = oracle.dense_swiglu(inp.x, inp.s_gate, inp.s_up, inp.s_down)
     assert_y_close(y.cpu().numpy(), ref, cfg.dtype, f"dense T={T}")
@@ -372,10 +375,12 @@ def test_large_tile_work_orders_bit_identical(name):
     base = run(pcm.Tuning(tile="L"))
     assert np.isfinite(base).all()
     assert_y_close(base, oracle.layer_inputs(inp), cfg.dtype, f"{name}/default order")
-    for order, window in [(0, 0), (1, 0), (2, 1), (2, 5), (2, 12), (2, 64)]:
-        say(f"work order {order} window {window} on {name}")
-        y = run(pcm.Tuning(tile="L", order_expand=order, order_down=order, em_window=window))
-        assert np.array_equal(y, base), f"{name}: order {order} window {window} changed the output"
+    for tile in ("L", "W"):      # the large tiles on four and on eight waves
+        for order, window in [(0, 0), (1, 0), (2, 1), (2, 5), (2, 12), (2, 64)]:
+            say(f"work order {order} window {window} tile {tile} on {name}")
+            y = run(pcm.Tuning(tile=tile, order_expand=order, order_down=order, em_window=window))
+            assert np.array_equal(y, base), \
+                f"{name}: tile {tile} order {order} window {window} changed the output"
 
 
 @pytest.mark.parametrize("name", ["decode_s", "olmoe_s", "fine_s"])
