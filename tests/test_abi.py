@@ -193,9 +193,15 @@ def test_tuning_validation(L):
                                               *(ctypes.byref(ctypes.c_size_t()) for _ in range(3)),
                                               ctypes.byref(ctypes.c_int())) == ARG, field
     # a valid tuning passes validation (T = 0 is a no-op), NULL tuning is the plain call
-    t = binding.Tuning(tile="L", order_expand=2, em_window=5, stream_depth=0).struct()
-    assert L.pcm_expand_tuned(1, None, None, None, None, 0, 128, 128, 8, 2, None, None, 0, None,
-                              ctypes.byref(t)) == OK
+    for tile in ("S", "M", "L", "W"):
+        t = binding.Tuning(tile=tile, order_expand=2, em_window=5, stream_depth=0).struct()
+        assert L.pcm_expand_tuned(1, None, None, None, None, 0, 128, 128, 8, 2, None, None, 0, None,
+                                  ctypes.byref(t)) == OK, tile
+    # the K split follows the tile family: the large tiles on four or eight waves split, the
+    # medium tiles do not
+    for tile, ks in (("L", 2), ("W", 2), ("M", 1)):
+        assert binding.project_workspace_layout(300, 256, 4096, 4, 2, binding.PCM_BF16,
+                                                binding.Tuning(tile=tile))["ksplit"] == ks, tile
     assert L.pcm_expand_tuned(1, FAKE, FAKE, FAKE, bp, 4, 100, 128, 8, 2, FAKE, None, 0, None,
                               None) == UNSUP
 
