@@ -12,7 +12,7 @@ workload under "workloads".
 
   python bench.py [--steps K] [--warmup W] [--config NAME] [--only] [--router topk|scored]
                   [--indexing fused|separate] [--down-weights f16|bf16] [--no-cpu-baseline]
-                  [--no-ablation]
+                  [--no-ablation] [--no-graph]
   python bench.py --trace-summary DIR     per-kernel durations (kernel traces) or counter
                                           means (--pmc runs) of the timed launches in the
                                           rocprofv3 output written under DIR
@@ -21,9 +21,13 @@ Per-kernel times come from HIP events recorded on the stream the kernels run on:
 each call, and inside pcm_project_combine between the mix, the projection GEMM and the
 combine (pcm_tuning's stage events). A second pass over the same steps writes a 512 MB
 buffer before each step, so that the memory-bound stages (indexing, mix, combine)
-read from HBM rather than from the 256 MB MALL; their GB/s come from that pass.
-The timed region is fenced by two short spin kernels, which --trace-summary uses to keep
-only the timed launches of a rocprofv3 trace. The CPU baseline times the float64 oracle on
+read from HBM rather than from the 256 MB MALL; their GB/s come from that pass. Then the
+same step is captured as one HIP graph (LayerPlan.capture's capture_graph) and its replays are
+timed the same way (ms_graph and tokens_per_s_graph per workload: the layer without the host's
+per-call cost; the headline stays the eager figure).
+The eager timed region and the graph replays are each fenced by two short spin kernels, which
+--trace-summary uses to keep only the timed launches of a rocprofv3 trace (region 0 the eager
+steps, region 1 the replays). The CPU baseline times the float64 oracle on
 a bounded sample of the headline workload's tokens.
 """
 from __future__ import annotations
@@ -70,6 +74,9 @@ def parse():
                     help="projection weights of bf16 layers: float16, widened once from the bf16 "
                          "weights by pcm_widen_f16 before the timed steps (the layer's output bits "
                          "are the same), or the bf16 weights, widened by the kernels per fragment")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the timing of each workload's step captured as one HIP graph "
+                         "(ms_graph, tokens_per_s_graph beside the eager figures)")
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the headline workload's ablation (the same layer executed per path, "
                          "with and without source reuse, and the vanilla top-k layer)")
@@ -353,7 +360,25 @@ def measure(pcm, name, cfg, d, args, flush, scored):
         step(fslots[s])
     torch.cuda.synchronize()
     flushed = stage_ms(fslots)
-    return plan, sinp, wall * 1e3 / args.steps, timed, flushed
+    # the same step captured as one HIP graph (no per-call host cost), its replays timed like the
+    # eager steps; kept beside the eager figure, which stays the headline
+    graph_ms = None
+    if not args.no_graph:
+        graph = binding.capture_graph(lambda: step(None))
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        fence()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        fence()
+        torch.cuda.synchronize()
+        del graph
+    return plan, sinp, wall * 1e3 / args.steps, timed, flushed, graph_ms
 
 
 def workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored):
@@ -579,8 +604,11 @@ def main():
         if cfg.dtype == "bf16" and args.down_weights == "f16":
             widen_down_weights(pcm, d)
         print(f"[bench] {name}: inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
-        plan, sinp, ms, st, fl = measure(pcm, name, cfg, d, args, flush, scored)
+        plan, sinp, ms, st, fl, graph_ms = measure(pcm, name, cfg, d, args, flush, scored)
         rec, f, R, touched_src = workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored)
+        if graph_ms is not None:
+            rec["ms_graph"] = round(graph_ms, 4)
+            rec["tokens_per_s_graph"] = round(cfg.T / (graph_ms * 1e-3), 1)
         records[name] = rec
         print(f"[bench] {name}: {ms:.3f} ms per layer", file=sys.stderr, flush=True)
         if name == head:

@@ -13,7 +13,7 @@ from .binding import (BETA_GLOBAL, BETA_PRODUCT, BETA_SRC_COND, PCM_BF16, PCM_BF
                       pcm_project_combine_scored,
                       pcm_residual_add, pcm_route, pcm_route_logits, pcm_route_scored,
                       pcm_mask_pack, pcm_route_paths, pcm_widen_f16,
-                      workspace_bytes)
+                      capture_graph, workspace_bytes)
 
 __all__ = ["BETA_GLOBAL", "BETA_PRODUCT", "BETA_SRC_COND", "PCM_BF16", "PCM_BF16_F16DOWN", "PCM_F32",
            "LayerPlan",
@@ -24,4 +24,4 @@ __all__ = ["BETA_GLOBAL", "BETA_PRODUCT", "BETA_SRC_COND", "PCM_BF16", "PCM_BF16
            "pcm_project_combine_scored",
            "pcm_residual_add", "pcm_route", "pcm_route_logits", "pcm_route_scored",
            "pcm_mask_pack", "pcm_route_paths", "pcm_widen_f16",
-           "workspace_bytes"]
+           "capture_graph", "workspace_bytes"]

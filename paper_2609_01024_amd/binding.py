@@ -555,6 +555,23 @@ def pcm_project_combine_scored(u, w_down, paths: ScoredPathTable, y=None, accumu
     return y
 
 
+def capture_graph(fn) -> "torch.cuda.CUDAGraph":
+    """A HIP graph of fn() (a layer plan's forward on fixed tensors, whose contents are read at
+    every replay): graph.replay() then enqueues the whole layer as one launch on the current
+    stream, without the host-side cost of each call. fn runs once eagerly on a side stream first
+    (so every lazy initialisation happens outside the capture). A plan's forward allocates
+    nothing and clears nothing (no memset nodes), so the graph holds kernel nodes only."""
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(g):
+        fn()
+    return g
+
+
 class ScoredLayerPlan:
     """Preallocated buffers for the scored-routing layer (forward enqueues kernels only).
     The active-pair layout is built once per layer (build_layout)."""
@@ -587,6 +604,12 @@ class ScoredLayerPlan:
         pcm_project_combine_scored(self.u, w_down, self.paths, y=self.y, accumulate=shared is not None,
                                    ws=self.ws_proj, stream=stream, tuning=tuning)
         return self.y
+
+    def capture(self, x, g_base, g_tgt, lam, w_gate, w_up, w_down, shared=None,
+                tuning: Optional[Tuning] = None) -> "torch.cuda.CUDAGraph":
+        """forward() on these tensors as a HIP graph (capture_graph); replay() writes self.y."""
+        return capture_graph(lambda: self.forward(x, g_base, g_tgt, lam, w_gate, w_up, w_down, shared,
+                                                  tuning=tuning))
 
 
 class LayerPlan:
@@ -633,6 +656,14 @@ class LayerPlan:
         pcm_project_combine(self.u, w_down, self.paths, y=self.y, accumulate=shared is not None,
                             ws=self.ws_proj, stream=stream, tuning=tuning)
         return self.y
+
+    def capture(self, x, logits, mask, w_gate, w_up, w_down, shared=None,
+                tuning: Optional[Tuning] = None) -> "torch.cuda.CUDAGraph":
+        """forward() on these tensors as a HIP graph (capture_graph); replay() writes self.y.
+        With the packed mask (pcm_mask_pack) of T <= 64 tokens the indexing's completion counter
+        returns to zero at the end of every replay, as after every eager call."""
+        return capture_graph(lambda: self.forward(x, logits, mask, w_gate, w_up, w_down, shared,
+                                                  tuning=tuning))
 
 
 def layer_forward(x, logits, mask, w_gate, w_up, w_down, k: int, beta_mode: int = BETA_SRC_COND,
