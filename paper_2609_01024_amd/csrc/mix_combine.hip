@@ -14,9 +14,11 @@
 namespace pcm {
 namespace {
 
+// U is read once, by the mix: its loads are non-temporal
 __device__ inline void load8(const float* p, float* v) {
-    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    const floatx4 a = __builtin_nontemporal_load((const floatx4*)p);
+    const floatx4 b = __builtin_nontemporal_load((const floatx4*)(p + 4));
+    v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3]; v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
 }
 
 struct TokenPaths {
@@ -102,9 +104,8 @@ __global__ __launch_bounds__(256) void mix_kernel(const float* __restrict__ u, v
 #pragma unroll
         for (int b = 0; b < kMaxK; ++b) {
             if (b >= p.nt) break;
-            float v = mx[b];
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+            // magnitudes are >= 0 (NaN never enters mx), so their bits order as the values
+            const float v = __uint_as_float(wave_max_u32(__float_as_uint(mx[b])));
             if (lane == 0) red[b][wave] = v;
         }
         __syncthreads();
@@ -182,8 +183,8 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
                 if constexpr (CPT == 8) {
                     load8(u + p.src[a] * F + c, ua[a]);
                 } else {
-                    const float4 v = *(const float4*)(u + p.src[a] * F + c);
-                    ua[a][0] = v.x; ua[a][1] = v.y; ua[a][2] = v.z; ua[a][3] = v.w;
+                    const floatx4 v = __builtin_nontemporal_load((const floatx4*)(u + p.src[a] * F + c));
+                    ua[a][0] = v[0]; ua[a][1] = v[1]; ua[a][2] = v[2]; ua[a][3] = v[3];
                 }
             }
 #pragma unroll
@@ -207,9 +208,8 @@ __global__ __launch_bounds__(1024) void mix_regs_kernel(const float* __restrict_
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
     for (int b = 0; b < KK; ++b) {
-        float v = mx[b];
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+        // magnitudes are >= 0 (NaN never enters mx), so their bits order as the values
+        const float v = __uint_as_float(wave_max_u32(__float_as_uint(mx[b])));
         if (lane == 0) red[b][wave] = v;
     }
     __syncthreads();
