@@ -17,9 +17,11 @@ workload under "workloads".
                                           means (--pmc runs) of the timed launches in the
                                           rocprofv3 output written under DIR
 
-Per-kernel times come from HIP events recorded on the stream the kernels run on: around
-each call, and inside pcm_project_combine between the mix, the projection GEMM and the
-combine (pcm_tuning's stage events). A second pass over the same steps writes a 512 MB
+The timed steps run the layer's calls only; per-kernel times come from a second pass over the
+same steps with HIP events recorded on the stream the kernels run on: around each call, and
+inside pcm_project_combine between the mix, the projection GEMM and the combine (pcm_tuning's
+stage events); that pass's wall time per step is reported as ms_with_stage_events. A third
+pass over the same steps writes a 512 MB
 buffer before each step, so that the memory-bound stages (indexing, mix, combine)
 read from HBM rather than from the 256 MB MALL; their GB/s come from that pass. Then the
 same step is captured as one HIP graph (LayerPlan.capture's capture_graph) and its replays are
@@ -341,18 +343,26 @@ def measure(pcm, name, cfg, d, args, flush, scored):
 
     for _ in range(args.warmup):
         step()
-    slots = [new_events() for _ in range(args.steps)]
+    # the timed steps: the layer's calls only (no event records inside the steps)
     torch.cuda.synchronize()
     fence()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        step(slots[s])
+        step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     fence()
     torch.cuda.synchronize()
+    # the same steps again with HIP events between the stages, for the per-stage times
+    slots = [new_events() for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(slots[s])
+    torch.cuda.synchronize()
+    wall_events = time.perf_counter() - t0
     timed = stage_ms(slots)
+    timed["step_with_events"] = wall_events * 1e3 / args.steps
     # the same steps with the MALL flushed before each (outside the recorded stages)
     fslots = [new_events() for _ in range(args.steps)]
     for s in range(args.steps):
@@ -423,7 +433,8 @@ def workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored):
            "paths": n_paths,
            "gemm_tflops": round(f["total"] / (gemm_ms * 1e-3) / 1e12, 1),
            "gemm_frac_peak": round(f["total"] / (gemm_ms * 1e-3) / 1e12 / peak, 4),
-           "stages_ms": {k: round(v, 4) for k, v in st.items()},
+           "ms_with_stage_events": round(st["step_with_events"], 4),
+           "stages_ms": {k: round(v, 4) for k, v in st.items() if k != "step_with_events"},
            "stages_flushed_ms": {k: round(v, 4) for k, v in fl.items()},
            "hbm_GBps": {k: round(v, 1) for k, v in hbm.items()},
            "hbm_frac": {k: round(v / acc.HBM_PEAK_GBS, 4) for k, v in hbm.items()}}
@@ -479,6 +490,20 @@ def stack_bench(args):
         st.forward(h)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_graph = None
+    if not args.no_graph:   # the step's layers as one HIP graph (the reset of h stays eager)
+        graph = st.capture(h)
+        for _ in range(args.warmup):
+            h.copy_(x0)
+            graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            h.copy_(x0)
+            graph.replay()
+        torch.cuda.synchronize()
+        ms_graph = (time.perf_counter() - t0) * 1e3 / args.steps
+        del graph
     wbytes = args.stack * 3 * cfg.n * cfg.H * cfg.F * (2 if dtype == torch.bfloat16 else 4)
     line = {"metric": "decode step through a stack of path-MoE layers, tokens/sec, 1 GPU",
             "value": round(cfg.T / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
@@ -490,6 +515,9 @@ def stack_bench(args):
                                    f"density {cfg.density}", "layers": args.stack},
             "ms_per_layer": round(ms / args.stack, 4),
             "all_expert_weight_GB": round(wbytes / 1e9, 1)}
+    if ms_graph is not None:
+        line["ms_per_step_graph"] = round(ms_graph, 4)
+        line["tokens_per_s_graph"] = round(cfg.T / (ms_graph * 1e-3), 1)
     print(json.dumps(line), flush=True)
 
 

@@ -60,6 +60,12 @@ class MoEStack:
             self.layer_step(l, h, stream=stream)
         return h
 
+    def capture(self, h: torch.Tensor) -> "torch.cuda.CUDAGraph":
+        """forward(h) as one HIP graph (binding.capture_graph): each replay runs every layer on
+        h's current contents, in place. The capture's eager warm-up runs forward(h) once, so
+        set h after capturing and before each replay."""
+        return b.capture_graph(lambda: self.forward(h))
+
 
 def random_stack(L: int, T: int, H: int, F: int, n: int, k: int, density: float, seed: int,
                  device, dtype=torch.bfloat16, native_layers: int = 2, w_std: float = 0.02) -> MoEStack:

@@ -60,3 +60,23 @@ def test_random_stack_runs_and_is_deterministic():
     torch.cuda.synchronize()
     assert torch.equal(a, b) and torch.isfinite(a.float()).all()
     assert cfg.k == 8
+
+
+@pytest.mark.parametrize("L", [1, 3])
+def test_stack_graph_replays_bit_identical(L):
+    """The stack's decode step as one HIP graph (MoEStack.capture): each replay, from the same
+    hidden states and with eager work and synchronisations between replays, must give the bits of
+    the eager step; the graph holds kernel nodes only (no memsets)."""
+    st = random_stack(L, 32, 512, 256, 64, 8, 0.2, seed=5, device=DEV)
+    x0 = (torch.randn((32, 512), generator=torch.Generator().manual_seed(1)) * 1.0).to(torch.bfloat16).to(DEV)
+    h = x0.clone()
+    eager = st.forward(h).clone()
+    torch.cuda.synchronize()
+    assert torch.isfinite(eager.float()).all() and not torch.equal(eager, x0)
+    graph = st.capture(h)
+    for i in range(3):
+        h.copy_(x0)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(h, eager), f"replay {i}"
+        float((torch.randn((1 << 16,), device=DEV) * 3).sum().item())   # other work, a sync
