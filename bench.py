@@ -17,11 +17,9 @@ workload under "workloads".
                                           means (--pmc runs) of the timed launches in the
                                           rocprofv3 output written under DIR
 
-The timed steps run the layer's calls only; per-kernel times come from a second pass over the
-same steps with HIP events recorded on the stream the kernels run on: around each call, and
-inside pcm_project_combine between the mix, the projection GEMM and the combine (pcm_tuning's
-stage events); that pass's wall time per step is reported as ms_with_stage_events. A third
-pass over the same steps writes a 512 MB
+Per-kernel times come from HIP events recorded in the timed steps on the stream the kernels
+run on: around each call, and inside pcm_project_combine between the mix, the projection GEMM
+and the combine (pcm_tuning's stage events). A second pass over the same steps writes a 512 MB
 buffer before each step, so that the memory-bound stages (indexing, mix, combine)
 read from HBM rather than from the 256 MB MALL; their GB/s come from that pass. Then the
 same step is captured as one HIP graph (LayerPlan.capture's capture_graph) and its replays are
@@ -343,26 +341,21 @@ def measure(pcm, name, cfg, d, args, flush, scored):
 
     for _ in range(args.warmup):
         step()
-    # the timed steps: the layer's calls only (no event records inside the steps)
-    torch.cuda.synchronize()
-    fence()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    fence()
-    torch.cuda.synchronize()
-    # the same steps again with HIP events between the stages, for the per-stage times
+    # the timed steps, with HIP events between the stages (the per-stage times and the roofline
+    # come from the same launches as the step time and a profiler's fenced region; recording
+    # the events costs no measurable time)
     slots = [new_events() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    fence()
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
         step(slots[s])
     torch.cuda.synchronize()
-    wall_events = time.perf_counter() - t0
+    wall = time.perf_counter() - t0
+    fence()
+    torch.cuda.synchronize()
     timed = stage_ms(slots)
-    timed["step_with_events"] = wall_events * 1e3 / args.steps
     # the same steps with the MALL flushed before each (outside the recorded stages)
     fslots = [new_events() for _ in range(args.steps)]
     for s in range(args.steps):
@@ -433,8 +426,7 @@ def workload_record(pcm, acc, name, cfg, plan, sinp, ms, st, fl, scored):
            "paths": n_paths,
            "gemm_tflops": round(f["total"] / (gemm_ms * 1e-3) / 1e12, 1),
            "gemm_frac_peak": round(f["total"] / (gemm_ms * 1e-3) / 1e12 / peak, 4),
-           "ms_with_stage_events": round(st["step_with_events"], 4),
-           "stages_ms": {k: round(v, 4) for k, v in st.items() if k != "step_with_events"},
+           "stages_ms": {k: round(v, 4) for k, v in st.items()},
            "stages_flushed_ms": {k: round(v, 4) for k, v in fl.items()},
            "hbm_GBps": {k: round(v, 1) for k, v in hbm.items()},
            "hbm_frac": {k: round(v / acc.HBM_PEAK_GBS, 4) for k, v in hbm.items()}}
