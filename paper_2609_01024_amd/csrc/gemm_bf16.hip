@@ -15,7 +15,9 @@
 //
 // Three kernel shapes share the epilogue and the work decomposition:
 //  * "interleaved" (large tiles, 256 x 256): four waves, one per SIMD, each owning a 128 x 128
-//    block of C in 256 accumulation registers. Global -> LDS direct buffer loads
+//    block of C in 256 accumulation registers, or eight waves, two per SIMD, each owning a
+//    128 x 64 block in 128 (the expansion's default: while one wave of a SIMD waits, the other
+//    can issue MFMAs; same loads, same bits). Global -> LDS direct buffer loads
 //    (buffer_load_dwordx4 ... lds, no register staging: one 32-bit offset per lane for the
 //    whole tile, the stage's K offset in a scalar register) of 64-wide K stages, two stages
 //    of A and three of B (the weights, mostly fetched from HBM, get two stages of latency
