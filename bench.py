@@ -367,7 +367,12 @@ def measure(pcm, name, cfg, d, args, flush, scored):
     # eager steps; kept beside the eager figure, which stays the headline
     graph_ms = None
     if not args.no_graph:
-        graph = binding.capture_graph(lambda: step(None))
+        try:
+            graph = binding.capture_graph(lambda: step(None))
+        except RuntimeError as err:   # an optional figure: the line is written without it
+            print(f"[bench] {name}: no graph timing ({err})", file=sys.stderr, flush=True)
+            torch.cuda.synchronize()
+            return plan, sinp, wall * 1e3 / args.steps, timed, flushed, None
         for _ in range(args.warmup):
             graph.replay()
         torch.cuda.synchronize()
