@@ -383,6 +383,35 @@ def test_large_tile_work_orders_bit_identical(name):
                 f"{name}: tile {tile} order {order} window {window} changed the output"
 
 
+@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "decode_s", "wide_s"])
+def test_tile_families_bit_identical(name):
+    """Where the projection does not split K, every tile family (streaming, medium, large tiles
+    on four and on eight waves) accumulates each output over K in the same order, so the layer
+    output is the same bits under each, the default choice included."""
+    cfg = SMALL[name]
+    inp = make_inputs(cfg, seed=25)
+    d = dev(inp)
+    for tile in ("L", "W"):
+        assert pcm.project_workspace_layout(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, pcm.PCM_BF16,
+                                            pcm.Tuning(tile=tile))["ksplit"] == 1, tile
+    plan = pcm.LayerPlan(cfg.T, cfg.H, cfg.F, cfg.n, cfg.k, torch.bfloat16, DEV, cfg.shared_F)
+
+    def run(tuning):
+        poison(plan)
+        y = plan.forward(d["x"], d["logits"], d["mask"], d["w_gate"], d["w_up"], d["w_down"],
+                         d.get("shared"), tuning=tuning)
+        torch.cuda.synchronize()
+        return y.cpu().numpy()
+
+    base = run(None)
+    assert np.isfinite(base).all()
+    assert_y_close(base, oracle.layer_inputs(inp), cfg.dtype, f"{name}/default")
+    for tile in ("S", "M", "L", "W"):
+        say(f"tile family {tile} on {name}")
+        y = run(pcm.Tuning(tile=tile))
+        assert np.array_equal(y.view(np.uint32), base.view(np.uint32)), f"{name}: tile {tile}"
+
+
 @pytest.mark.parametrize("name", ["decode_s", "olmoe_s", "fine_s"])
 def test_stream_kernels_bit_identical(name):
     """The streaming GEMMs of few-row groups: the LDS-ring kernel (whole-line weight loads) at
