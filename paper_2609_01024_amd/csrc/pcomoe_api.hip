@@ -154,7 +154,7 @@ PathWs path_ws(int64_t T, int H, int F, int n, int k, pcm_dtype dt) {
 
 extern "C" {
 
-int pcm_abi_version(void) { return 122; }
+int pcm_abi_version(void) { return 123; }
 
 const char* pcm_status_string(pcm_status s) {
     switch (s) {

@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert L.pcm_abi_version() == 122
+    assert L.pcm_abi_version() == 123
     for s in (OK, ARG, UNSUP, WS, HIP):
         assert L.pcm_status_string(s).decode().startswith("PCM_")
     assert L.pcm_status_string(77) == b"unknown pcm_status"
