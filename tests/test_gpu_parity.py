@@ -199,6 +199,10 @@ SMALL = {
     # 16 N tiles per group in the expansion: the expert-major order deals each group's windows
     # over the 8 XCDs (window-interleaved), with one to four 256-row tiles per expert
     "wide_s": scaled(CONFIGS["mixtral"], T=1500, H=256, F=2048, name="wide_s"),
+    # 24 N tiles per group, three per XCD: windows of one or three N tiles, and experts whose
+    # last row block takes the tail tile (run after the full row blocks' windows) next to
+    # experts with only a tail row block
+    "wide3_s": scaled(CONFIGS["mixtral"], T=1200, H=192, F=3072, name="wide3_s"),
 }
 
 
@@ -266,7 +270,7 @@ def test_expand_rows_against_oracle():
     assert np.all(np.abs(got - ref) <= 1e-5 * np.abs(ref) + 1e-5 * scale)
 
 
-@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "decode_s", "wide_s"])
+@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "decode_s", "wide_s", "wide3_s"])
 def test_expand_output_bits_across_kernels(name):
     """Every expansion kernel (streaming at each ring depth and the register ring, medium
     tiles, large tiles in every work order) writes the same U bits: the same MFMA products in
@@ -353,7 +357,7 @@ def test_dense_swiglu_large_tile_tails(T, tile):
     assert_y_close(y.cpu().numpy(), ref, cfg.dtype, f"dense T={T}")
 
 
-@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "splitk_s", "wide_s"])
+@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "splitk_s", "wide_s", "wide3_s"])
 def test_large_tile_work_orders_bit_identical(name):
     """The work order of the large tiles (grouped, longest first, expert-major with several
     windows) decides only which workgroup computes which tile: the layer output must be the
@@ -383,7 +387,7 @@ def test_large_tile_work_orders_bit_identical(name):
                 f"{name}: tile {tile} order {order} window {window} changed the output"
 
 
-@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "decode_s", "wide_s"])
+@pytest.mark.parametrize("name", ["mixtral_s", "olmoe_s", "fine_s", "decode_s", "wide_s", "wide3_s"])
 def test_tile_families_bit_identical(name):
     """Where the projection does not split K, every tile family (streaming, medium, large tiles
     on four and on eight waves) accumulates each output over K in the same order, so the layer
