@@ -16,6 +16,9 @@ workload under "workloads".
   python bench.py --trace-summary DIR     per-kernel durations (kernel traces) or counter
                                           means (--pmc runs) of the timed launches in the
                                           rocprofv3 output written under DIR
+  python bench.py --vendor-compare [--config NAME]
+                                          the two grouped GEMMs under uniform routing beside
+                                          torch.bmm (the vendor library) of the same shapes
 
 Per-kernel times come from HIP events recorded in the timed steps on the stream the kernels
 run on: around each call, and inside pcm_project_combine between the mix, the projection GEMM
@@ -82,6 +85,10 @@ def parse():
                          "with and without source reuse, and the vanilla top-k layer)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--vendor-compare", action="store_true",
+                    help="only time the workload's two grouped GEMMs under uniform routing (every "
+                         "expert T*k/n rows) beside the vendor library's batched GEMM (torch.bmm) "
+                         "of the same shapes, alternating per iteration; one JSON line")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer 5 times (calibrates HBM byte counters)")
     ap.add_argument("--trace-summary", default=None, metavar="DIR",
@@ -158,6 +165,74 @@ def trace_summary(path: str):
                               f"{gui / max(ns, 1):.2f}" if ns >= 50e3 else "—"]
                 print(f"| `{_short(name)}` | {len(vs)} | {ns / 1e3:.1f} | " + " | ".join(cells) + " |")
             print()
+
+
+def vendor_compare(args):
+    """The workload's expansion and projection GEMMs with uniform routing (token t takes experts
+    (t + j) mod n, j < k, so that every expert has T*k/n rows: the case a batched GEMM handles)
+    against torch.bmm over n experts of the same shapes: bf16 for the expansion (the plain
+    products, without the gather, SwiGLU and float32 U), bf16 and float16 for the projection
+    (operands contiguous). Iterations alternate between the kernels; medians are reported."""
+    import torch
+    import paper_2609_01024_amd as pcm
+    from workloads import CONFIGS, HEADLINE
+    name = args.config or HEADLINE
+    cfg = CONFIGS[name]
+    T, H, F, n, k = cfg.T, cfg.H, cfg.F, cfg.n, cfg.k
+    if cfg.dtype != "bf16" or T % n or (T * k) % n:
+        sys.exit(f"--vendor-compare needs a bf16 workload with T and T*k multiples of n ({name})")
+    dev, rows = "cuda:0", T * k // n
+    d = device_inputs(cfg, args.seed, host_weights=False)
+    widen_down_weights(pcm, d)
+    g = torch.Generator(device=dev).manual_seed(args.seed * 1000 + 29)
+    logits = torch.empty((T, n), dtype=torch.float32, device=dev).uniform_(0.0, 0.5, generator=g)
+    t = torch.arange(T, device=dev)
+    for j in range(k):
+        logits[t, (t + j) % n] = 10.0 - j
+    plan = pcm.LayerPlan(T, H, F, n, k, torch.bfloat16, dev)
+    plan.index(logits, pcm.pcm_mask_pack(d["mask"]))
+    counts = torch.diff(plan.paths.expert_offsets).tolist()
+    assert counts == [rows] * n, counts
+    a_e = torch.empty((n, rows, H), device=dev).normal_(0.0, 1.0, generator=g).to(torch.bfloat16)
+    b_e = torch.empty((n, H, 2 * F), device=dev).normal_(0.0, cfg.w_std, generator=g).to(torch.bfloat16)
+    a_p = torch.empty((n, rows, F), device=dev).normal_(0.0, 1.0, generator=g).to(torch.bfloat16)
+    b_p = torch.empty((n, F, H), device=dev).normal_(0.0, cfg.w_std, generator=g).to(torch.bfloat16)
+    bmm = {"bmm_expand_bf16": (a_e, b_e), "bmm_project_bf16": (a_p, b_p),
+           "bmm_project_f16": (a_p.to(torch.float16), b_p.to(torch.float16))}
+    runs = {"ours_expand": [], "ours_project": [], **{key: [] for key in bmm}}
+    for it in range(args.warmup + args.steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        inner = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        for e in inner:
+            e.record()
+        ev[0].record()
+        pcm.pcm_expand(d["x"], d["wg"], d["wu"], plan.paths, u=plan.u)
+        ev[1].record()
+        pcm.pcm_project_combine(plan.u, d["wd"], plan.paths, y=plan.y, ws=plan.ws_proj,
+                                tuning=pcm.Tuning(stage_events=inner))
+        times = {}
+        for key, (a, b) in bmm.items():
+            e2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            e2[0].record()
+            torch.bmm(a, b)
+            e2[1].record()
+            times[key] = e2
+        torch.cuda.synchronize()
+        if it >= args.warmup:
+            runs["ours_expand"].append(ev[0].elapsed_time(ev[1]))
+            runs["ours_project"].append(inner[1].elapsed_time(inner[2]))
+            for key, e2 in times.items():
+                runs[key].append(e2[0].elapsed_time(e2[1]))
+    flops = {"expand": 4.0 * T * k * H * F, "project": 2.0 * T * k * H * F}
+    out = {}
+    for key, v in runs.items():
+        ms = float(np.median(v))
+        f = flops["expand" if "expand" in key else "project"]
+        out[key] = {"us": round(ms * 1e3, 1), "TFLOP/s": round(f / (ms * 1e-3) / 1e12, 1),
+                    "frac_bf16_peak": round(f / (ms * 1e-3) / 2.5e15, 4)}
+    print(json.dumps({"vendor_compare": out, "config": {
+        "workload": f"{name}: T={T} H={H} n={n} F={F} k={k}, uniform routing ({rows} rows per expert)",
+        "steps": args.steps, "warmup": args.warmup}}), flush=True)
 
 
 def copy_probe(mib: int):
@@ -609,6 +684,9 @@ def main():
         sys.exit(2)
     if args.stack:
         stack_bench(args)
+        return
+    if args.vendor_compare:
+        vendor_compare(args)
         return
 
     import torch
